@@ -1,0 +1,183 @@
+"""Benchmark of one layer's QCFuse fusion step on one MI355X.
+
+A step is the whole hot path over one batch: re-positioning, query-row
+rotation, anchor gather, anchor probe attention, critical-layer scores,
+per-chunk top-k, scatter of the recomputed rows and their causal attention.
+The workload is the Llama-3-8B-shaped layer (10 chunks x 512 tokens + a
+64-token query, H_q=32, H_kv=8, d=128, bf16, rho=30%), seeded synthetic data.
+Inputs are resident in HBM before the timed region; several buffer sets are
+rotated so the 256 MB last-level cache does not hold the previous step's data.
+
+Prints one JSON line:  metric = selected-token fused-prefill tokens/s per layer
+(|R| recomputed rows / step time), with the attention kernel's roofline
+fraction (algorithmic FLOPs per launch / its average HIP-event duration) and
+the CPU oracle's throughput on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def attn_flops(step, R_pos):
+    """Algorithmic FLOPs of the causal row attention: 4*H_q*d*sum(pos+1) over recomputed rows."""
+    w = step.w
+    return 4.0 * w.n_q_heads * w.head_dim * float(np.sum(R_pos.astype(np.float64) + 1.0))
+
+
+def probe_attn_flops(step):
+    w, p = step.w, step.plan
+    tot = 0.0
+    for b in range(w.batch):
+        na = int(p.cu_probe[b + 1] - p.cu_probe[b]) - int(w.q_lens[b])
+        nq = int(w.q_lens[b])
+        tot += sum(na + i + 1 for i in range(nq))
+    return 4.0 * w.n_q_heads * w.head_dim * tot
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c2", help="workload (c2 is the measured one)")
+    ap.add_argument("--sets", type=int, default=0, help="buffer sets rotated (0: enough for 512 MB)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the step shards by request or KV-head group; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_05875_amd.step import FusionStep
+    from paper_2606_05875_amd.workloads import make_workload
+
+    torch.cuda.set_device(0)
+    w = make_workload(args.config)
+    first = FusionStep(w)
+    per_set = sum(t.numel() * t.element_size() for t in (first.k_pic, first.v_pic, first.q_new,
+                                                         first.k_new, first.v_new, first.k, first.v))
+    n_sets = args.sets or max(1, math.ceil(512e6 / per_set))
+    steps = [first] + [FusionStep(w) for _ in range(n_sets - 1)]
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        steps[i % n_sets].run()
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(args.steps):
+        s = steps[i % n_sets]
+        s.stage_rerope()
+        s.stage_query_rows()
+        s.stage_anchor_gather()
+        s.stage_probe_attn()
+        s.stage_scores()
+        s.stage_select()
+        s.stage_scatter()
+        ev[i][0].record()
+        s.stage_attn()
+        ev[i][1].record()
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    R_pos = first.R_pos.cpu().numpy()
+    n_R = int(R_pos.size)
+    flops = attn_flops(first, R_pos)
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+
+    # per-stage breakdown (separate, untimed for the headline): events around each stage
+    stage_ms = {}
+    for name in FusionStep.STAGES:
+        fn = getattr(first, "stage_" + name)
+        reps = 20
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for i in range(reps):
+            getattr(steps[i % n_sets], "stage_" + name)()
+        b.record()
+        torch.cuda.synchronize()
+        stage_ms[name] = a.elapsed_time(b) / reps
+    n_ctx = int(w.seg_len.sum())
+    elem = 2 if w.dtype == "bf16" else 4
+    rerope_bytes = 2.0 * n_ctx * w.n_kv_heads * w.head_dim * elem
+    rerope_gbs = rerope_bytes / (stage_ms["rerope"] * 1e-3) / 1e9
+
+    out = {
+        "metric": "selected-token fused-prefill tokens/s per layer",
+        "value": n_R / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded; shapes of the paper's 512-token-chunk RAG requests)",
+        "config": {"workload": f"{args.config}: {w.meta['desc']}", "recomputed_rows": n_R,
+                   "rho_bp": w.rho_bp, "tokens": w.n_rows, "buffer_sets": n_sets},
+        "roofline": {"kernel": "attn_bf16_kernel (qcf_sparse_prefill_attn, recomputed rows)",
+                     "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flops_per_launch": flops, "avg_launch_ms": attn_ms},
+        "stage_ms": stage_ms,
+        "rerope_GBs": rerope_gbs,
+        "rerope_hbm_frac": rerope_gbs / PEAK_HBM_GBS,
+    }
+
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, budget_s):
+    """The oracle's step on the host cores: whole steps of the same workload until ~budget_s."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    n_R = None
+    times = []
+    t0 = time.perf_counter()
+    while True:
+        t = time.perf_counter()
+        r = oracle.fusion_step(w, band_attention=False)
+        times.append(time.perf_counter() - t)
+        n_R = sum(x.size for x in r["R"])
+        if time.perf_counter() - t0 > budget_s or len(times) >= 5:
+            break
+    sec = float(np.median(times))
+    return {"value": n_R / sec, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(times)} whole oracle steps of the same workload ({sec:.2f} s each, median)",
+            "host_cpus": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+
+
+if __name__ == "__main__":
+    main()

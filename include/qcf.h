@@ -1,0 +1,193 @@
+/*
+ * qcf.h -- C ABI of libqcf: one transformer layer of the QCFuse cache-fusion
+ * step (arXiv 2606.05875) as hand-written HIP kernels for gfx950 (MI355X).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every tensor argument is a DEVICE pointer owned by the caller.  The
+ *    library allocates nothing, keeps no pointer after the call returns and
+ *    launches its kernels on the caller's stream in stream order (no implicit
+ *    synchronisation).  Buffers must stay alive until the stream has passed
+ *    the work.  Calls are reentrant; two calls that write the same buffer on
+ *    different streams race.
+ *  - Tensors are token-major: a K/V cache row holds n_kv_heads * head_dim
+ *    elements (head-major inside the row); consecutive rows are `row_stride`
+ *    elements apart (row_stride >= n_kv_heads * head_dim).  Query and output
+ *    tensors are dense ([rows, n_q_heads, head_dim]).  Base pointers are 16-byte
+ *    aligned; row strides are multiples of 16 bytes.
+ *  - Index and position arrays are int32 device arrays; sizes fit int32.
+ *  - dtype is QCF_F32 or QCF_BF16 (storage type of every floating tensor of the
+ *    call, except score vectors, which are always float32); arithmetic is
+ *    float32 (bf16 products on the matrix cores accumulate in float32); rotary
+ *    angles are formed in float64.
+ *  - head_dim is 64 or 128; n_q_heads is a multiple of n_kv_heads and the
+ *    group size n_q_heads / n_kv_heads is a power of two no larger than 32
+ *    (grouped-query attention: query head h reads KV head h / group).
+ *  - Host-visible arguments are validated before anything is launched; a bad
+ *    argument returns an error code and launches nothing.  The CONTENTS of
+ *    device index arrays are preconditions: the kernels skip any index that
+ *    falls outside the tensor bounds given in the call instead of touching
+ *    memory out of bounds, but such input gives unspecified results.  A
+ *    launch failure returns QCF_ERR_HIP.  Asynchronous device faults surface
+ *    at the caller's next synchronisation.
+ *  - Rotary embedding: rotate-half pairs (j, j + head_dim/2) turn by angle
+ *    p * theta^(-2j/head_dim), no frequency scaling.
+ */
+#ifndef QCF_H_
+#define QCF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QCF_VERSION 100
+
+typedef enum {
+  QCF_OK = 0,
+  QCF_ERR_INVALID_ARG = 1, /* null pointer, bad size, misaligned pointer or stride */
+  QCF_ERR_UNSUPPORTED = 2, /* valid but not implemented (head_dim, group size, dtype) */
+  QCF_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the _workspace_size query */
+  QCF_ERR_HIP = 4          /* a HIP launch reported an error */
+} qcf_status;
+
+typedef enum { QCF_F32 = 0, QCF_BF16 = 1 } qcf_dtype;
+
+/* Library version (QCF_VERSION) and a static text for a status code. */
+int qcf_version(void);
+const char* qcf_status_string(qcf_status status);
+
+/*
+ * qcf_rerope -- position remapping Pi_i of the reused chunk keys
+ * (Section 2.1.2, eq. pic_online).  A stored chunk key is rotated at its
+ * chunk-local position; rotating it once more by the chunk's offset o_i moves
+ * it to its request position o_i + r.  Values need no remapping.
+ *
+ *   k_out, k_in  [n_tokens rows, row_stride] keys; k_out may equal k_in
+ *                (in place).  Rows outside every segment are not touched.
+ *   seg_start    [n_seg] first row of each segment (a chunk)
+ *   seg_len      [n_seg] rows in each segment (<= max_seg_len)
+ *   seg_delta    [n_seg] rotation offset of each segment in positions
+ *   rope_theta   rotary base
+ * Errors: null pointers, n_seg < 0, head_dim/group unsupported, misalignment.
+ */
+qcf_status qcf_rerope(void* k_out, const void* k_in, qcf_dtype dtype,
+                      int64_t n_tokens, int n_kv_heads, int head_dim, int64_t row_stride,
+                      int n_seg, const int32_t* seg_start, const int32_t* seg_len,
+                      const int32_t* seg_delta, int max_seg_len, double rope_theta,
+                      hipStream_t stream);
+
+/*
+ * qcf_gather_rows -- row copy dst[i] = src[idx[i]] (the anchor cache
+ * KV^A = KV^PIC[A], Section 3.3.2, eq. anchor_cache; also the compact
+ * fresh-row gather).
+ *   dst  [n_rows rows, dst_stride_bytes]; src [n_src_rows rows, src_stride_bytes]
+ *   idx  [n_rows] source rows; rows with idx outside [0, n_src_rows) are skipped
+ *   row_bytes  bytes copied per row (multiple of 16, <= both strides)
+ */
+qcf_status qcf_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
+                           int64_t n_src_rows, int64_t row_bytes, int64_t src_stride_bytes,
+                           int64_t dst_stride_bytes, hipStream_t stream);
+
+/*
+ * qcf_scatter_kv -- fused-cache update of eq. fuse_cache: recomputed rows
+ * replace their PIC entries (Section 2.1.3).  For each r < n_rows with
+ * s = src_idx ? src_idx[r] : r and p = row_pos[r]:
+ *     k_cache[row_idx[r]] = rope(k_new[s], p)
+ *     v_cache[row_idx[r]] = v_new[s]
+ *     q_out[r]            = rope(q_new[s], p)      (when q_out != NULL)
+ *   k_cache, v_cache  [n_cache_rows, cache_row_stride]
+ *   k_new, v_new      [n_src_rows, n_kv_heads * head_dim] dense
+ *   q_new             [n_src_rows, n_q_heads * head_dim] dense (may be NULL iff q_out is NULL)
+ *   q_out             [n_rows, n_q_heads * head_dim] dense, may alias q_new only when
+ *                     src_idx is NULL (in-place rotation)
+ * Duplicate row_idx values give unspecified results.
+ */
+qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
+                          int64_t cache_row_stride, const void* k_new, const void* v_new,
+                          const void* q_new, void* q_out, int64_t n_src_rows,
+                          const int32_t* src_idx, qcf_dtype dtype, int64_t n_rows,
+                          const int32_t* row_idx, const int32_t* row_pos, int n_q_heads,
+                          int n_kv_heads, int head_dim, double rope_theta, hipStream_t stream);
+
+/*
+ * qcf_probe_scores -- per-token importance of one critical layer,
+ * eq. single_layer_importance (Section 3.4.1); with accumulate != 0 the result
+ * is added to `scores`, which sums it over the critical layers
+ * (eq. critical_layer_importance).  For request b, context token t < ctx_len[b]:
+ *   scores[cu_kv[b] + t] (+)= sum_{i, h} softmax_t'( q[cu_q[b]+i, h] . k[cu_kv[b]+t', h/group]
+ *                                                  * softmax_scale )[t]
+ * The softmax runs over the request's ctx_len[b] context keys.  Score slots
+ * of other rows are not written.  The result is deterministic (fixed
+ * reduction order).
+ *   scores  float32 [n_kv_rows]
+ *   q       [n_q_rows, n_q_heads, head_dim] rotated user-query states
+ *   k       [n_kv_rows, k_row_stride] keys at their request positions
+ *   cu_q    [batch+1], cu_kv [batch+1], ctx_len [batch] device arrays;
+ *   max_q_len >= max_b(cu_q[b+1]-cu_q[b]), max_ctx_len >= max_b ctx_len[b]
+ *   workspace  >= qcf_probe_scores_workspace_size(...) bytes, 256-byte aligned
+ */
+size_t qcf_probe_scores_workspace_size(int batch, int max_q_len, int max_ctx_len,
+                                       int n_q_heads, int n_kv_heads, int head_dim);
+qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                            const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                            qcf_dtype dtype, int batch, const int32_t* cu_q,
+                            const int32_t* cu_kv, const int32_t* ctx_len, int max_q_len,
+                            int max_ctx_len, int n_q_heads, int n_kv_heads, int head_dim,
+                            float softmax_scale, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/*
+ * qcf_select_topk -- recomputation set of eq. critical_mask, taken per
+ * segment (per chunk).  For segment s the k = seg_k[s] rows of
+ * [seg_start[s], seg_start[s] + seg_len[s]) with the largest scores are
+ * chosen; equal scores go to the lower row, and -0 equals +0.  The chosen
+ * rows are written in ascending order to out_idx[out_start[s] .. + k); when
+ * out_pos is not NULL, out_pos gets row - pos_base[s] (the position inside
+ * the request).  Scores must be finite.  k > seg_len is clamped to seg_len.
+ *   scores   float32 [n_scores]
+ *   out_idx, out_pos  int32 [n_out]
+ *   max_seg_len >= every seg_len (chooses the LDS staging path)
+ */
+qcf_status qcf_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
+                           const float* scores, int64_t n_scores, int n_seg,
+                           const int32_t* seg_start, const int32_t* seg_len,
+                           const int32_t* seg_k, const int32_t* out_start,
+                           const int32_t* pos_base, int max_seg_len, hipStream_t stream);
+
+/*
+ * qcf_sparse_prefill_attn -- causal grouped-query attention of the selected
+ * rows over the fused cache (Section 2.1.3: a recomputed row at position p
+ * reads every prefix key j <= p, itself included); with an explicit kv_pos it
+ * is also the anchor-conditioned query probe over [anchor cache ; query]
+ * (Section 3.3.2, eq. anchor_query_state).  For request b, row r in
+ * [cu_rows[b], cu_rows[b+1]) and head h:
+ *   out[r, h] = sum_j softmax_j( q[r, h] . k[cu_kv[b]+j, h/group] * softmax_scale ) v[cu_kv[b]+j, h/group]
+ * over keys j < cu_kv[b+1]-cu_kv[b] with kpos(j) <= row_pos[r], where
+ * kpos(j) = kv_pos[cu_kv[b]+j] if kv_pos != NULL, else j.  A row that sees no
+ * key gets zeros (and lse = -inf).
+ *   out  [n_rows, n_q_heads, head_dim]; lse float32 [n_rows, n_q_heads] or NULL
+ *        (natural-log log-sum-exp of the scaled logits)
+ *   q    [n_rows, n_q_heads, head_dim]; row_pos int32 [n_rows]
+ *   k_cache, v_cache [n_kv_rows, kv_row_stride]
+ *   cu_rows [batch+1], cu_kv [batch+1]; max_rows / max_kv bound the per-request counts
+ *   workspace >= qcf_sparse_prefill_attn_workspace_size(...) bytes (may be 0)
+ */
+size_t qcf_sparse_prefill_attn_workspace_size(int batch, int max_rows, int max_kv,
+                                              int n_q_heads, int n_kv_heads, int head_dim,
+                                              qcf_dtype dtype);
+qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
+                                   int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
+                                   const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
+                                   const int32_t* cu_kv, const int32_t* kv_pos, qcf_dtype dtype,
+                                   int batch, int max_rows, int max_kv, int n_q_heads,
+                                   int n_kv_heads, int head_dim, float softmax_scale,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* QCF_H_ */

@@ -212,7 +212,7 @@ def select_per_chunk(scores_rows, seg_start, seg_len, rho_bp):
 # ---------------------------------------------------------------------------
 # one layer of the fusion step
 # ---------------------------------------------------------------------------
-def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3):
+def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True):
     """Run one layer's QCFuse fusion step on workload ``w`` (see the package's workloads).
 
     Steps, per request b:
@@ -231,7 +231,10 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3):
     R per request picked deterministically from the oracle's own R (for big
     configs).  Rows of the near-tie band (|I - I_kth| < band inside a chunk)
     that are not in P are also evaluated so that a swap of near-tied rows can
-    be checked.  Returns a dict of float64 arrays / int arrays.
+    be checked (``band_attention``; off for configs whose band is large).
+    ``fresh_k`` holds the rotated fresh key of EVERY row (what any row of the
+    fused cache holds if it is recomputed).  Returns a dict of float64 arrays /
+    int arrays.
     """
     dt = w.dtype
     d, hq, hkv = w.head_dim, w.n_q_heads, w.n_kv_heads
@@ -245,7 +248,7 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3):
     V = np.array(w.v_pic, np.float64, copy=True)
     scores = np.zeros(T, np.float64)
     res = dict(k_rerope=k_rerope, o_probe=[], q_u=[], P=[], R=[], R_pos=[], o={},
-               band_rows=[], fresh_k={}, fresh_v={}, q_fresh={})
+               band_rows=[], q_fresh={})
 
     # fresh, rotated tensors for any row (used for R and for the near-tie band)
     def fresh_row(rows, pos):
@@ -308,7 +311,7 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3):
         if attn_rows is not None and R.size > attn_rows:
             pick = np.unique(np.linspace(0, R.size - 1, attn_rows).round().astype(int))
             rows = R[pick]
-        extra = np.setdiff1d(band_rows, P)
+        extra = np.setdiff1d(band_rows, P) if band_attention else np.zeros(0, np.int64)
         rows_all = np.concatenate([rows, extra])
         pos_all = rows_all - base
         q_all, k_all, v_all = fresh_row(rows_all, pos_all)
@@ -331,10 +334,13 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3):
                 kt[:, :, j], vt[:, j] = keep_k, keep_v
                 res["o"][r] = round_storage(o_x, dt)
         for i, r in enumerate(rows_all):
-            res["fresh_k"][int(r)] = k_all[i]
-            res["fresh_v"][int(r)] = v_all[i]
             res["q_fresh"][int(r)] = q_all[i]
 
+    fresh_k = np.zeros_like(K)
+    for b in range(w.batch):
+        base, n = int(w.cu_kv[b]), int(w.cu_kv[b + 1] - w.cu_kv[b])
+        fresh_k[base:base + n] = round_storage(rope(w.k_new[base:base + n], np.arange(n), theta), dt)
+    res["fresh_k"] = fresh_k
     res["scores"] = scores
     res["k_fuse"] = K
     res["v_fuse"] = V

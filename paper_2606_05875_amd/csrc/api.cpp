@@ -1,0 +1,222 @@
+// C ABI of libqcf: host-side validation, then the kernel launchers.
+// Every check runs before any HIP call, so a rejected call touches no device
+// state (and works on a machine without a GPU).
+#include <stdint.h>
+
+#include "../../include/qcf.h"
+#include "qcf_launch.h"
+
+namespace {
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+inline bool dtype_ok(qcf_dtype t) { return t == QCF_F32 || t == QCF_BF16; }
+inline int64_t esize(qcf_dtype t) { return t == QCF_BF16 ? 2 : 4; }
+// a device tensor pointer: non-null and 16-byte aligned (null allowed when empty)
+inline bool tensor_ok(const void* p, bool empty) { return empty ? (p == nullptr || aligned16(p)) : (p && aligned16(p)); }
+inline bool index_ok(const void* p, bool empty) {
+  return empty || (p && (reinterpret_cast<uintptr_t>(p) & 3u) == 0);
+}
+
+qcf_status check_heads(int hq, int hkv, int d) {
+  if (hkv <= 0 || hq <= 0) return QCF_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return QCF_ERR_UNSUPPORTED;
+  if (hq % hkv != 0) return QCF_ERR_INVALID_ARG;
+  const int grp = hq / hkv;
+  if ((grp & (grp - 1)) != 0 || grp > 32) return QCF_ERR_UNSUPPORTED;
+  if (hq > 65535) return QCF_ERR_UNSUPPORTED;
+  return QCF_OK;
+}
+
+inline qcf_status hip_status(hipError_t e) { return e == hipSuccess ? QCF_OK : QCF_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int qcf_version(void) { return QCF_VERSION; }
+
+const char* qcf_status_string(qcf_status s) {
+  switch (s) {
+    case QCF_OK: return "ok";
+    case QCF_ERR_INVALID_ARG: return "invalid argument";
+    case QCF_ERR_UNSUPPORTED: return "unsupported configuration";
+    case QCF_ERR_WORKSPACE: return "workspace missing or too small";
+    case QCF_ERR_HIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+qcf_status qcf_rerope(void* k_out, const void* k_in, qcf_dtype dtype, int64_t n_tokens,
+                      int n_kv_heads, int head_dim, int64_t row_stride, int n_seg,
+                      const int32_t* seg_start, const int32_t* seg_len, const int32_t* seg_delta,
+                      int max_seg_len, double rope_theta, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
+  if (n_tokens < 0 || n_tokens > INT32_MAX || n_seg < 0 || max_seg_len < 0) return QCF_ERR_INVALID_ARG;
+  if (n_kv_heads <= 0) return QCF_ERR_INVALID_ARG;
+  if (head_dim != 64 && head_dim != 128) return QCF_ERR_UNSUPPORTED;
+  if (n_seg > 65535) return QCF_ERR_UNSUPPORTED;
+  if (row_stride < (int64_t)n_kv_heads * head_dim || (row_stride * esize(dtype)) % 16 != 0)
+    return QCF_ERR_INVALID_ARG;
+  if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
+  const bool empty = n_tokens == 0 || n_seg == 0 || max_seg_len == 0;
+  if (!tensor_ok(k_out, empty) || !tensor_ok(k_in, empty)) return QCF_ERR_INVALID_ARG;
+  if (!index_ok(seg_start, n_seg == 0) || !index_ok(seg_len, n_seg == 0) ||
+      !index_ok(seg_delta, n_seg == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (empty) return QCF_OK;
+  return hip_status(qcf::launch_rerope(k_out, k_in, dtype == QCF_BF16, n_tokens, n_kv_heads,
+                                       head_dim, row_stride, n_seg, seg_start, seg_len, seg_delta,
+                                       max_seg_len, rope_theta, stream));
+}
+
+qcf_status qcf_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
+                           int64_t n_src_rows, int64_t row_bytes, int64_t src_stride_bytes,
+                           int64_t dst_stride_bytes, hipStream_t stream) {
+  if (n_rows < 0 || n_src_rows < 0 || row_bytes < 0 || n_rows > INT32_MAX) return QCF_ERR_INVALID_ARG;
+  if (row_bytes % 16 != 0 || src_stride_bytes % 16 != 0 || dst_stride_bytes % 16 != 0)
+    return QCF_ERR_INVALID_ARG;
+  if (row_bytes > src_stride_bytes || row_bytes > dst_stride_bytes) return QCF_ERR_INVALID_ARG;
+  const bool empty = n_rows == 0 || row_bytes == 0;
+  if (!tensor_ok(dst, empty) || !tensor_ok(src, empty || n_src_rows == 0) || !index_ok(idx, empty))
+    return QCF_ERR_INVALID_ARG;
+  if (empty) return QCF_OK;
+  return hip_status(qcf::launch_gather_rows(dst, src, idx, n_rows, n_src_rows, row_bytes,
+                                            src_stride_bytes, dst_stride_bytes, stream));
+}
+
+qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
+                          int64_t cache_row_stride, const void* k_new, const void* v_new,
+                          const void* q_new, void* q_out, int64_t n_src_rows,
+                          const int32_t* src_idx, qcf_dtype dtype, int64_t n_rows,
+                          const int32_t* row_idx, const int32_t* row_pos, int n_q_heads,
+                          int n_kv_heads, int head_dim, double rope_theta, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
+  qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != QCF_OK) return st;
+  if (n_rows < 0 || n_rows > INT32_MAX || n_cache_rows < 0 || n_src_rows < 0) return QCF_ERR_INVALID_ARG;
+  if (cache_row_stride < (int64_t)n_kv_heads * head_dim || (cache_row_stride * esize(dtype)) % 16 != 0)
+    return QCF_ERR_INVALID_ARG;
+  if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
+  if (q_out && !q_new) return QCF_ERR_INVALID_ARG;
+  if (q_out && src_idx && q_out == q_new) return QCF_ERR_INVALID_ARG;
+  const bool empty = n_rows == 0;
+  if (!tensor_ok(k_cache, empty) || !tensor_ok(v_cache, empty) || !tensor_ok(k_new, empty) ||
+      !tensor_ok(v_new, empty))
+    return QCF_ERR_INVALID_ARG;
+  if (q_out && (!aligned16(q_out) || !aligned16(q_new))) return QCF_ERR_INVALID_ARG;
+  if (!index_ok(row_idx, empty) || !index_ok(row_pos, empty) || (src_idx && !index_ok(src_idx, false)))
+    return QCF_ERR_INVALID_ARG;
+  if (empty) return QCF_OK;
+  return hip_status(qcf::launch_scatter_kv(k_cache, v_cache, n_cache_rows, cache_row_stride, k_new,
+                                           v_new, q_new, q_out, n_src_rows, src_idx,
+                                           dtype == QCF_BF16, n_rows, row_idx, row_pos, n_q_heads,
+                                           n_kv_heads, head_dim, rope_theta, stream));
+}
+
+size_t qcf_probe_scores_workspace_size(int batch, int max_q_len, int max_ctx_len, int n_q_heads,
+                                       int n_kv_heads, int head_dim) {
+  if (batch < 0 || max_q_len < 0 || max_ctx_len < 0) return 0;
+  if (check_heads(n_q_heads, n_kv_heads, head_dim) != QCF_OK) return 0;
+  qcf::ProbeShape s{batch, max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim};
+  return qcf::probe_scores_workspace(s);
+}
+
+qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                            const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                            qcf_dtype dtype, int batch, const int32_t* cu_q, const int32_t* cu_kv,
+                            const int32_t* ctx_len, int max_q_len, int max_ctx_len, int n_q_heads,
+                            int n_kv_heads, int head_dim, float softmax_scale, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
+  qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != QCF_OK) return st;
+  if (batch < 0 || batch > 65535 || max_q_len < 0 || max_ctx_len < 0) return QCF_ERR_INVALID_ARG;
+  if (n_q_rows < 0 || n_kv_rows < 0 || n_q_rows > INT32_MAX || n_kv_rows > INT32_MAX)
+    return QCF_ERR_INVALID_ARG;
+  if (k_row_stride < (int64_t)n_kv_heads * head_dim || (k_row_stride * esize(dtype)) % 16 != 0)
+    return QCF_ERR_INVALID_ARG;
+  if (!(softmax_scale > 0.f)) return QCF_ERR_INVALID_ARG;
+  const bool empty = batch == 0 || max_ctx_len == 0;
+  if (!index_ok(scores, empty) || !tensor_ok(q, empty || n_q_rows == 0) ||
+      !tensor_ok(k, empty || n_kv_rows == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (!index_ok(cu_q, batch == 0) || !index_ok(cu_kv, batch == 0) || !index_ok(ctx_len, batch == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (empty) return QCF_OK;
+  const size_t need = qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, n_q_heads,
+                                                      n_kv_heads, head_dim);
+  if (workspace_bytes < need || (need > 0 && (!workspace || !aligned256(workspace))))
+    return QCF_ERR_WORKSPACE;
+  qcf::ProbeShape s{batch, max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim};
+  return hip_status(qcf::launch_probe_scores(scores, accumulate, q, n_q_rows, k, n_kv_rows,
+                                             k_row_stride, dtype == QCF_BF16, cu_q, cu_kv, ctx_len,
+                                             s, softmax_scale, workspace, stream));
+}
+
+qcf_status qcf_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out, const float* scores,
+                           int64_t n_scores, int n_seg, const int32_t* seg_start,
+                           const int32_t* seg_len, const int32_t* seg_k, const int32_t* out_start,
+                           const int32_t* pos_base, int max_seg_len, hipStream_t stream) {
+  if (n_out < 0 || n_scores < 0 || n_seg < 0 || max_seg_len < 0) return QCF_ERR_INVALID_ARG;
+  if (n_out > INT32_MAX || n_scores > INT32_MAX) return QCF_ERR_INVALID_ARG;
+  if (n_seg > INT32_MAX / 2) return QCF_ERR_UNSUPPORTED;
+  const bool empty = n_seg == 0 || max_seg_len == 0;
+  if (!index_ok(out_idx, empty || n_out == 0) || !index_ok(scores, empty || n_scores == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (out_pos && !index_ok(out_pos, false)) return QCF_ERR_INVALID_ARG;
+  if (!index_ok(seg_start, n_seg == 0) || !index_ok(seg_len, n_seg == 0) ||
+      !index_ok(seg_k, n_seg == 0) || !index_ok(out_start, n_seg == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (pos_base && !index_ok(pos_base, false)) return QCF_ERR_INVALID_ARG;
+  if (empty) return QCF_OK;
+  return hip_status(qcf::launch_select_topk(out_idx, out_pos, n_out, scores, n_scores, n_seg,
+                                            seg_start, seg_len, seg_k, out_start, pos_base,
+                                            max_seg_len, stream));
+}
+
+size_t qcf_sparse_prefill_attn_workspace_size(int batch, int max_rows, int max_kv, int n_q_heads,
+                                              int n_kv_heads, int head_dim, qcf_dtype dtype) {
+  if (batch < 0 || max_rows < 0 || max_kv < 0 || !dtype_ok(dtype)) return 0;
+  if (check_heads(n_q_heads, n_kv_heads, head_dim) != QCF_OK) return 0;
+  qcf::AttnShape s{batch, max_rows, max_kv, n_q_heads, n_kv_heads, head_dim};
+  return qcf::attn_workspace(s, dtype == QCF_BF16);
+}
+
+qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
+                                   int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
+                                   const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
+                                   const int32_t* cu_kv, const int32_t* kv_pos, qcf_dtype dtype,
+                                   int batch, int max_rows, int max_kv, int n_q_heads,
+                                   int n_kv_heads, int head_dim, float softmax_scale,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
+  qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != QCF_OK) return st;
+  if (n_rows < 0 || n_rows > INT32_MAX || n_kv_rows < 0 || n_kv_rows > INT32_MAX)
+    return QCF_ERR_INVALID_ARG;
+  if (batch < 0 || batch > 65535 || max_rows < 0 || max_kv < 0) return QCF_ERR_INVALID_ARG;
+  if (kv_row_stride < (int64_t)n_kv_heads * head_dim || (kv_row_stride * esize(dtype)) % 16 != 0)
+    return QCF_ERR_INVALID_ARG;
+  if (!(softmax_scale > 0.f)) return QCF_ERR_INVALID_ARG;
+  const bool empty = n_rows == 0 || batch == 0 || max_rows == 0;
+  if (!tensor_ok(out, empty) || !tensor_ok(q, empty) || !index_ok(row_pos, empty) ||
+      !index_ok(cu_rows, batch == 0) || !index_ok(cu_kv, batch == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (!tensor_ok(k_cache, empty || n_kv_rows == 0) || !tensor_ok(v_cache, empty || n_kv_rows == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (lse && !index_ok(lse, false)) return QCF_ERR_INVALID_ARG;
+  if (kv_pos && !index_ok(kv_pos, false)) return QCF_ERR_INVALID_ARG;
+  if (empty) return QCF_OK;
+  if (dtype == QCF_F32 && n_rows > 0x7fffffff) return QCF_ERR_UNSUPPORTED;
+  const size_t need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, n_q_heads,
+                                                             n_kv_heads, head_dim, dtype);
+  if (workspace_bytes < need || (need > 0 && (!workspace || !aligned256(workspace))))
+    return QCF_ERR_WORKSPACE;
+  qcf::AttnShape s{batch, max_rows, max_kv, n_q_heads, n_kv_heads, head_dim};
+  return hip_status(qcf::launch_sparse_attn(out, lse, q, row_pos, n_rows, cu_rows, k_cache, v_cache,
+                                            n_kv_rows, kv_row_stride, cu_kv, kv_pos,
+                                            dtype == QCF_BF16, s, softmax_scale, workspace, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,325 @@
+// Causal grouped-query attention of the recomputed rows over the fused cache
+// (Section 2.1.3: a recomputed row at position p reads every prefix key j <= p,
+// itself included) and, with explicit key positions, the anchor-conditioned
+// query probe (Section 3.3.2, eq. anchor_query_state).
+//
+// bf16 path (matrix cores, flash-style, one pass over the keys):
+//  * a block owns 128 query vectors of one KV head: 128/G consecutive rows of
+//    the request times the G query heads that share the KV head (GQA
+//    packing), 32 vectors per wave;
+//  * the keys 0 .. max(row position in the block) stream through LDS in
+//    64-key tiles (K row-major, V transposed with a key order that matches the
+//    P operand), with the next tile prefetched into registers;
+//  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (Q stays in registers as the B
+//    operand), so each lane holds 16 logits of ONE query vector: row max,
+//    rescale and row sum stay in the lane plus one exchange with lane ^ 32;
+//  * O^T += V^T P^T on the same instruction: P^T comes straight from the
+//    logit registers (rounded to bf16), V^T from LDS;
+//  * online softmax in float32 (base-2 exponentials); the per-row causal
+//    limit masks only tiles that reach past the wave's smallest position, and
+//    waves skip tiles past their largest position.
+// fp32 path (vector ALUs): one wave per (row, head).
+#include <limits.h>
+#include <math.h>
+
+#include "qcf_device.h"
+#include "qcf_launch.h"
+
+namespace qcf {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kKT = 64;  // keys per tile
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
+
+// position inside a 16-key group of the transposed V tile: bits 2 and 3 swap,
+// so lane half h of the P operand (keys {0-3, 8-11} or {4-7, 12-15}) reads one
+// contiguous 16-byte run
+__device__ __forceinline__ int vt_slot(int key) {
+  return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
+    uint16_t* __restrict__ out, float* __restrict__ lse, const uint16_t* __restrict__ q,
+    const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
+    const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
+    int64_t kv_stride, const int32_t* __restrict__ cu_kv, const int32_t* __restrict__ kv_pos,
+    int hq, int lg, float scale2) {
+  constexpr int KSTR = D + 8;    // K tile row (bf16 elements), 16-byte pad
+  constexpr int VSTR = kKT + 8;  // V^T tile row (bf16 elements), 16-byte pad
+  constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
+  constexpr int KPT = kKT * CPR / kThreads;  // K chunks per thread per tile
+  constexpr int VTASKS = (kKT / 4) * CPR;    // (4-key group, chunk) tasks per tile
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKT * KSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[D * VSTR];
+  __shared__ int kpos_lds[kKT];
+  __shared__ int red[4];
+
+  const int tile = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int G = 1 << lg;
+  const int rpb = 128 >> lg;
+  const int64_t r0 = cu_rows[b];
+  const int nr = cu_rows[b + 1] - (int)r0;
+  const int rbase = tile * rpb;
+  if (rbase >= nr) return;
+  const int64_t kv0 = cu_kv[b];
+  int nkv = cu_kv[b + 1] - (int)kv0;
+  if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
+  const int qv = 32 * w + lq;
+  const int rl = rbase + (qv >> lg);
+  const int head = g * G + (qv & (G - 1));
+  const int64_t grow = r0 + rl;
+  const bool valid = rl < nr && grow < n_rows;
+  const int qpos = valid ? row_pos[grow] : INT_MIN;
+
+  const int wmax = wave_max_i(valid ? qpos : -1);
+  const int wmin = wave_min_i(valid ? qpos : INT_MAX);
+  if (l == 0) red[w] = wmax;
+  __syncthreads();
+  const int bmax = max(max(red[0], red[1]), max(red[2], red[3]));
+  const int kv_end = kv_pos ? nkv : min(nkv, bmax + 1);
+  const int wave_end = kv_pos ? nkv : min(nkv, wmax + 1);
+
+  bf16x8 qreg[D / 16];
+  {
+    const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st)
+      qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
+  }
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
+  float m = -INFINITY, ls = 0.f;
+
+  uint4 kbuf[KPT], vbuf[4];
+  int kpos_reg = 0;
+  const uint16_t* kbase = kc + kv0 * kv_stride + (int64_t)g * D;
+  const uint16_t* vbase = vc + kv0 * kv_stride + (int64_t)g * D;
+  auto gload = [&](int kt0) {
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+      const int idx = threadIdx.x + c * kThreads;
+      const int key = idx / CPR, ch = idx - key * CPR;
+      const int j = kt0 + key;
+      kbuf[c] = j < nkv ? ld16(kbase + (int64_t)j * kv_stride + ch * 8) : make_uint4(0, 0, 0, 0);
+    }
+    if (threadIdx.x < VTASKS) {
+      const int grp = threadIdx.x / CPR, ch = threadIdx.x - grp * CPR;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = kt0 + 4 * grp + e;
+        vbuf[e] = j < nkv ? ld16(vbase + (int64_t)j * kv_stride + ch * 8) : make_uint4(0, 0, 0, 0);
+      }
+    }
+    if (kv_pos && threadIdx.x < kKT) {
+      const int j = kt0 + threadIdx.x;
+      kpos_reg = j < nkv ? kv_pos[kv0 + j] : INT_MAX;
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+      const int idx = threadIdx.x + c * kThreads;
+      const int key = idx / CPR, ch = idx - key * CPR;
+      st16(&k_lds[key * KSTR + ch * 8], kbuf[c]);
+    }
+    if (threadIdx.x < VTASKS) {
+      const int grp = threadIdx.x / CPR, ch = threadIdx.x - grp * CPR;
+      const int slot = (4 * grp & ~15) + vt_slot(4 * grp & 15);
+      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vbuf[0]);
+      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vbuf[1]);
+      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vbuf[2]);
+      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vbuf[3]);
+#pragma unroll
+      for (int dd = 0; dd < 8; ++dd) {
+        const int sh = (dd & 1) * 16;
+        const uint32_t a0 = (w0[dd >> 1] >> sh) & 0xffffu, a1 = (w1[dd >> 1] >> sh) & 0xffffu;
+        const uint32_t a2 = (w2[dd >> 1] >> sh) & 0xffffu, a3 = (w3[dd >> 1] >> sh) & 0xffffu;
+        *reinterpret_cast<uint2*>(&v_lds[(ch * 8 + dd) * VSTR + slot]) =
+            make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
+      }
+    }
+    if (kv_pos && threadIdx.x < kKT) kpos_lds[threadIdx.x] = kpos_reg;
+  };
+
+  if (kv_end > 0) {
+    gload(0);
+    lstore();
+  }
+  __syncthreads();
+  for (int kt0 = 0; kt0 < kv_end; kt0 += kKT) {
+    const bool has_next = kt0 + kKT < kv_end;
+    if (has_next) gload(kt0 + kKT);
+    if (kt0 < wave_end) {
+      f32x16 s[2];
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        s[blk] = f32x16{};
+#pragma unroll
+        for (int st = 0; st < D / 16; ++st) {
+          const bf16x8 a = as_bf16x8(ld16(&k_lds[(blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
+          s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], s[blk], 0, 0, 0);
+        }
+      }
+      const bool need_mask = kv_pos != nullptr || kt0 + kKT > wmin || kt0 + kKT > nkv;
+      float mt = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float x = s[blk][v] * scale2;
+          if (need_mask) {
+            const int jt = blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
+            const int j = kt0 + jt;
+            const int kp = kv_pos ? kpos_lds[jt] : j;
+            if (j >= nkv || kp > qpos) x = -INFINITY;
+          }
+          s[blk][v] = x;
+          mt = fmaxf(mt, x);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float mn = fmaxf(m, mt);
+      const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m - mn);
+      float psum = 0.f;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float p = (mn == -INFINITY) ? 0.f : exp2f(s[blk][v] - mn);
+          psum += p;
+          pb[blk * 2 + (v >> 3)][v & 7] = (__bf16)p;
+        }
+      ls = ls * alpha + psum;
+      m = mn;
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb) {
+          const bf16x8 a = as_bf16x8(ld16(&v_lds[(32 * mb + lq) * VSTR + 16 * s4 + 8 * hi]));
+          o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[s4], o[mb], 0, 0, 0);
+        }
+    }
+    __syncthreads();
+    if (has_next) {
+      lstore();
+      __syncthreads();
+    }
+  }
+
+  const float lt = ls + __shfl_xor(ls, 32, 64);
+  if (!valid) return;
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D;
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int d0 = 32 * mb + 8 * i + 4 * hi;
+      *reinterpret_cast<uint2*>(op + d0) =
+          make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
+                     pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
+    }
+  if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
+}
+
+// ---------------------------------------------------------------- fp32 path
+template <int D>
+__global__ __launch_bounds__(64) void attn_f32_kernel(
+    float* __restrict__ out, float* __restrict__ lse, const float* __restrict__ q,
+    const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
+    int batch, const float* __restrict__ kc, const float* __restrict__ vc, int64_t n_kv_rows,
+    int64_t kv_stride, const int32_t* __restrict__ cu_kv, const int32_t* __restrict__ kv_pos,
+    int hq, int hkv, float scale2) {
+  constexpr int E = D / 64;
+  const int64_t r = blockIdx.x;
+  const int h = blockIdx.y;
+  const int l = threadIdx.x;
+  // request of row r: last b with cu_rows[b] <= r
+  int lo = 0, hi = batch - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu_rows[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo;
+  if (r < cu_rows[b] || r >= cu_rows[b + 1] || r >= n_rows) return;
+  const int64_t kv0 = cu_kv[b];
+  int nkv = cu_kv[b + 1] - (int)kv0;
+  if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
+  const int g = h / (hq / hkv);
+  const int qpos = row_pos[r];
+  float qr[E], o[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    qr[e] = q[r * (int64_t)hq * D + (int64_t)h * D + l + 64 * e];
+    o[e] = 0.f;
+  }
+  float m = -INFINITY, ls = 0.f;
+  const int jend = kv_pos ? nkv : min(nkv, qpos + 1);
+  for (int j = 0; j < jend; ++j) {
+    if (kv_pos && kv_pos[kv0 + j] > qpos) continue;
+    const float* kp = kc + (kv0 + j) * kv_stride + (int64_t)g * D;
+    const float* vp = vc + (kv0 + j) * kv_stride + (int64_t)g * D;
+    float part = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) part += qr[e] * kp[l + 64 * e];
+    const float x = wave_sum(part) * scale2;
+    const float mn = fmaxf(m, x);
+    const float alpha = exp2f(m - mn), p = exp2f(x - mn);
+    ls = ls * alpha + p;
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = o[e] * alpha + p * vp[l + 64 * e];
+    m = mn;
+  }
+  const float inv = ls > 0.f ? 1.f / ls : 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) out[r * (int64_t)hq * D + (int64_t)h * D + l + 64 * e] = o[e] * inv;
+  if (lse && l == 0) lse[r * hq + h] = ls > 0.f ? (m + log2f(ls)) * kLn2 : -INFINITY;
+}
+
+}  // namespace
+
+size_t attn_workspace(const AttnShape&, bool) { return 0; }
+
+hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
+                              int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
+                              const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
+                              const int32_t* cu_kv, const int32_t* kv_pos, bool bf16,
+                              const AttnShape& s, float scale, void*, hipStream_t stream) {
+  if (n_rows == 0 || s.batch == 0 || s.max_rows == 0) return hipSuccess;
+  const float scale2 = scale * kLog2e;
+  int lg = 0;
+  while ((1 << lg) < s.hq / s.hkv) ++lg;
+  if (bf16) {
+    const int rpb = 128 >> lg;
+    dim3 grid((s.max_rows + rpb - 1) / rpb, s.hkv, s.batch);
+#define QCF_ATTN(D)                                                                               \
+  attn_bf16_kernel<D><<<grid, kThreads, 0, stream>>>(                                             \
+      static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
+      static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
+      kv_row_stride, cu_kv, kv_pos, s.hq, lg, scale2)
+    if (s.d == 64) QCF_ATTN(64); else QCF_ATTN(128);
+#undef QCF_ATTN
+    return hipGetLastError();
+  }
+  dim3 grid((unsigned)n_rows, s.hq);
+  if (s.d == 64)
+    attn_f32_kernel<64><<<grid, 64, 0, stream>>>(
+        static_cast<float*>(out), lse, static_cast<const float*>(q), row_pos, n_rows, cu_rows,
+        s.batch, static_cast<const float*>(k_cache), static_cast<const float*>(v_cache), n_kv_rows,
+        kv_row_stride, cu_kv, kv_pos, s.hq, s.hkv, scale2);
+  else
+    attn_f32_kernel<128><<<grid, 64, 0, stream>>>(
+        static_cast<float*>(out), lse, static_cast<const float*>(q), row_pos, n_rows, cu_rows,
+        s.batch, static_cast<const float*>(k_cache), static_cast<const float*>(v_cache), n_kv_rows,
+        kv_row_stride, cu_kv, kv_pos, s.hq, s.hkv, scale2);
+  return hipGetLastError();
+}
+
+}  // namespace qcf

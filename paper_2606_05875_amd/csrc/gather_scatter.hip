@@ -1,0 +1,135 @@
+// Row gather (anchor cache, eq. anchor_cache) and the fused-cache scatter
+// (eq. fuse_cache) with the rotary embedding of the recomputed rows.
+//
+// Both are HBM-bound streams of 16-byte vectors.  The scatter gives every
+// recomputed row its own block: the block forms the row's d/2 (cos, sin) pairs
+// once (float64 angle) and its threads then rotate the row's key heads and
+// query heads and copy its value heads, so the per-row trigonometry is shared
+// by all H_q + H_kv heads of the row.
+#include "qcf_device.h"
+#include "qcf_launch.h"
+
+namespace qcf {
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void gather_rows_kernel(
+    uint8_t* __restrict__ dst, const uint8_t* __restrict__ src, const int32_t* __restrict__ idx,
+    int64_t n_rows, int64_t n_src_rows, int64_t chunks_per_row, int64_t src_stride,
+    int64_t dst_stride) {
+  const int64_t total = n_rows * chunks_per_row;
+  for (int64_t u = (int64_t)blockIdx.x * kThreads + threadIdx.x; u < total;
+       u += (int64_t)gridDim.x * kThreads) {
+    const int64_t r = u / chunks_per_row;
+    const int64_t c = u - r * chunks_per_row;
+    const int64_t s = idx[r];
+    if (s < 0 || s >= n_src_rows) continue;
+    st16(dst + r * dst_stride + c * 16, ld16(src + s * src_stride + c * 16));
+  }
+}
+
+// Rotate `units` 16-byte rotate-half vectors of a row: unit u covers head
+// u / UPH, pair offset j = (u % UPH) * VEC.
+template <typename T, int D>
+__device__ __forceinline__ void rope_row(T* dst, const T* src, int units, const float2* cs) {
+  constexpr int HALF = D / 2;
+  constexpr int VEC = Vec16<T>::N;
+  constexpr int UPH = HALF / VEC;
+  for (int u = threadIdx.x; u < units; u += kThreads) {
+    const int h = u / UPH;
+    const int j = (u - h * UPH) * VEC;
+    const int off = h * D + j;
+    float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
+    Vec16<T>::unpack(ld16(src + off), x1);
+    Vec16<T>::unpack(ld16(src + off + HALF), x2);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const float2 r = cs[j + e];
+      y1[e] = x1[e] * r.x - x2[e] * r.y;
+      y2[e] = x1[e] * r.y + x2[e] * r.x;
+    }
+    st16(dst + off, Vec16<T>::pack(y1));
+    st16(dst + off + HALF, Vec16<T>::pack(y2));
+  }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void scatter_kv_kernel(
+    T* k_cache, T* v_cache, int64_t n_cache_rows, int64_t cache_stride, const T* k_new,
+    const T* v_new, const T* q_new, T* q_out, int64_t n_src_rows, const int32_t* src_idx,
+    const int32_t* __restrict__ row_idx, const int32_t* __restrict__ row_pos, int hq, int hkv,
+    double theta) {
+  constexpr int HALF = D / 2;
+  constexpr int VEC = Vec16<T>::N;
+  __shared__ float2 cs[HALF];
+  const int64_t r = blockIdx.x;
+  const int64_t s = src_idx ? (int64_t)src_idx[r] : r;
+  if (s < 0 || s >= n_src_rows) return;
+  const int64_t dst = row_idx[r];
+  const bool dst_ok = dst >= 0 && dst < n_cache_rows;
+  if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)row_pos[r], threadIdx.x, D, theta);
+  __syncthreads();
+  const int kv_row = hkv * D;
+  if (dst_ok) {
+    rope_row<T, D>(k_cache + dst * cache_stride, k_new + s * kv_row, hkv * (HALF / VEC), cs);
+    const T* vs = v_new + s * kv_row;
+    T* vd = v_cache + dst * cache_stride;
+    for (int c = threadIdx.x; c < kv_row / VEC; c += kThreads) st16(vd + c * VEC, ld16(vs + c * VEC));
+  }
+  if (q_out) {
+    const int q_row = hq * D;
+    rope_row<T, D>(q_out + r * q_row, q_new + s * q_row, hq * (HALF / VEC), cs);
+  }
+}
+
+template <typename T, int D>
+hipError_t scatter_t(void* k_cache, void* v_cache, int64_t n_cache_rows, int64_t cache_stride,
+                     const void* k_new, const void* v_new, const void* q_new, void* q_out,
+                     int64_t n_src_rows, const int32_t* src_idx, int64_t n_rows,
+                     const int32_t* row_idx, const int32_t* row_pos, int hq, int hkv,
+                     double theta, hipStream_t stream) {
+  scatter_kv_kernel<T, D><<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(
+      static_cast<T*>(k_cache), static_cast<T*>(v_cache), n_cache_rows, cache_stride,
+      static_cast<const T*>(k_new), static_cast<const T*>(v_new), static_cast<const T*>(q_new),
+      static_cast<T*>(q_out), n_src_rows, src_idx, row_idx, row_pos, hq, hkv, theta);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
+                              int64_t n_src_rows, int64_t row_bytes, int64_t src_stride,
+                              int64_t dst_stride, hipStream_t stream) {
+  if (n_rows == 0 || row_bytes == 0) return hipSuccess;
+  const int64_t chunks = row_bytes / 16;
+  const int64_t total = n_rows * chunks;
+  int64_t blocks = (total + kThreads - 1) / kThreads;
+  if (blocks > 65536) blocks = 65536;
+  gather_rows_kernel<<<dim3((unsigned)blocks), kThreads, 0, stream>>>(
+      static_cast<uint8_t*>(dst), static_cast<const uint8_t*>(src), idx, n_rows, n_src_rows,
+      chunks, src_stride, dst_stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
+                             int64_t cache_row_stride, const void* k_new, const void* v_new,
+                             const void* q_new, void* q_out, int64_t n_src_rows,
+                             const int32_t* src_idx, bool bf16, int64_t n_rows,
+                             const int32_t* row_idx, const int32_t* row_pos, int hq, int hkv,
+                             int d, double theta, hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+#define QCF_SCATTER(T, D)                                                                   \
+  return scatter_t<T, D>(k_cache, v_cache, n_cache_rows, cache_row_stride, k_new, v_new, q_new, \
+                         q_out, n_src_rows, src_idx, n_rows, row_idx, row_pos, hq, hkv, theta, \
+                         stream)
+  if (bf16) {
+    if (d == 64) QCF_SCATTER(uint16_t, 64);
+    QCF_SCATTER(uint16_t, 128);
+  }
+  if (d == 64) QCF_SCATTER(float, 64);
+  QCF_SCATTER(float, 128);
+#undef QCF_SCATTER
+}
+
+}  // namespace qcf

@@ -1,0 +1,53 @@
+// Internal launchers of libqcf (host side).  Arguments were validated by the
+// C ABI layer; each launcher enqueues its kernels on `stream` and returns the
+// HIP launch status.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace qcf {
+
+hipError_t launch_rerope(void* k_out, const void* k_in, bool bf16, int64_t n_tokens, int hkv,
+                         int d, int64_t row_stride, int n_seg, const int32_t* seg_start,
+                         const int32_t* seg_len, const int32_t* seg_delta, int max_seg_len,
+                         double theta, hipStream_t stream);
+
+hipError_t launch_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
+                              int64_t n_src_rows, int64_t row_bytes, int64_t src_stride,
+                              int64_t dst_stride, hipStream_t stream);
+
+hipError_t launch_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
+                             int64_t cache_row_stride, const void* k_new, const void* v_new,
+                             const void* q_new, void* q_out, int64_t n_src_rows,
+                             const int32_t* src_idx, bool bf16, int64_t n_rows,
+                             const int32_t* row_idx, const int32_t* row_pos, int hq, int hkv,
+                             int d, double theta, hipStream_t stream);
+
+hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
+                              const float* scores, int64_t n_scores, int n_seg,
+                              const int32_t* seg_start, const int32_t* seg_len,
+                              const int32_t* seg_k, const int32_t* out_start,
+                              const int32_t* pos_base, int max_seg_len, hipStream_t stream);
+
+struct ProbeShape {
+  int batch, max_q_len, max_ctx_len, hq, hkv, d;
+};
+size_t probe_scores_workspace(const ProbeShape& s);
+hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                               const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                               bool bf16, const int32_t* cu_q, const int32_t* cu_kv,
+                               const int32_t* ctx_len, const ProbeShape& s, float scale,
+                               void* ws, hipStream_t stream);
+
+struct AttnShape {
+  int batch, max_rows, max_kv, hq, hkv, d;
+};
+size_t attn_workspace(const AttnShape& s, bool bf16);
+hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
+                              int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
+                              const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
+                              const int32_t* cu_kv, const int32_t* kv_pos, bool bf16,
+                              const AttnShape& s, float scale, void* ws, hipStream_t stream);
+
+}  // namespace qcf

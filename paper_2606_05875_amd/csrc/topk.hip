@@ -1,0 +1,168 @@
+// Per-segment top-k of the importance scores: the recomputation set of
+// eq. critical_mask, taken chunk by chunk.
+//
+// One block per segment.  Scores become order-preserving uint32 keys (larger
+// score -> larger key, -0 == +0) staged in LDS when the segment fits.  A
+// most-significant-digit radix select (4 passes of 8 bits, LDS histograms)
+// finds the key tau of the k-th largest score and how many of the keys equal
+// to tau are still needed.  A final pass walks the segment in index order:
+// wave ballots and lane-prefix bit counts give each selected row its output
+// slot, taking keys > tau and the lowest-index keys == tau, so the output is
+// ascending and ties go to the lower row -- exactly the order (score desc,
+// index asc).  The result is bit-exact and independent of scheduling.
+#include "qcf_device.h"
+#include "qcf_launch.h"
+
+namespace qcf {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kLdsKeys = 8192;  // 32 KB of staged keys
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t b = __float_as_uint(x);
+  if ((b & 0x7fffffffu) == 0u) b = 0u;  // -0 == +0
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Exclusive block-wide prefix count of `pred` (in thread order) and the total.
+__device__ __forceinline__ uint32_t block_prefix(bool pred, uint32_t* wave_tot, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t m = __ballot(pred);
+  const uint32_t below = lanes_below(m);
+  if (lane == 0) wave_tot[wave] = (uint32_t)__popcll(m);
+  __syncthreads();
+  uint32_t before = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t t = wave_tot[w];
+    before += (w < wave) ? t : 0u;
+    total += t;
+  }
+  __syncthreads();
+  return before + below;
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(kThreads) void select_topk_kernel(
+    int32_t* __restrict__ out_idx, int32_t* __restrict__ out_pos, int64_t n_out,
+    const float* __restrict__ scores, int64_t n_scores, const int32_t* __restrict__ seg_start,
+    const int32_t* __restrict__ seg_len, const int32_t* __restrict__ seg_k,
+    const int32_t* __restrict__ out_start, const int32_t* __restrict__ pos_base) {
+  __shared__ uint32_t keys[kLds ? kLdsKeys : 1];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t wave_tot[kWaves];
+  __shared__ uint32_t sh_digit, sh_above;
+
+  const int s = blockIdx.x;
+  const int64_t start = seg_start[s];
+  int n = seg_len[s];
+  int k = seg_k[s];
+  const int64_t o = out_start[s];
+  const int pb = pos_base ? pos_base[s] : 0;
+  if (n <= 0 || k <= 0 || start < 0 || start + n > n_scores) return;
+  if (kLds && n > kLdsKeys) return;  // violates max_seg_len: nothing is written
+  if (k > n) k = n;
+  if (o < 0 || o + k > n_out) return;
+  const float* sc = scores + start;
+  const int tid = threadIdx.x;
+
+  if (kLds) {
+    for (int i = tid; i < n; i += kThreads) keys[i] = order_key(sc[i]);
+    __syncthreads();
+  }
+  auto key_at = [&](int i) -> uint32_t { return kLds ? keys[i] : order_key(sc[i]); };
+
+  const bool take_all = (k == n);
+  uint32_t prefix = 0u, mask = 0u;
+  int remaining = k;  // how many of the keys matching `prefix` are still to be taken
+  if (!take_all) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      hist[tid] = 0u;  // kThreads == 256 bins
+      __syncthreads();
+      for (int i = tid; i < n; i += kThreads) {
+        const uint32_t key = key_at(i);
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      if (tid < 64) {
+        // lane l owns digits 255-4l .. 252-4l (descending digit order)
+        uint32_t c[4];
+        uint32_t own = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          c[e] = hist[255 - 4 * tid - e];
+          own += c[e];
+        }
+        // exclusive prefix over lanes = keys with a larger digit
+        uint32_t incl = own;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const uint32_t t = __shfl_up(incl, off, 64);
+          if (tid >= off) incl += t;
+        }
+        uint32_t above = incl - own;
+        if (above < (uint32_t)remaining && (uint32_t)remaining <= incl) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (above + c[e] >= (uint32_t)remaining) {
+              sh_digit = 255u - 4u * tid - e;
+              sh_above = above;
+              break;
+            }
+            above += c[e];
+          }
+        }
+      }
+      __syncthreads();
+      const uint32_t digit = sh_digit;
+      remaining -= (int)sh_above;
+      prefix |= digit << shift;
+      mask |= 255u << shift;
+      __syncthreads();
+    }
+  }
+  const uint32_t tau = prefix;
+
+  // ordered compaction: keys > tau, then the `remaining` lowest-index keys == tau
+  uint32_t eq_base = 0, sel_base = 0;
+  for (int t0 = 0; t0 < n; t0 += kThreads) {
+    const int i = t0 + tid;
+    const bool valid = i < n;
+    const uint32_t key = valid ? key_at(i) : 0u;
+    const bool gt = valid && (take_all || key > tau);
+    const bool eq = valid && !take_all && key == tau;
+    uint32_t eq_tot, sel_tot;
+    const uint32_t eq_rank = eq_base + block_prefix(eq, wave_tot, eq_tot);
+    const bool sel = gt || (eq && eq_rank < (uint32_t)remaining);
+    const uint32_t slot = sel_base + block_prefix(sel, wave_tot, sel_tot);
+    if (sel && slot < (uint32_t)k) {
+      out_idx[o + slot] = (int32_t)(start + i);
+      if (out_pos) out_pos[o + slot] = (int32_t)(start + i) - pb;
+    }
+    eq_base += eq_tot;
+    sel_base += sel_tot;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
+                              const float* scores, int64_t n_scores, int n_seg,
+                              const int32_t* seg_start, const int32_t* seg_len,
+                              const int32_t* seg_k, const int32_t* out_start,
+                              const int32_t* pos_base, int max_seg_len, hipStream_t stream) {
+  if (n_seg == 0 || max_seg_len == 0) return hipSuccess;
+  if (max_seg_len <= kLdsKeys) {
+    select_topk_kernel<true><<<dim3(n_seg), kThreads, 0, stream>>>(
+        out_idx, out_pos, n_out, scores, n_scores, seg_start, seg_len, seg_k, out_start, pos_base);
+  } else {
+    select_topk_kernel<false><<<dim3(n_seg), kThreads, 0, stream>>>(
+        out_idx, out_pos, n_out, scores, n_scores, seg_start, seg_len, seg_k, out_start, pos_base);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace qcf

@@ -1,0 +1,264 @@
+"""Python binding of libqcf (ctypes).  Argument marshalling only.
+
+Each function has the name of the C entry point it calls, takes torch tensors
+on the GPU, checks their device, dtype, layout and shape, and passes raw
+pointers plus the current HIP stream.  All work runs in the library's
+kernels.  If ``libqcf.so`` has not been built the first call raises: there is
+no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "QcfError", "lib", "lib_path", "qcf_version", "qcf_status_string", "qcf_rerope",
+    "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
+    "qcf_select_topk", "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
+    "EXPORTS",
+]
+
+QCF_F32, QCF_BF16 = 0, 1
+_DT = {torch.float32: QCF_F32, torch.bfloat16: QCF_BF16}
+_LIB = None
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+
+# name -> (restype, argtypes); mirrors include/qcf.h
+EXPORTS = {
+    "qcf_version": (_I, []),
+    "qcf_status_string": (ctypes.c_char_p, [_I]),
+    "qcf_rerope": (_I, [_P, _P, _I, _I64, _I, _I, _I64, _I, _P, _P, _P, _I, ctypes.c_double, _P]),
+    "qcf_gather_rows": (_I, [_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _P]),
+    "qcf_scatter_kv": (_I, [_P, _P, _I64, _I64, _P, _P, _P, _P, _I64, _P, _I, _I64, _P, _P, _I, _I,
+                            _I, ctypes.c_double, _P]),
+    "qcf_probe_scores_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "qcf_probe_scores": (_I, [_P, _I, _P, _I64, _P, _I64, _I64, _I, _I, _P, _P, _P, _I, _I, _I, _I,
+                              _I, ctypes.c_float, _P, _SZ, _P]),
+    "qcf_select_topk": (_I, [_P, _P, _I64, _P, _I64, _I, _P, _P, _P, _P, _P, _I, _P]),
+    "qcf_sparse_prefill_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
+    "qcf_sparse_prefill_attn": (_I, [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I, _I,
+                                     _I, _I, _I, _I, _I, ctypes.c_float, _P, _SZ, _P]),
+}
+
+
+class QcfError(RuntimeError):
+    pass
+
+
+def lib_path() -> str:
+    return os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqcf.so")
+
+
+def lib():
+    """Load libqcf.so once; raise if it is missing (no fallback path exists)."""
+    global _LIB
+    if _LIB is None:
+        path = lib_path()
+        if not os.path.exists(path):
+            raise QcfError(f"{path} is missing: build it with `python -m paper_2606_05875_amd.build`")
+        h = ctypes.CDLL(path)
+        for name, (res, args) in EXPORTS.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = h
+    return _LIB
+
+
+def _check(status: int, name: str):
+    if status != 0:
+        msg = lib().qcf_status_string(status).decode()
+        raise QcfError(f"{name} failed with status {status}: {msg}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise QcfError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise QcfError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _rows(t, name):
+    """Token-major tensor [rows, heads, d] (or [rows, cols]) with a dense row; returns row stride."""
+    if t.dim() < 2 or (t.shape[0] > 0 and not t[0].is_contiguous()):
+        raise QcfError(f"{name} must have dense rows")
+    return t.stride(0)
+
+
+def _dtype(t):
+    if t.dtype not in _DT:
+        raise QcfError(f"unsupported dtype {t.dtype}")
+    return _DT[t.dtype]
+
+
+def _i32(t, name):
+    _dev(t, name, torch.int32)
+    if t is not None and not t.is_contiguous():
+        raise QcfError(f"{name} must be contiguous")
+
+
+def qcf_version() -> int:
+    return lib().qcf_version()
+
+
+def qcf_status_string(status: int) -> str:
+    return lib().qcf_status_string(status).decode()
+
+
+def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_theta):
+    """Rotate each segment's keys by its offset; k_out may be k_in.  Shapes [T, H_kv, d]."""
+    _dev(k_out, "k_out", k_in.dtype)
+    _dev(k_in, "k_in")
+    for n, t in (("seg_start", seg_start), ("seg_len", seg_len), ("seg_delta", seg_delta)):
+        _i32(t, n)
+    if k_out.shape != k_in.shape or k_out.stride(0) != k_in.stride(0):
+        raise QcfError("k_out and k_in must have the same shape and row stride")
+    T, H, d = k_in.shape
+    st = lib().qcf_rerope(_ptr(k_out), _ptr(k_in), _dtype(k_in), T, H, d, _rows(k_in, "k_in"),
+                          seg_start.numel(), _ptr(seg_start), _ptr(seg_len), _ptr(seg_delta),
+                          int(max_seg_len), float(rope_theta), _stream())
+    _check(st, "qcf_rerope")
+
+
+def qcf_gather_rows(dst, src, idx):
+    """dst[i] = src[idx[i]] for every row (rows of equal byte size)."""
+    _dev(dst, "dst", src.dtype)
+    _dev(src, "src")
+    _i32(idx, "idx")
+    if dst.shape[0] != idx.numel() or dst.shape[1:] != src.shape[1:]:
+        raise QcfError("dst must be [len(idx), *src.shape[1:]]")
+    row_bytes = src[0].numel() * src.element_size() if src.shape[0] else dst[0].numel() * dst.element_size()
+    st = lib().qcf_gather_rows(_ptr(dst), _ptr(src), _ptr(idx), idx.numel(), src.shape[0], row_bytes,
+                               _rows(src, "src") * src.element_size(),
+                               _rows(dst, "dst") * dst.element_size(), _stream())
+    _check(st, "qcf_gather_rows")
+
+
+def qcf_scatter_kv(k_cache, v_cache, k_new, v_new, row_idx, row_pos, rope_theta, q_new=None,
+                   q_out=None, src_idx=None):
+    """Fused-cache update: rope(k_new[s]) and v_new[s] into cache rows row_idx; rope(q_new[s]) -> q_out."""
+    for n, t in (("k_cache", k_cache), ("v_cache", v_cache), ("k_new", k_new), ("v_new", v_new),
+                 ("q_new", q_new), ("q_out", q_out)):
+        _dev(t, n, k_cache.dtype)
+    for n, t in (("row_idx", row_idx), ("row_pos", row_pos), ("src_idx", src_idx)):
+        _i32(t, n)
+    T, Hkv, d = k_cache.shape
+    if v_cache.shape != k_cache.shape or v_cache.stride(0) != k_cache.stride(0):
+        raise QcfError("k_cache and v_cache must match")
+    if not (k_new.is_contiguous() and v_new.is_contiguous() and k_new.shape[1:] == (Hkv, d)
+            and v_new.shape == k_new.shape):
+        raise QcfError("k_new/v_new must be dense [rows, H_kv, d]")
+    n = row_idx.numel()
+    if row_pos.numel() != n or (src_idx is not None and src_idx.numel() != n):
+        raise QcfError("row_idx, row_pos and src_idx must have the same length")
+    hq = Hkv
+    if q_out is not None:
+        if q_new is None or not (q_new.is_contiguous() and q_out.is_contiguous()):
+            raise QcfError("q_new/q_out must be dense")
+        hq = q_new.shape[1]
+        if q_out.shape != (n, hq, d) or q_new.shape[1:] != (hq, d) or q_new.shape[0] != k_new.shape[0]:
+            raise QcfError("q_out must be [n_rows, H_q, d] and q_new [n_src_rows, H_q, d]")
+    st = lib().qcf_scatter_kv(_ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"), _ptr(k_new),
+                              _ptr(v_new), _ptr(q_new), _ptr(q_out), k_new.shape[0], _ptr(src_idx),
+                              _dtype(k_cache), n, _ptr(row_idx), _ptr(row_pos), hq, Hkv, d,
+                              float(rope_theta), _stream())
+    _check(st, "qcf_scatter_kv")
+
+
+def qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim):
+    return int(lib().qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, n_q_heads,
+                                                     n_kv_heads, head_dim))
+
+
+def qcf_probe_scores(scores, q, k, cu_q, cu_kv, ctx_len, max_q_len, max_ctx_len, softmax_scale,
+                     accumulate=False, workspace=None):
+    """Critical-layer importance of every context token; q [n_q, H_q, d], k [T, H_kv, d]."""
+    _dev(scores, "scores", torch.float32)
+    _dev(q, "q")
+    _dev(k, "k", q.dtype)
+    for n, t in (("cu_q", cu_q), ("cu_kv", cu_kv), ("ctx_len", ctx_len)):
+        _i32(t, n)
+    if not q.is_contiguous():
+        raise QcfError("q must be dense")
+    nq, hq, d = q.shape
+    T, hkv, d2 = k.shape
+    if d2 != d or scores.numel() != T:
+        raise QcfError("scores must have one entry per row of k; head_dim must match")
+    batch = ctx_len.numel()
+    need = qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, hq, hkv, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    st = lib().qcf_probe_scores(_ptr(scores), int(bool(accumulate)), _ptr(q), nq, _ptr(k), T,
+                                _rows(k, "k"), _dtype(q), batch, _ptr(cu_q), _ptr(cu_kv), _ptr(ctx_len),
+                                int(max_q_len), int(max_ctx_len), hq, hkv, d, float(softmax_scale),
+                                _ptr(workspace), workspace.numel(), _stream())
+    _check(st, "qcf_probe_scores")
+
+
+def qcf_select_topk(out_idx, scores, seg_start, seg_len, seg_k, out_start, max_seg_len, out_pos=None,
+                    pos_base=None):
+    """Per-segment top-k rows (ascending, ties to the lower row) into out_idx[out_start[s] ..]."""
+    _dev(scores, "scores", torch.float32)
+    for n, t in (("out_idx", out_idx), ("seg_start", seg_start), ("seg_len", seg_len),
+                 ("seg_k", seg_k), ("out_start", out_start), ("out_pos", out_pos),
+                 ("pos_base", pos_base)):
+        _i32(t, n)
+    if out_pos is not None and out_pos.numel() != out_idx.numel():
+        raise QcfError("out_pos must match out_idx")
+    st = lib().qcf_select_topk(_ptr(out_idx), _ptr(out_pos), out_idx.numel(), _ptr(scores),
+                               scores.numel(), seg_start.numel(), _ptr(seg_start), _ptr(seg_len),
+                               _ptr(seg_k), _ptr(out_start), _ptr(pos_base), int(max_seg_len), _stream())
+    _check(st, "qcf_select_topk")
+
+
+def qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, n_q_heads, n_kv_heads, head_dim,
+                                           dtype=torch.bfloat16):
+    return int(lib().qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, n_q_heads,
+                                                            n_kv_heads, head_dim, _DT[dtype]))
+
+
+def qcf_sparse_prefill_attn(out, q, row_pos, cu_rows, k_cache, v_cache, cu_kv, max_rows, max_kv,
+                            softmax_scale, kv_pos=None, lse=None, workspace=None):
+    """Causal GQA attention of rows q over the cache (explicit key positions with kv_pos)."""
+    _dev(out, "out", q.dtype)
+    _dev(q, "q")
+    _dev(k_cache, "k_cache", q.dtype)
+    _dev(v_cache, "v_cache", q.dtype)
+    _dev(lse, "lse", torch.float32)
+    for n, t in (("row_pos", row_pos), ("cu_rows", cu_rows), ("cu_kv", cu_kv), ("kv_pos", kv_pos)):
+        _i32(t, n)
+    if not (q.is_contiguous() and out.is_contiguous()) or out.shape != q.shape:
+        raise QcfError("q and out must be dense and of the same shape")
+    n, hq, d = q.shape
+    T, hkv, d2 = k_cache.shape
+    if v_cache.shape != k_cache.shape or v_cache.stride(0) != k_cache.stride(0) or d2 != d:
+        raise QcfError("k_cache/v_cache mismatch")
+    if row_pos.numel() != n or (kv_pos is not None and kv_pos.numel() != T):
+        raise QcfError("row_pos must have one entry per row, kv_pos one per cache row")
+    if lse is not None and lse.shape != (n, hq):
+        raise QcfError("lse must be [n_rows, H_q]")
+    batch = cu_rows.numel() - 1
+    need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, hq, hkv, d, q.dtype)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    st = lib().qcf_sparse_prefill_attn(_ptr(out), _ptr(lse), _ptr(q), _ptr(row_pos), n, _ptr(cu_rows),
+                                       _ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"),
+                                       _ptr(cu_kv), _ptr(kv_pos), _dtype(q), batch, int(max_rows),
+                                       int(max_kv), hq, hkv, d, float(softmax_scale), _ptr(workspace),
+                                       0 if workspace is None else workspace.numel(), _stream())
+    _check(st, "qcf_sparse_prefill_attn")

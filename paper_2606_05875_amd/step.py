@@ -1,0 +1,225 @@
+"""One layer's QCFuse fusion step on the GPU, as a stream-ordered chain of libqcf calls.
+
+The host only lays out index arrays whose sizes it already knows (chunk
+offsets, per-chunk selection budgets k_i = floor(rho * n_i), the slots of the
+recomputed rows, the probe buffer layout); they are computed once per batch
+layout and uploaded before the step.  Every step of the path itself --
+re-positioning, anchor gather, probe attention, scores, selection, scatter,
+attention -- runs in the library's kernels, with no device-to-host
+synchronisation inside the step.
+
+Sequence of one step (Section 3.5, selective token localization followed by
+one layer of cache fusion):
+  1. qcf_rerope          stored chunk keys -> request positions (eq. pic_online)
+  2. qcf_scatter_kv      user-query rows: rotate q/k at N+i, write K/V into the cache
+  3. qcf_gather_rows x2  anchor cache [KV^A ; query K/V] (eq. anchor_cache)
+  4. qcf_sparse_prefill_attn  query probe over the anchor cache (eq. anchor_query_state)
+  5. qcf_probe_scores    I(t) over the context keys (eq. single_layer_importance)
+  6. qcf_select_topk     per-chunk top-k -> P (eq. critical_mask)
+  7. qcf_scatter_kv      rows R = P + query: rotate fresh q/k, write fresh K/V (eq. fuse_cache)
+  8. qcf_sparse_prefill_attn  causal attention of R over the fused cache (Section 2.1.3)
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import qcf
+
+__all__ = ["FusionPlan", "FusionStep"]
+
+
+@dataclass
+class FusionPlan:
+    """Host-side layout of one layer's step for a batch (sizes only, no scores)."""
+
+    seg_k: np.ndarray        # [n_chunks] selection budget of each chunk
+    out_start: np.ndarray    # [n_chunks] first slot of each chunk's selection in R
+    cu_R: np.ndarray         # [B+1] recomputed-row slots per request: [P_b ; U_b]
+    n_P: np.ndarray          # [B] |P_b|
+    R_idx_init: np.ndarray   # [|R|] cache rows; query-row slots filled, P slots -1
+    R_pos_init: np.ndarray   # [|R|] positions; query-row slots filled
+    pos_base: np.ndarray     # [n_chunks] first cache row of the chunk's request
+    u_idx: np.ndarray        # [n_q] cache rows of all query tokens
+    u_pos: np.ndarray        # [n_q] positions N_b + i
+    probe_idx: np.ndarray    # [n_probe] cache rows gathered into the probe buffer
+    probe_pos: np.ndarray    # [n_probe] request positions of those rows
+    cu_probe: np.ndarray     # [B+1]
+    max_q: int
+    max_ctx: int
+    max_R: int
+    max_probe: int
+    max_seg: int
+
+    @staticmethod
+    def build(w, rho_bp: int) -> "FusionPlan":
+        B = w.batch
+        seg_k = (int(rho_bp) * w.seg_len.astype(np.int64)) // 10000
+        n_P = np.zeros(B, np.int64)
+        for s in range(w.n_chunks):
+            n_P[w.seg_req[s]] += seg_k[s]
+        q_lens = np.array(w.q_lens, np.int64)
+        cu_R = np.concatenate([[0], np.cumsum(n_P + q_lens)])
+        out_start = np.zeros(w.n_chunks, np.int64)
+        fill = cu_R[:-1].copy()
+        for s in range(w.n_chunks):
+            out_start[s] = fill[w.seg_req[s]]
+            fill[w.seg_req[s]] += seg_k[s]
+        R_idx = np.full(int(cu_R[-1]), -1, np.int64)
+        R_pos = np.full(int(cu_R[-1]), -1, np.int64)
+        u_idx, u_pos, probe_idx, probe_pos, cu_probe = [], [], [], [], [0]
+        for b in range(B):
+            base, N, nq = int(w.cu_kv[b]), int(w.ctx_len[b]), int(w.q_lens[b])
+            rows = np.arange(base + N, base + N + nq)
+            pos = np.arange(N, N + nq)
+            s0 = int(cu_R[b] + n_P[b])
+            R_idx[s0:s0 + nq] = rows
+            R_pos[s0:s0 + nq] = pos
+            u_idx.append(rows)
+            u_pos.append(pos)
+            segs = np.nonzero(w.seg_req == b)[0]
+            arows = [w.seg_start[s] + w.anchor_local[s] for s in segs]
+            arows = np.concatenate(arows) if arows else np.zeros(0, np.int64)
+            probe_idx += [arows, rows]
+            probe_pos += [arows - base, pos]
+            cu_probe.append(cu_probe[-1] + arows.size + nq)
+        cat = lambda xs: np.concatenate(xs).astype(np.int32) if xs else np.zeros(0, np.int32)
+        pos_base = w.cu_kv[w.seg_req].astype(np.int32)
+        return FusionPlan(
+            seg_k=seg_k.astype(np.int32), out_start=out_start.astype(np.int32),
+            cu_R=cu_R.astype(np.int32), n_P=n_P, R_idx_init=R_idx.astype(np.int32),
+            R_pos_init=R_pos.astype(np.int32), pos_base=pos_base, u_idx=cat(u_idx),
+            u_pos=cat(u_pos), probe_idx=cat(probe_idx), probe_pos=cat(probe_pos),
+            cu_probe=np.array(cu_probe, np.int32), max_q=int(max(w.q_lens) if B else 0),
+            max_ctx=int(w.ctx_len.max() if B else 0),
+            max_R=int(np.diff(cu_R).max() if B else 0),
+            max_probe=int(np.diff(cu_probe).max() if B else 0),
+            max_seg=int(w.seg_len.max() if w.n_chunks else 0))
+
+
+class FusionStep:
+    """Device buffers and the call chain of one layer's fusion step for workload ``w``.
+
+    ``run()`` enqueues the eight stages on the current stream.  The stored
+    chunk keys (``k_pic``) are never modified (re-positioning writes the
+    working cache ``k``), so ``run()`` can be repeated; the working value cache
+    ``v`` starts as the stored values and receives the recomputed rows.
+    """
+
+    def __init__(self, w, rho_bp: int | None = None, device="cuda"):
+        self.w = w
+        self.rho_bp = w.rho_bp if rho_bp is None else int(rho_bp)
+        self.plan = p = FusionPlan.build(w, self.rho_bp)
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.dtype = dt
+        dev = torch.device(device)
+        self.device = dev
+        T, hq, hkv, d = w.n_rows, w.n_q_heads, w.n_kv_heads, w.head_dim
+        self.scale = 1.0 / math.sqrt(d)
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        f = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+        # inputs
+        self.k_pic = f(w.k_pic)
+        self.v_pic = f(w.v_pic)
+        self.q_new = f(w.q_new)
+        self.k_new = f(w.k_new)
+        self.v_new = f(w.v_new)
+        # layout (int32)
+        self.seg_start, self.seg_len, self.seg_delta = t(w.seg_start), t(w.seg_len), t(w.seg_delta)
+        self.seg_k, self.out_start, self.pos_base = t(p.seg_k), t(p.out_start), t(p.pos_base)
+        self.cu_kv, self.ctx_len, self.cu_q = t(w.cu_kv), t(w.ctx_len), t(w.cu_q)
+        self.cu_R, self.cu_probe = t(p.cu_R), t(p.cu_probe)
+        self.u_idx, self.u_pos = t(p.u_idx), t(p.u_pos)
+        self.probe_idx, self.probe_pos = t(p.probe_idx), t(p.probe_pos)
+        self.R_idx_init, self.R_pos_init = t(p.R_idx_init), t(p.R_pos_init)
+        # working state and outputs
+        self.k = torch.zeros_like(self.k_pic)
+        self.v = self.v_pic.clone()
+        self.R_idx = self.R_idx_init.clone()
+        self.R_pos = self.R_pos_init.clone()
+        nU, nR, nP = p.u_idx.size, p.R_idx_init.size, p.probe_idx.size
+        self.q_u = torch.empty((nU, hq, d), dtype=dt, device=dev)
+        self.q_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
+        self.k_probe = torch.empty((nP, hkv, d), dtype=dt, device=dev)
+        self.v_probe = torch.empty((nP, hkv, d), dtype=dt, device=dev)
+        self.o_probe = torch.empty((nU, hq, d), dtype=dt, device=dev)
+        self.o = torch.empty((nR, hq, d), dtype=dt, device=dev)
+        self.scores = torch.zeros(T, dtype=torch.float32, device=dev)
+        nws = qcf.qcf_probe_scores_workspace_size(w.batch, p.max_q, p.max_ctx, hq, hkv, d)
+        self.ws_scores = torch.empty(max(nws, 256), dtype=torch.uint8, device=dev)
+        nwa = qcf.qcf_sparse_prefill_attn_workspace_size(w.batch, max(p.max_R, p.max_probe),
+                                                         max(int(w.cu_kv.max() if w.batch else 0), 1),
+                                                         hq, hkv, d, dt)
+        self.ws_attn = torch.empty(max(nwa, 256), dtype=torch.uint8, device=dev)
+
+    # -- stages ---------------------------------------------------------------
+    def stage_rerope(self):
+        w, p = self.w, self.plan
+        qcf.qcf_rerope(self.k, self.k_pic, self.seg_start, self.seg_len, self.seg_delta, p.max_seg,
+                       w.rope_theta)
+
+    def stage_query_rows(self):
+        qcf.qcf_scatter_kv(self.k, self.v, self.k_new, self.v_new, self.u_idx, self.u_pos,
+                           self.w.rope_theta, q_new=self.q_new, q_out=self.q_u, src_idx=self.u_idx)
+
+    def stage_anchor_gather(self):
+        qcf.qcf_gather_rows(self.k_probe, self.k, self.probe_idx)
+        qcf.qcf_gather_rows(self.v_probe, self.v, self.probe_idx)
+
+    def stage_probe_attn(self):
+        p = self.plan
+        qcf.qcf_sparse_prefill_attn(self.o_probe, self.q_u, self.u_pos, self.cu_q, self.k_probe,
+                                    self.v_probe, self.cu_probe, p.max_q, p.max_probe, self.scale,
+                                    kv_pos=self.probe_pos, workspace=self.ws_attn)
+
+    def stage_scores(self, accumulate=False):
+        p = self.plan
+        qcf.qcf_probe_scores(self.scores, self.q_u, self.k, self.cu_q, self.cu_kv, self.ctx_len,
+                             p.max_q, p.max_ctx, self.scale, accumulate=accumulate,
+                             workspace=self.ws_scores)
+
+    def stage_select(self):
+        p = self.plan
+        qcf.qcf_select_topk(self.R_idx, self.scores, self.seg_start, self.seg_len, self.seg_k,
+                            self.out_start, p.max_seg, out_pos=self.R_pos, pos_base=self.pos_base)
+
+    def stage_scatter(self):
+        qcf.qcf_scatter_kv(self.k, self.v, self.k_new, self.v_new, self.R_idx, self.R_pos,
+                           self.w.rope_theta, q_new=self.q_new, q_out=self.q_R, src_idx=self.R_idx)
+
+    def stage_attn(self):
+        p = self.plan
+        qcf.qcf_sparse_prefill_attn(self.o, self.q_R, self.R_pos, self.cu_R, self.k, self.v,
+                                    self.cu_kv, p.max_R, int(self.w.cu_kv.max() if self.w.batch else 0),
+                                    self.scale, workspace=self.ws_attn)
+
+    STAGES = ("rerope", "query_rows", "anchor_gather", "probe_attn", "scores", "select", "scatter",
+              "attn")
+
+    def run(self):
+        self.stage_rerope()
+        self.stage_query_rows()
+        self.stage_anchor_gather()
+        self.stage_probe_attn()
+        self.stage_scores()
+        self.stage_select()
+        self.stage_scatter()
+        self.stage_attn()
+
+    # -- results on the host ----------------------------------------------------
+    def results(self):
+        torch.cuda.synchronize()
+        c = lambda x: x.float().cpu().numpy().astype(np.float64)
+        p = self.plan
+        R = self.R_idx.cpu().numpy()
+        Rp = self.R_pos.cpu().numpy()
+        P = [R[p.cu_R[b]:p.cu_R[b] + p.n_P[b]] for b in range(self.w.batch)]
+        op = c(self.o_probe)
+        cq = self.w.cu_q
+        return dict(k_fuse=c(self.k), v_fuse=c(self.v), scores=self.scores.double().cpu().numpy(),
+                    R=R, R_pos=Rp, P=P, cu_R=p.cu_R, o=c(self.o), o_probe=op,
+                    o_probe_list=[op[cq[b]:cq[b + 1]] for b in range(self.w.batch)],
+                    q_u=c(self.q_u), q_R=c(self.q_R))

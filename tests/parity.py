@@ -1,0 +1,102 @@
+"""Parity helpers shared by the GPU tests: tolerances and the step comparison.
+
+Tolerances
+  bf16 tensors (attention outputs, K/V): max-abs <= 2e-2 and relative L2 <= 1e-2.
+  fp32 tensors: max-abs <= 1e-4 and relative L2 <= 1e-5 (float32 arithmetic
+    against float64: a few hundred accumulated roundings of 6e-8 each).
+  scores (always float32 on the GPU): |d| <= 1e-4 + 1e-3 * |I|.
+  selection: equal counts per chunk; a row may differ only if the oracle's
+    scores of every swapped pair differ by less than 1e-3 (sum units).
+"""
+import numpy as np
+
+TOL = {"bf16": dict(max_abs=2e-2, rel_l2=1e-2), "f32": dict(max_abs=1e-4, rel_l2=1e-5)}
+GAP = 1e-3
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a - b))
+
+
+def assert_close(got, want, dtype, what):
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    assert got.shape == want.shape, (what, got.shape, want.shape)
+    if got.size == 0:
+        return
+    t = TOL[dtype]
+    mx = float(np.max(np.abs(got - want)))
+    rl = rel_l2(got, want)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite values"
+    assert mx <= t["max_abs"] and rl <= t["rel_l2"], f"{what}: max-abs {mx:.3g}, rel-L2 {rl:.3g}"
+    return mx, rl
+
+
+def assert_scores(got, want, what="scores"):
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    bad = np.abs(got - want) > 1e-4 + 1e-3 * np.abs(want)
+    assert not bad.any(), f"{what}: {bad.sum()} entries off, worst {np.max(np.abs(got - want)):.3g}"
+
+
+def check_selection(w, P_gpu, scores_orc, P_orc):
+    """Per chunk: same count; swapped rows only across near-ties (gap < 1e-3)."""
+    Pg = np.sort(np.concatenate(P_gpu)) if len(P_gpu) else np.zeros(0, int)
+    Po = np.sort(np.concatenate(P_orc)) if len(P_orc) else np.zeros(0, int)
+    swaps = 0
+    for s in range(w.n_chunks):
+        a, n = int(w.seg_start[s]), int(w.seg_len[s])
+        g = Pg[(Pg >= a) & (Pg < a + n)]
+        o = Po[(Po >= a) & (Po < a + n)]
+        assert g.size == o.size, f"chunk {s}: {g.size} selected, oracle {o.size}"
+        assert np.all(np.diff(g) > 0)
+        xg = np.setdiff1d(g, o)
+        xo = np.setdiff1d(o, g)
+        if xg.size:
+            gap = np.abs(scores_orc[xg][:, None] - scores_orc[xo][None, :]).max()
+            assert gap < GAP, f"chunk {s}: swapped rows with score gap {gap:.3g}"
+            swaps += xg.size
+    return swaps
+
+
+def check_step(w, g, o, sampled=False):
+    """Compare a GPU step (``FusionStep.results()``) with the oracle's ``fusion_step``."""
+    dt = w.dtype
+    report = {}
+    # scores of the context rows
+    ctx = np.zeros(w.n_rows, bool)
+    for s in range(w.n_chunks):
+        ctx[w.seg_start[s]:w.seg_start[s] + w.seg_len[s]] = True
+    assert_scores(g["scores"][ctx], o["scores"][ctx])
+    # selection
+    report["swaps"] = check_selection(w, g["P"], o["scores"], o["P"])
+    # R layout: per request, P ascending then the query rows
+    for b in range(w.batch):
+        Rg = g["R"][g["cu_R"][b]:g["cu_R"][b + 1]] if "cu_R" in g else None
+        if Rg is not None:
+            np.testing.assert_array_equal(Rg[len(g["P"][b]):], o["R"][b][len(o["P"][b]):])
+    # fused cache: each row must hold its fresh value if the GPU recomputed it,
+    # else its re-positioned PIC value
+    Rg_all = np.zeros(w.n_rows, bool)
+    Rg_all[g["R"]] = True
+    want_k = np.where(Rg_all[:, None, None], o["fresh_k"], o["k_rerope"])
+    want_v = np.where(Rg_all[:, None, None], np.asarray(w.v_new, np.float64), np.asarray(w.v_pic, np.float64))
+    report["k"] = assert_close(g["k_fuse"], want_k, dt, "fused K")
+    report["v"] = assert_close(g["v_fuse"], want_v, dt, "fused V")
+    np.testing.assert_array_equal(g["v_fuse"][~Rg_all], np.asarray(w.v_pic, np.float64)[~Rg_all])
+    # probe outputs
+    report["o_probe"] = assert_close(np.concatenate(g["o_probe_list"]), np.concatenate(o["o_probe"]), dt,
+                                     "probe output")
+    # attention outputs on every row the oracle evaluated
+    rows = [i for i, r in enumerate(g["R"]) if int(r) in o["o"]]
+    if not sampled:
+        assert len(rows) == len(g["R"]), f"{len(g['R']) - len(rows)} GPU rows without an oracle value"
+    assert rows, "no attention rows to compare"
+    got = g["o"][rows]
+    want = np.stack([o["o"][int(g["R"][i])] for i in rows])
+    report["o"] = assert_close(got, want, dt, "attention output")
+    report["o_rows"] = len(rows)
+    return report

@@ -1,0 +1,120 @@
+"""libqcf loads, exports every entry point that include/qcf.h declares, and
+rejects bad host arguments before launching anything (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_05875_amd import qcf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qcf.h")
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+A = 0x10000          # a fake, 256-byte aligned address (never dereferenced: calls fail validation)
+MIS = 0x10004        # misaligned
+F32, BF16 = 0, 1
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    out = {}
+    for m in re.finditer(r"\b(?:qcf_status|size_t|int|const char\*)\s+(qcf_\w+)\s*\(([^;]*?)\)\s*;", text, re.S):
+        args = m.group(2).strip()
+        out[m.group(1)] = 0 if args in ("", "void") else args.count(",") + 1
+    return out
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(qcf.lib_path()):
+        from paper_2606_05875_amd.build import build
+        build(verbose=False)
+    return qcf.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    decl = _declared()
+    assert set(decl) == {"qcf_version", "qcf_status_string", "qcf_rerope", "qcf_gather_rows",
+                         "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
+                         "qcf_select_topk", "qcf_sparse_prefill_attn_workspace_size",
+                         "qcf_sparse_prefill_attn"}
+    for name, nargs in decl.items():
+        assert hasattr(L, name), name
+        assert name in qcf.EXPORTS
+        assert len(qcf.EXPORTS[name][1]) == nargs, name
+
+
+def test_version_and_status_strings(L):
+    assert L.qcf_version() == 100
+    for code in range(5):
+        assert L.qcf_status_string(code)
+    assert L.qcf_status_string(0) == b"ok"
+
+
+def test_rerope_validation(L):
+    s = None
+    # null tensors with work to do
+    assert L.qcf_rerope(None, None, BF16, 10, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == INVALID
+    # unsupported head_dim, dtype
+    assert L.qcf_rerope(A, A, BF16, 10, 8, 96, 1024, 1, A, A, A, 10, 1e4, s) == UNSUPPORTED
+    assert L.qcf_rerope(A, A, 7, 10, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == UNSUPPORTED
+    # row stride too small / not 16-byte multiple, misaligned base, bad theta
+    assert L.qcf_rerope(A, A, BF16, 10, 8, 128, 512, 1, A, A, A, 10, 1e4, s) == INVALID
+    assert L.qcf_rerope(A, A, BF16, 10, 8, 128, 1028, 1, A, A, A, 10, 1e4, s) == INVALID
+    assert L.qcf_rerope(MIS, A, BF16, 10, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == INVALID
+    assert L.qcf_rerope(A, A, BF16, 10, 8, 128, 1024, 1, A, A, A, 10, 0.0, s) == INVALID
+    assert L.qcf_rerope(A, A, BF16, -1, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == INVALID
+    # nothing to do: OK without touching the device
+    assert L.qcf_rerope(None, None, BF16, 0, 8, 128, 1024, 0, None, None, None, 0, 1e4, s) == OK
+
+
+def test_gather_validation(L):
+    assert L.qcf_gather_rows(A, A, A, 4, 4, 24, 32, 32, None) == INVALID     # row bytes % 16
+    assert L.qcf_gather_rows(A, A, A, 4, 4, 64, 32, 64, None) == INVALID     # row > stride
+    assert L.qcf_gather_rows(None, A, A, 4, 4, 32, 32, 32, None) == INVALID
+    assert L.qcf_gather_rows(None, None, None, 0, 0, 32, 32, 32, None) == OK
+
+
+def test_scatter_validation(L):
+    args = lambda hq, hkv, d, **kw: [kw.get("kc", A), A, 100, kw.get("stride", hkv * d), A, A,
+                                    kw.get("qn", A), kw.get("qo", A), 100, kw.get("src", None), BF16,
+                                    kw.get("n", 5), A, A, hq, hkv, d, 1e4, None]
+    assert L.qcf_scatter_kv(*args(32, 8, 96)) == UNSUPPORTED
+    assert L.qcf_scatter_kv(*args(30, 8, 128)) == INVALID                     # H_q % H_kv
+    assert L.qcf_scatter_kv(*args(24, 8, 128)) == UNSUPPORTED                 # group 3
+    assert L.qcf_scatter_kv(*args(64, 1, 128)) == UNSUPPORTED                 # group 64 > 32
+    assert L.qcf_scatter_kv(*args(32, 8, 128, kc=None)) == INVALID
+    assert L.qcf_scatter_kv(*args(32, 8, 128, qn=None)) == INVALID            # q_out without q_new
+    assert L.qcf_scatter_kv(*args(32, 8, 128, src=A)) == INVALID              # in-place q with src_idx
+    assert L.qcf_scatter_kv(*args(32, 8, 128, stride=8 * 128 + 4)) == INVALID
+    assert L.qcf_scatter_kv(*args(32, 8, 128, n=0, kc=None)) == OK
+
+
+def test_probe_scores_validation_and_workspace(L):
+    need = L.qcf_probe_scores_workspace_size(2, 64, 5120, 32, 8, 128)
+    assert need > 0 and need % 256 == 0
+    assert L.qcf_probe_scores_workspace_size(2, 64, 5120, 32, 8, 96) == 0
+    base = lambda **kw: [A, 0, A, 128, A, 10368, kw.get("stride", 1024), BF16, 2, A, A, A, 64, 5120,
+                         32, 8, kw.get("d", 128), kw.get("scale", 0.088), kw.get("ws", A),
+                         kw.get("wsb", need), None]
+    assert L.qcf_probe_scores(*base(wsb=need - 1)) == WORKSPACE
+    assert L.qcf_probe_scores(*base(ws=None)) == WORKSPACE
+    assert L.qcf_probe_scores(*base(ws=A + 16)) == WORKSPACE                   # not 256-aligned
+    assert L.qcf_probe_scores(*base(d=96)) == UNSUPPORTED
+    assert L.qcf_probe_scores(*base(scale=0.0)) == INVALID
+    assert L.qcf_probe_scores(*base(stride=1000)) == INVALID
+
+
+def test_topk_and_attn_validation(L):
+    assert L.qcf_select_topk(None, None, 10, A, 100, 2, A, A, A, A, None, 64, None) == INVALID
+    assert L.qcf_select_topk(A, None, 10, A, -1, 2, A, A, A, A, None, 64, None) == INVALID
+    assert L.qcf_select_topk(None, None, 0, None, 0, 0, None, None, None, None, None, 0, None) == OK
+    a = lambda **kw: [A, None, A, A, kw.get("n", 10), A, A, A, 100, kw.get("stride", 1024), A, None,
+                      kw.get("dt", BF16), 1, 10, 100, kw.get("hq", 32), 8, 128, 0.088, None, 0, None]
+    assert L.qcf_sparse_prefill_attn(*a(dt=3)) == UNSUPPORTED
+    assert L.qcf_sparse_prefill_attn(*a(hq=36)) == INVALID
+    assert L.qcf_sparse_prefill_attn(*a(stride=1000)) == INVALID
+    assert L.qcf_sparse_prefill_attn(*a(n=-2)) == INVALID
+    assert L.qcf_sparse_prefill_attn_workspace_size(1, 10, 100, 32, 8, 128, BF16) >= 0

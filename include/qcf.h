@@ -61,24 +61,31 @@ int qcf_version(void);
 const char* qcf_status_string(qcf_status status);
 
 /*
- * qcf_rerope -- position remapping Pi_i of the reused chunk keys
- * (Section 2.1.2, eq. pic_online).  A stored chunk key is rotated at its
- * chunk-local position; rotating it once more by the chunk's offset o_i moves
- * it to its request position o_i + r.  Values need no remapping.
- *
- *   k_out, k_in  [n_tokens rows, row_stride] keys; k_out may equal k_in
- *                (in place).  Rows outside every segment are not touched.
- *   seg_start    [n_seg] first row of each segment (a chunk)
- *   seg_len      [n_seg] rows in each segment (<= max_seg_len)
- *   seg_delta    [n_seg] rotation offset of each segment in positions
- *   rope_theta   rotary base
- * Errors: null pointers, n_seg < 0, head_dim/group unsupported, misalignment.
+ * qcf_rerope -- position remapping Pi_i and stitching of the reused chunk
+ * caches into the request cache (Section 2.1.2, eq. pic_online).  A stored
+ * chunk key is rotated at its chunk-local position; rotating it once more by
+ * the chunk's offset o_i moves it to its request position o_i + r.  The
+ * chunk's values are copied in the same token order.  For segment s and row
+ * r < seg_len[s], with src = (src_start ? src_start[s] : seg_start[s]) + r and
+ * dst = seg_start[s] + r:
+ *     k_out[dst] = rope(k_in[src], seg_delta[s])
+ *     v_out[dst] = v_in[src]                       (when v_out != NULL)
+ *   k_out, v_out  [n_out_rows, row_stride]; k_in, v_in [n_in_rows, row_stride]
+ *                 k_out may equal k_in (in place) when src == dst; v_in must be
+ *                 non-NULL iff v_out is, and the V copy is skipped when
+ *                 v_out == v_in.  Rows outside every segment are not touched.
+ *   seg_start     [n_seg] first destination row of each segment (a chunk)
+ *   seg_len       [n_seg] rows in each segment (<= max_seg_len)
+ *   seg_delta     [n_seg] rotation offset of each segment in positions
+ *   src_start     [n_seg] first source row of each segment, or NULL
+ *   rope_theta    rotary base
+ * Errors: null pointers, n_seg > 65535, head_dim unsupported, misalignment.
  */
-qcf_status qcf_rerope(void* k_out, const void* k_in, qcf_dtype dtype,
-                      int64_t n_tokens, int n_kv_heads, int head_dim, int64_t row_stride,
-                      int n_seg, const int32_t* seg_start, const int32_t* seg_len,
-                      const int32_t* seg_delta, int max_seg_len, double rope_theta,
-                      hipStream_t stream);
+qcf_status qcf_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in,
+                      qcf_dtype dtype, int64_t n_out_rows, int64_t n_in_rows, int n_kv_heads,
+                      int head_dim, int64_t row_stride, int n_seg, const int32_t* seg_start,
+                      const int32_t* seg_len, const int32_t* seg_delta, const int32_t* src_start,
+                      int max_seg_len, double rope_theta, hipStream_t stream);
 
 /*
  * qcf_gather_rows -- row copy dst[i] = src[idx[i]] (the anchor cache

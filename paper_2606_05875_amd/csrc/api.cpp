@@ -47,27 +47,34 @@ const char* qcf_status_string(qcf_status s) {
   return "unknown status";
 }
 
-qcf_status qcf_rerope(void* k_out, const void* k_in, qcf_dtype dtype, int64_t n_tokens,
-                      int n_kv_heads, int head_dim, int64_t row_stride, int n_seg,
-                      const int32_t* seg_start, const int32_t* seg_len, const int32_t* seg_delta,
+qcf_status qcf_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in,
+                      qcf_dtype dtype, int64_t n_out_rows, int64_t n_in_rows, int n_kv_heads,
+                      int head_dim, int64_t row_stride, int n_seg, const int32_t* seg_start,
+                      const int32_t* seg_len, const int32_t* seg_delta, const int32_t* src_start,
                       int max_seg_len, double rope_theta, hipStream_t stream) {
   if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
-  if (n_tokens < 0 || n_tokens > INT32_MAX || n_seg < 0 || max_seg_len < 0) return QCF_ERR_INVALID_ARG;
+  if (n_out_rows < 0 || n_out_rows > INT32_MAX || n_in_rows < 0 || n_in_rows > INT32_MAX ||
+      n_seg < 0 || max_seg_len < 0)
+    return QCF_ERR_INVALID_ARG;
   if (n_kv_heads <= 0) return QCF_ERR_INVALID_ARG;
   if (head_dim != 64 && head_dim != 128) return QCF_ERR_UNSUPPORTED;
   if (n_seg > 65535) return QCF_ERR_UNSUPPORTED;
   if (row_stride < (int64_t)n_kv_heads * head_dim || (row_stride * esize(dtype)) % 16 != 0)
     return QCF_ERR_INVALID_ARG;
   if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
-  const bool empty = n_tokens == 0 || n_seg == 0 || max_seg_len == 0;
-  if (!tensor_ok(k_out, empty) || !tensor_ok(k_in, empty)) return QCF_ERR_INVALID_ARG;
+  if ((v_out == nullptr) != (v_in == nullptr)) return QCF_ERR_INVALID_ARG;
+  const bool empty = n_out_rows == 0 || n_in_rows == 0 || n_seg == 0 || max_seg_len == 0;
+  if (!tensor_ok(k_out, empty) || !tensor_ok(k_in, empty) || !tensor_ok(v_out, true) ||
+      !tensor_ok(v_in, true))
+    return QCF_ERR_INVALID_ARG;
   if (!index_ok(seg_start, n_seg == 0) || !index_ok(seg_len, n_seg == 0) ||
-      !index_ok(seg_delta, n_seg == 0))
+      !index_ok(seg_delta, n_seg == 0) || (src_start && !index_ok(src_start, false)))
     return QCF_ERR_INVALID_ARG;
   if (empty) return QCF_OK;
-  return hip_status(qcf::launch_rerope(k_out, k_in, dtype == QCF_BF16, n_tokens, n_kv_heads,
-                                       head_dim, row_stride, n_seg, seg_start, seg_len, seg_delta,
-                                       max_seg_len, rope_theta, stream));
+  return hip_status(qcf::launch_rerope(k_out, k_in, v_out, v_in, dtype == QCF_BF16, n_out_rows,
+                                       n_in_rows, n_kv_heads, head_dim, row_stride, n_seg,
+                                       seg_start, seg_len, seg_delta, src_start, max_seg_len,
+                                       rope_theta, stream));
 }
 
 qcf_status qcf_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,

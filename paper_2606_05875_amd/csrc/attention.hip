@@ -40,7 +40,7 @@ __device__ __forceinline__ int vt_slot(int key) {
   return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
 }
 
-template <int D>
+template <int D, bool kPos>
 __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, const uint16_t* __restrict__ q,
     const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
@@ -80,8 +80,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   if (l == 0) red[w] = wmax;
   __syncthreads();
   const int bmax = max(max(red[0], red[1]), max(red[2], red[3]));
-  const int kv_end = kv_pos ? nkv : min(nkv, bmax + 1);
-  const int wave_end = kv_pos ? nkv : min(nkv, wmax + 1);
+  const int kv_end = kPos ? nkv : min(nkv, bmax + 1);
+  const int wave_end = kPos ? nkv : min(nkv, wmax + 1);
 
   bf16x8 qreg[D / 16];
   {
@@ -115,7 +115,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
         vbuf[e] = j < nkv ? ld16(vbase + (int64_t)j * kv_stride + ch * 8) : make_uint4(0, 0, 0, 0);
       }
     }
-    if (kv_pos && threadIdx.x < kKT) {
+    if (kPos && threadIdx.x < kKT) {
       const int j = kt0 + threadIdx.x;
       kpos_reg = j < nkv ? kv_pos[kv0 + j] : INT_MAX;
     }
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
             make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
       }
     }
-    if (kv_pos && threadIdx.x < kKT) kpos_lds[threadIdx.x] = kpos_reg;
+    if (kPos && threadIdx.x < kKT) kpos_lds[threadIdx.x] = kpos_reg;
   };
 
   if (kv_end > 0) {
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
           s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], s[blk], 0, 0, 0);
         }
       }
-      const bool need_mask = kv_pos != nullptr || kt0 + kKT > wmin || kt0 + kKT > nkv;
+      const bool need_mask = kPos || kt0 + kKT > wmin || kt0 + kKT > nkv;
       float mt = -INFINITY;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
           if (need_mask) {
             const int jt = blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
             const int j = kt0 + jt;
-            const int kp = kv_pos ? kpos_lds[jt] : j;
+            const int kp = kPos ? kpos_lds[jt] : j;
             if (j >= nkv || kp > qpos) x = -INFINITY;
           }
           s[blk][v] = x;
@@ -299,12 +299,16 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
   if (bf16) {
     const int rpb = 128 >> lg;
     dim3 grid((s.max_rows + rpb - 1) / rpb, s.hkv, s.batch);
-#define QCF_ATTN(D)                                                                               \
-  attn_bf16_kernel<D><<<grid, kThreads, 0, stream>>>(                                             \
+#define QCF_ATTN(D, P)                                                                            \
+  attn_bf16_kernel<D, P><<<grid, kThreads, 0, stream>>>(                                          \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
       kv_row_stride, cu_kv, kv_pos, s.hq, lg, scale2)
-    if (s.d == 64) QCF_ATTN(64); else QCF_ATTN(128);
+    if (kv_pos) {
+      if (s.d == 64) QCF_ATTN(64, true); else QCF_ATTN(128, true);
+    } else {
+      if (s.d == 64) QCF_ATTN(64, false); else QCF_ATTN(128, false);
+    }
 #undef QCF_ATTN
     return hipGetLastError();
   }

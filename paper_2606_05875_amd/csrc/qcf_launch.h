@@ -8,10 +8,12 @@
 
 namespace qcf {
 
-hipError_t launch_rerope(void* k_out, const void* k_in, bool bf16, int64_t n_tokens, int hkv,
-                         int d, int64_t row_stride, int n_seg, const int32_t* seg_start,
-                         const int32_t* seg_len, const int32_t* seg_delta, int max_seg_len,
-                         double theta, hipStream_t stream);
+hipError_t launch_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in, bool bf16,
+                         int64_t n_out_rows, int64_t n_in_rows, int hkv, int d,
+                         int64_t row_stride, int n_seg, const int32_t* seg_start,
+                         const int32_t* seg_len, const int32_t* seg_delta,
+                         const int32_t* src_start, int max_seg_len, double theta,
+                         hipStream_t stream);
 
 hipError_t launch_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
                               int64_t n_src_rows, int64_t row_bytes, int64_t src_stride,

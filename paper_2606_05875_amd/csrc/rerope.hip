@@ -1,12 +1,14 @@
-// Position remapping of the reused chunk keys (Section 2.1.2, eq. pic_online).
+// Position remapping and stitching of the reused chunk caches (Section 2.1.2,
+// eq. pic_online).
 //
 // A stored chunk key is rotated at its chunk-local position; moving the chunk
-// to request offset o_i is one more rotation by o_i.  The rotation is the same
-// for every row of a chunk, so a block works inside one chunk: its first
-// threads form the chunk's d/2 (cos, sin) pairs once (float64 angle), and every
-// thread then streams 16-byte vectors of the rotate-half pairs (j .. j+v,
-// j+d/2 .. j+d/2+v) of one head of one row.  HBM-bound: every key byte is read
-// once and written once with coalesced 16-byte accesses.
+// to request offset o_i is one more rotation by o_i, and its values are copied
+// in the same token order.  The rotation is the same for every row of a chunk,
+// so a block works inside one chunk: its first threads form the chunk's d/2
+// (cos, sin) pairs once (float64 angle), and every thread then streams 16-byte
+// vectors of the rotate-half pairs (j .. j+v, j+d/2 .. j+d/2+v) of one head of
+// one row, then 16-byte vectors of the value rows.  HBM-bound: every byte is
+// read once and written once with coalesced 16-byte accesses.
 #include "qcf_device.h"
 #include "qcf_launch.h"
 
@@ -17,23 +19,22 @@ constexpr int kThreads = 256;
 constexpr int kUnitsPerThread = 4;  // (row, head, j-vector) units each thread owns
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void rerope_kernel(T* out, const T* in,
-                                                          int64_t n_tokens, int hkv,
-                                                          int64_t row_stride, int rows_per_block,
-                                                          const int32_t* __restrict__ seg_start,
-                                                          const int32_t* __restrict__ seg_len,
-                                                          const int32_t* __restrict__ seg_delta,
-                                                          double theta) {
+__global__ __launch_bounds__(kThreads) void rerope_kernel(
+    T* k_out, const T* k_in, T* v_out, const T* v_in, int64_t n_out_rows, int64_t n_in_rows,
+    int hkv, int64_t row_stride, int rows_per_block, const int32_t* __restrict__ seg_start,
+    const int32_t* __restrict__ seg_len, const int32_t* __restrict__ seg_delta,
+    const int32_t* __restrict__ src_start, double theta) {
   constexpr int HALF = D / 2;
   constexpr int VEC = Vec16<T>::N;
-  constexpr int UPH = HALF / VEC;  // units per head
+  constexpr int UPH = HALF / VEC;  // key units per head
   __shared__ float2 cs[HALF];
 
   const int s = blockIdx.y;
   const int len = seg_len[s];
   const int r0 = blockIdx.x * rows_per_block;
   if (r0 >= len) return;
-  const int64_t start = seg_start[s];
+  const int64_t dst0 = (int64_t)seg_start[s] + r0;
+  const int64_t src0 = (src_start ? (int64_t)src_start[s] : (int64_t)seg_start[s]) + r0;
   if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)seg_delta[s], threadIdx.x, D, theta);
   __syncthreads();
 
@@ -42,33 +43,35 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(T* out, const T* in,
   const int total = rows * units_per_row;
 
   // Loads of all owned units are issued before any store: in-place calls
-  // (out == in) stay correct because every unit is read and written by the
-  // same thread.
+  // (k_out == k_in, src == dst) stay correct because every unit is read and
+  // written by the same thread.
   for (int base = 0; base < total; base += kThreads * kUnitsPerThread) {
     uint4 lo[kUnitsPerThread], hi[kUnitsPerThread];
-    int64_t off[kUnitsPerThread];
+    int64_t off_in[kUnitsPerThread], off_out[kUnitsPerThread];
     int jj[kUnitsPerThread];
 #pragma unroll
     for (int k = 0; k < kUnitsPerThread; ++k) {
       const int u = base + threadIdx.x + k * kThreads;
-      off[k] = -1;
+      off_in[k] = -1;
       jj[k] = 0;
       if (u < total) {
         const int rr = u / units_per_row;
         const int c = u - rr * units_per_row;
         const int h = c / UPH;
         jj[k] = (c - h * UPH) * VEC;
-        const int64_t row = start + r0 + rr;
-        if (row >= 0 && row < n_tokens) {
-          off[k] = row * row_stride + (int64_t)h * D + jj[k];
-          lo[k] = ld16(in + off[k]);
-          hi[k] = ld16(in + off[k] + HALF);
+        const int64_t src = src0 + rr, dst = dst0 + rr;
+        if (src >= 0 && src < n_in_rows && dst >= 0 && dst < n_out_rows) {
+          const int64_t in_head = (int64_t)h * D + jj[k];
+          off_in[k] = src * row_stride + in_head;
+          off_out[k] = dst * row_stride + in_head;
+          lo[k] = ld16(k_in + off_in[k]);
+          hi[k] = ld16(k_in + off_in[k] + HALF);
         }
       }
     }
 #pragma unroll
     for (int k = 0; k < kUnitsPerThread; ++k) {
-      if (off[k] < 0) continue;
+      if (off_in[k] < 0) continue;
       float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
       Vec16<T>::unpack(lo[k], x1);
       Vec16<T>::unpack(hi[k], x2);
@@ -78,44 +81,72 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(T* out, const T* in,
         y1[e] = x1[e] * r.x - x2[e] * r.y;
         y2[e] = x1[e] * r.y + x2[e] * r.x;
       }
-      st16(out + off[k], Vec16<T>::pack(y1));
-      st16(out + off[k] + HALF, Vec16<T>::pack(y2));
+      st16(k_out + off_out[k], Vec16<T>::pack(y1));
+      st16(k_out + off_out[k] + HALF, Vec16<T>::pack(y2));
     }
+  }
+  // values: stitched unchanged, in the same token order
+  if (v_out == nullptr || v_out == v_in) return;
+  const int vchunks = hkv * D / VEC;
+  const int vtotal = rows * vchunks;
+  for (int base = 0; base < vtotal; base += kThreads * kUnitsPerThread) {
+    uint4 buf[kUnitsPerThread];
+    int64_t oi[kUnitsPerThread], oo[kUnitsPerThread];
+#pragma unroll
+    for (int k = 0; k < kUnitsPerThread; ++k) {
+      const int u = base + threadIdx.x + k * kThreads;
+      oi[k] = -1;
+      if (u < vtotal) {
+        const int rr = u / vchunks;
+        const int c = u - rr * vchunks;
+        const int64_t src = src0 + rr, dst = dst0 + rr;
+        if (src >= 0 && src < n_in_rows && dst >= 0 && dst < n_out_rows) {
+          oi[k] = src * row_stride + (int64_t)c * VEC;
+          oo[k] = dst * row_stride + (int64_t)c * VEC;
+          buf[k] = ld16(v_in + oi[k]);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnitsPerThread; ++k)
+      if (oi[k] >= 0) st16(v_out + oo[k], buf[k]);
   }
 }
 
 template <typename T, int D>
-hipError_t launch_t(void* k_out, const void* k_in, int64_t n_tokens, int hkv, int64_t row_stride,
-                    int n_seg, const int32_t* seg_start, const int32_t* seg_len,
-                    const int32_t* seg_delta, int max_seg_len, double theta, hipStream_t stream) {
+hipError_t launch_t(void* k_out, const void* k_in, void* v_out, const void* v_in,
+                    int64_t n_out_rows, int64_t n_in_rows, int hkv, int64_t row_stride, int n_seg,
+                    const int32_t* seg_start, const int32_t* seg_len, const int32_t* seg_delta,
+                    const int32_t* src_start, int max_seg_len, double theta, hipStream_t stream) {
   const int units_per_row = hkv * (D / 2) / Vec16<T>::N;
   const int rpb = max(1, kThreads * kUnitsPerThread / units_per_row);
   dim3 grid((max_seg_len + rpb - 1) / rpb, n_seg);
   rerope_kernel<T, D><<<grid, kThreads, 0, stream>>>(
-      static_cast<T*>(k_out), static_cast<const T*>(k_in), n_tokens, hkv, row_stride, rpb,
-      seg_start, seg_len, seg_delta, theta);
+      static_cast<T*>(k_out), static_cast<const T*>(k_in), static_cast<T*>(v_out),
+      static_cast<const T*>(v_in), n_out_rows, n_in_rows, hkv, row_stride, rpb, seg_start,
+      seg_len, seg_delta, src_start, theta);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_rerope(void* k_out, const void* k_in, bool bf16, int64_t n_tokens, int hkv,
-                         int d, int64_t row_stride, int n_seg, const int32_t* seg_start,
-                         const int32_t* seg_len, const int32_t* seg_delta, int max_seg_len,
-                         double theta, hipStream_t stream) {
-  if (n_seg == 0 || max_seg_len == 0 || n_tokens == 0) return hipSuccess;
+hipError_t launch_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in, bool bf16,
+                         int64_t n_out_rows, int64_t n_in_rows, int hkv, int d,
+                         int64_t row_stride, int n_seg, const int32_t* seg_start,
+                         const int32_t* seg_len, const int32_t* seg_delta,
+                         const int32_t* src_start, int max_seg_len, double theta,
+                         hipStream_t stream) {
+  if (n_seg == 0 || max_seg_len == 0 || n_out_rows == 0 || n_in_rows == 0) return hipSuccess;
+#define QCF_REROPE(T, D)                                                                       \
+  return launch_t<T, D>(k_out, k_in, v_out, v_in, n_out_rows, n_in_rows, hkv, row_stride, n_seg, \
+                        seg_start, seg_len, seg_delta, src_start, max_seg_len, theta, stream)
   if (bf16) {
-    return d == 64 ? launch_t<uint16_t, 64>(k_out, k_in, n_tokens, hkv, row_stride, n_seg,
-                                            seg_start, seg_len, seg_delta, max_seg_len, theta,
-                                            stream)
-                   : launch_t<uint16_t, 128>(k_out, k_in, n_tokens, hkv, row_stride, n_seg,
-                                             seg_start, seg_len, seg_delta, max_seg_len, theta,
-                                             stream);
+    if (d == 64) QCF_REROPE(uint16_t, 64);
+    QCF_REROPE(uint16_t, 128);
   }
-  return d == 64 ? launch_t<float, 64>(k_out, k_in, n_tokens, hkv, row_stride, n_seg, seg_start,
-                                       seg_len, seg_delta, max_seg_len, theta, stream)
-                 : launch_t<float, 128>(k_out, k_in, n_tokens, hkv, row_stride, n_seg, seg_start,
-                                        seg_len, seg_delta, max_seg_len, theta, stream);
+  if (d == 64) QCF_REROPE(float, 64);
+  QCF_REROPE(float, 128);
+#undef QCF_REROPE
 }
 
 }  // namespace qcf

@@ -32,7 +32,8 @@ _SZ = ctypes.c_size_t
 EXPORTS = {
     "qcf_version": (_I, []),
     "qcf_status_string": (ctypes.c_char_p, [_I]),
-    "qcf_rerope": (_I, [_P, _P, _I, _I64, _I, _I, _I64, _I, _P, _P, _P, _I, ctypes.c_double, _P]),
+    "qcf_rerope": (_I, [_P, _P, _P, _P, _I, _I64, _I64, _I, _I, _I64, _I, _P, _P, _P, _P, _I,
+                        ctypes.c_double, _P]),
     "qcf_gather_rows": (_I, [_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _P]),
     "qcf_scatter_kv": (_I, [_P, _P, _I64, _I64, _P, _P, _P, _P, _I64, _P, _I, _I64, _P, _P, _I, _I,
                             _I, ctypes.c_double, _P]),
@@ -120,17 +121,27 @@ def qcf_status_string(status: int) -> str:
     return lib().qcf_status_string(status).decode()
 
 
-def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_theta):
-    """Rotate each segment's keys by its offset; k_out may be k_in.  Shapes [T, H_kv, d]."""
+def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_theta, v_out=None,
+               v_in=None, src_start=None):
+    """Remap each segment's keys by its offset (and stitch its values); shapes [T, H_kv, d]."""
     _dev(k_out, "k_out", k_in.dtype)
     _dev(k_in, "k_in")
-    for n, t in (("seg_start", seg_start), ("seg_len", seg_len), ("seg_delta", seg_delta)):
+    _dev(v_out, "v_out", k_in.dtype)
+    _dev(v_in, "v_in", k_in.dtype)
+    for n, t in (("seg_start", seg_start), ("seg_len", seg_len), ("seg_delta", seg_delta),
+                 ("src_start", src_start)):
         _i32(t, n)
-    if k_out.shape != k_in.shape or k_out.stride(0) != k_in.stride(0):
-        raise QcfError("k_out and k_in must have the same shape and row stride")
-    T, H, d = k_in.shape
-    st = lib().qcf_rerope(_ptr(k_out), _ptr(k_in), _dtype(k_in), T, H, d, _rows(k_in, "k_in"),
-                          seg_start.numel(), _ptr(seg_start), _ptr(seg_len), _ptr(seg_delta),
+    if k_out.shape[1:] != k_in.shape[1:] or k_out.stride(0) != k_in.stride(0):
+        raise QcfError("k_out and k_in must have the same row shape and row stride")
+    if (v_out is None) != (v_in is None):
+        raise QcfError("v_out and v_in go together")
+    if v_out is not None and (v_out.shape != k_out.shape or v_in.shape != k_in.shape
+                              or v_out.stride(0) != k_out.stride(0) or v_in.stride(0) != k_in.stride(0)):
+        raise QcfError("v_out/v_in must match k_out/k_in")
+    T_in, H, d = k_in.shape
+    st = lib().qcf_rerope(_ptr(k_out), _ptr(k_in), _ptr(v_out), _ptr(v_in), _dtype(k_in),
+                          k_out.shape[0], T_in, H, d, _rows(k_in, "k_in"), seg_start.numel(),
+                          _ptr(seg_start), _ptr(seg_len), _ptr(seg_delta), _ptr(src_start),
                           int(max_seg_len), float(rope_theta), _stream())
     _check(st, "qcf_rerope")
 

@@ -10,7 +10,8 @@ synchronisation inside the step.
 
 Sequence of one step (Section 3.5, selective token localization followed by
 one layer of cache fusion):
-  1. qcf_rerope          stored chunk keys -> request positions (eq. pic_online)
+  1. qcf_rerope          stored chunk caches -> request cache: keys re-positioned,
+                         values stitched (eq. pic_online)
   2. qcf_scatter_kv      user-query rows: rotate q/k at N+i, write K/V into the cache
   3. qcf_gather_rows x2  anchor cache [KV^A ; query K/V] (eq. anchor_cache)
   4. qcf_sparse_prefill_attn  query probe over the anchor cache (eq. anchor_query_state)
@@ -104,9 +105,9 @@ class FusionStep:
     """Device buffers and the call chain of one layer's fusion step for workload ``w``.
 
     ``run()`` enqueues the eight stages on the current stream.  The stored
-    chunk keys (``k_pic``) are never modified (re-positioning writes the
-    working cache ``k``), so ``run()`` can be repeated; the working value cache
-    ``v`` starts as the stored values and receives the recomputed rows.
+    chunk caches (``k_pic``, ``v_pic``) are never modified: re-positioning
+    writes the request cache (``k``, ``v``), which then receives the recomputed
+    rows, so ``run()`` can be repeated with identical results.
     """
 
     def __init__(self, w, rho_bp: int | None = None, device="cuda"):
@@ -137,7 +138,7 @@ class FusionStep:
         self.R_idx_init, self.R_pos_init = t(p.R_idx_init), t(p.R_pos_init)
         # working state and outputs
         self.k = torch.zeros_like(self.k_pic)
-        self.v = self.v_pic.clone()
+        self.v = torch.zeros_like(self.v_pic)
         self.R_idx = self.R_idx_init.clone()
         self.R_pos = self.R_pos_init.clone()
         nU, nR, nP = p.u_idx.size, p.R_idx_init.size, p.probe_idx.size
@@ -159,7 +160,7 @@ class FusionStep:
     def stage_rerope(self):
         w, p = self.w, self.plan
         qcf.qcf_rerope(self.k, self.k_pic, self.seg_start, self.seg_len, self.seg_delta, p.max_seg,
-                       w.rope_theta)
+                       w.rope_theta, v_out=self.v, v_in=self.v_pic)
 
     def stage_query_rows(self):
         qcf.qcf_scatter_kv(self.k, self.v, self.k_new, self.v_new, self.u_idx, self.u_pos,

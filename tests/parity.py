@@ -35,6 +35,18 @@ def assert_close(got, want, dtype, what):
     return mx, rl
 
 
+def assert_ulp(got, want, dtype, what, rel_slack=2.0 ** -20):
+    """Each element within one storage-dtype step of the correctly rounded value
+    (plus a float32 cancellation slack relative to the tensor's largest value)."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    bits = 8 if dtype == "bf16" else 24
+    step = np.ldexp(1.0, np.frexp(np.abs(want))[1] - bits)
+    slack = rel_slack * float(np.max(np.abs(want))) if want.size else 0.0
+    bad = np.abs(got - want) > np.maximum(step * 1.0001, slack)
+    assert not bad.any(), f"{what}: {bad.sum()} elements more than one step off"
+
+
 def assert_scores(got, want, what="scores"):
     got = np.asarray(got, np.float64)
     want = np.asarray(want, np.float64)
@@ -85,6 +97,7 @@ def check_step(w, g, o, sampled=False):
     want_k = np.where(Rg_all[:, None, None], o["fresh_k"], o["k_rerope"])
     want_v = np.where(Rg_all[:, None, None], np.asarray(w.v_new, np.float64), np.asarray(w.v_pic, np.float64))
     report["k"] = assert_close(g["k_fuse"], want_k, dt, "fused K")
+    assert_ulp(g["k_fuse"], want_k, dt, "fused K")
     report["v"] = assert_close(g["v_fuse"], want_v, dt, "fused V")
     np.testing.assert_array_equal(g["v_fuse"][~Rg_all], np.asarray(w.v_pic, np.float64)[~Rg_all])
     # probe outputs

@@ -55,19 +55,22 @@ def test_version_and_status_strings(L):
 
 def test_rerope_validation(L):
     s = None
-    # null tensors with work to do
-    assert L.qcf_rerope(None, None, BF16, 10, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == INVALID
-    # unsupported head_dim, dtype
-    assert L.qcf_rerope(A, A, BF16, 10, 8, 96, 1024, 1, A, A, A, 10, 1e4, s) == UNSUPPORTED
-    assert L.qcf_rerope(A, A, 7, 10, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == UNSUPPORTED
-    # row stride too small / not 16-byte multiple, misaligned base, bad theta
-    assert L.qcf_rerope(A, A, BF16, 10, 8, 128, 512, 1, A, A, A, 10, 1e4, s) == INVALID
-    assert L.qcf_rerope(A, A, BF16, 10, 8, 128, 1028, 1, A, A, A, 10, 1e4, s) == INVALID
-    assert L.qcf_rerope(MIS, A, BF16, 10, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == INVALID
-    assert L.qcf_rerope(A, A, BF16, 10, 8, 128, 1024, 1, A, A, A, 10, 0.0, s) == INVALID
-    assert L.qcf_rerope(A, A, BF16, -1, 8, 128, 1024, 1, A, A, A, 10, 1e4, s) == INVALID
+    r = lambda ko=A, ki=A, vo=None, vi=None, dt=BF16, n=10, d=128, stride=1024, theta=1e4, nseg=1: \
+        L.qcf_rerope(ko, ki, vo, vi, dt, n, n, 8, d, stride, nseg, A, A, A, None, 10, theta, s)
+    assert r(ko=None, ki=None) == INVALID                 # null tensors with work to do
+    assert r(d=96) == UNSUPPORTED
+    assert r(dt=7) == UNSUPPORTED
+    assert r(stride=512) == INVALID                       # row stride below H_kv * d
+    assert r(stride=1028) == INVALID                      # not a 16-byte multiple
+    assert r(ko=MIS) == INVALID                           # misaligned base
+    assert r(theta=0.0) == INVALID
+    assert r(n=-1) == INVALID
+    assert r(vo=A) == INVALID                             # v_out without v_in
+    assert r(vo=A, vi=MIS) == INVALID
+    assert r(nseg=70000) == UNSUPPORTED
     # nothing to do: OK without touching the device
-    assert L.qcf_rerope(None, None, BF16, 0, 8, 128, 1024, 0, None, None, None, 0, 1e4, s) == OK
+    assert L.qcf_rerope(None, None, None, None, BF16, 0, 0, 8, 128, 1024, 0, None, None, None, None,
+                        0, 1e4, s) == OK
 
 
 def test_gather_validation(L):

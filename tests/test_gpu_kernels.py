@@ -14,7 +14,7 @@ import oracle
 from oracle import qcfuse as Q
 from paper_2606_05875_amd import qcf
 from paper_2606_05875_amd.workloads import round_to_bf16
-from parity import assert_close, assert_scores
+from parity import assert_close, assert_scores, assert_ulp
 
 pytestmark = pytest.mark.gpu
 DT = {"bf16": torch.bfloat16, "f32": torch.float32}
@@ -48,24 +48,53 @@ def test_rerope(dtype, hkv, d):
     T = int(starts[-1] + lens[-1] + 5)
     delta = np.array([0, 513, 514, 551, 31000])
     k = draw(rng, (T, hkv, d), dtype)
-    kt = dev(k, DT[dtype])
+    v = draw(rng, (T, hkv, d), dtype)
+    kt, vt = dev(k, DT[dtype]), dev(v, DT[dtype])
     out = torch.full_like(kt, 7.0)
-    qcf.qcf_rerope(out, kt, dev(starts.astype(np.int32)), dev(lens.astype(np.int32)),
-                   dev(delta.astype(np.int32)), int(lens.max()), 5e5)
+    vout = torch.full_like(vt, 7.0)
+    i32 = lambda a: dev(np.asarray(a, np.int32))
+    qcf.qcf_rerope(out, kt, i32(starts), i32(lens), i32(delta), int(lens.max()), 5e5, v_out=vout, v_in=vt)
     want = Q.rerope(k, starts, lens, delta, 5e5, dtype)
     inside = np.zeros(T, bool)
     for a, n in zip(starts, lens):
         inside[a:a + n] = True
     got = host(out)
     assert_close(got[inside], want[inside], dtype, "rerope")
+    assert_ulp(got[inside], want[inside], dtype, "rerope")
     assert np.all(got[~inside] == 7.0)                                # untouched rows
-    if dtype == "bf16":   # at most one bf16 step from the correctly rounded value
-        ulp = np.ldexp(1.0, np.frexp(np.abs(want[inside]) + 1e-38)[1] - 8)
-        assert np.all(np.abs(got[inside] - want[inside]) <= ulp * 1.0001)
+    np.testing.assert_array_equal(host(vout)[inside], v[inside])     # values stitched unchanged
+    assert np.all(host(vout)[~inside] == 7.0)
     # in place gives the same bits
-    qcf.qcf_rerope(kt, kt, dev(starts.astype(np.int32)), dev(lens.astype(np.int32)),
-                   dev(delta.astype(np.int32)), int(lens.max()), 5e5)
-    assert torch.equal(kt[torch.from_numpy(inside).cuda()], out[torch.from_numpy(inside).cuda()])
+    qcf.qcf_rerope(kt, kt, i32(starts), i32(lens), i32(delta), int(lens.max()), 5e5)
+    m = torch.from_numpy(inside).cuda()
+    assert torch.equal(kt[m], out[m])
+
+
+def test_rerope_from_chunk_store():
+    # chunks stored in a separate pool, in another order; stitched into the request cache
+    say("rerope chunk store")
+    rng = np.random.default_rng(11)
+    hkv, d = 8, 128
+    store_lens = np.array([300, 512, 77, 512])
+    store_start = np.concatenate([[0], np.cumsum(store_lens)[:-1]])
+    pool_k = draw(rng, (int(store_lens.sum()), hkv, d), "bf16")
+    pool_v = draw(rng, (int(store_lens.sum()), hkv, d), "bf16")
+    order = np.array([3, 0, 2])                                       # request = chunks 3, 0, 2
+    lens = store_lens[order]
+    seg_start = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    T = int(lens.sum()) + 16                                          # + query slots
+    i32 = lambda a: dev(np.asarray(a, np.int32))
+    ko = torch.zeros((T, hkv, d), dtype=torch.bfloat16, device="cuda")
+    vo = torch.zeros_like(ko)
+    qcf.qcf_rerope(ko, dev(pool_k, torch.bfloat16), i32(seg_start), i32(lens), i32(seg_start), 512, 5e5,
+                   v_out=vo, v_in=dev(pool_v, torch.bfloat16), src_start=i32(store_start[order]))
+    gk, gv = host(ko), host(vo)
+    for s_, c in enumerate(order):
+        a, n, src = int(seg_start[s_]), int(lens[s_]), int(store_start[c])
+        want = Q.rerope(pool_k[src:src + n], [0], [n], [a], 5e5, "bf16")
+        assert_ulp(gk[a:a + n], want, "bf16", f"chunk {c}")
+        np.testing.assert_array_equal(gv[a:a + n], pool_v[src:src + n])
+    assert np.all(gk[-16:] == 0)
 
 
 def test_gather_rows_exact():
@@ -100,7 +129,8 @@ def test_scatter_kv(dtype, hq, hkv, d):
     wk = Q.round_storage(Q.rope(kn[src], pos, 1e6), dtype)
     wq = Q.round_storage(Q.rope(qn[src], pos, 1e6), dtype)
     assert_close(gk[rows], wk, dtype, "scattered K")
-    assert_close(host(qo), wq, dtype, "rotated Q")
+    assert_ulp(gk[rows], wk, dtype, "scattered K")
+    assert_ulp(host(qo), wq, dtype, "rotated Q")        # |q| ~ 10: an absolute bound does not apply
     np.testing.assert_array_equal(gv[rows], vn[src])
     keep = np.setdiff1d(np.arange(T), rows)
     np.testing.assert_array_equal(gk[keep], kc[keep])

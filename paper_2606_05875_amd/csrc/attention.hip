@@ -46,18 +46,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
     const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, const int32_t* __restrict__ kv_pos,
-    int hq, int lg, float scale2) {
+    int batch, int max_tiles, int hkv, int hq, int lg, float scale2) {
   constexpr int KSTR = D + 8;    // K tile row (bf16 elements), 16-byte pad
   constexpr int VSTR = kKT + 8;  // V^T tile row (bf16 elements), 16-byte pad
   constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
   constexpr int KPT = kKT * CPR / kThreads;  // K chunks per thread per tile
   constexpr int VTASKS = (kKT / 4) * CPR;    // (4-key group, chunk) tasks per tile
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKT * KSTR];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[D * VSTR];
-  __shared__ int kpos_lds[kKT];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKT * KSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][D * VSTR];
+  __shared__ int kpos_lds[2][kPos ? kKT : 1];
   __shared__ int red[4];
 
-  const int tile = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  // Block order: consecutive block ids land on consecutive XCDs, so all
+  // blocks of one KV head share an XCD (and its L2); the tiles with the
+  // most keys (the last rows of each request) are dispatched first.
+  const int L = blockIdx.x;
+  const int g = L % hkv;
+  const int rest = L / hkv;
+  const int b = rest % batch;
+  const int tile = max_tiles - 1 - rest / batch;
   const int G = 1 << lg;
   const int rpb = 128 >> lg;
   const int64_t r0 = cu_rows[b];
@@ -93,26 +100,32 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   f32x16 o[D / 32];
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
-  float m = -INFINITY, ls = 0.f;
+  // running max in log2 units; padding lanes start at +inf so they never
+  // trigger a rescale and produce p = 0
+  float m = valid ? -INFINITY : INFINITY;
+  float ls = 0.f;
 
+  // Loads are clamped to the last key, so they never branch; keys past the
+  // end are masked out of the softmax.
   uint4 kbuf[KPT], vbuf[4];
   int kpos_reg = 0;
   const uint16_t* kbase = kc + kv0 * kv_stride + (int64_t)g * D;
   const uint16_t* vbase = vc + kv0 * kv_stride + (int64_t)g * D;
+  const int jmax = max(nkv - 1, 0);
   auto gload = [&](int kt0) {
 #pragma unroll
     for (int c = 0; c < KPT; ++c) {
       const int idx = threadIdx.x + c * kThreads;
       const int key = idx / CPR, ch = idx - key * CPR;
-      const int j = kt0 + key;
-      kbuf[c] = j < nkv ? ld16(kbase + (int64_t)j * kv_stride + ch * 8) : make_uint4(0, 0, 0, 0);
+      const int j = min(kt0 + key, jmax);
+      kbuf[c] = ld16(kbase + (int64_t)j * kv_stride + ch * 8);
     }
     if (threadIdx.x < VTASKS) {
       const int grp = threadIdx.x / CPR, ch = threadIdx.x - grp * CPR;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int j = kt0 + 4 * grp + e;
-        vbuf[e] = j < nkv ? ld16(vbase + (int64_t)j * kv_stride + ch * 8) : make_uint4(0, 0, 0, 0);
+        const int j = min(kt0 + 4 * grp + e, jmax);
+        vbuf[e] = ld16(vbase + (int64_t)j * kv_stride + ch * 8);
       }
     }
     if (kPos && threadIdx.x < kKT) {
@@ -120,16 +133,19 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
       kpos_reg = j < nkv ? kv_pos[kv0 + j] : INT_MAX;
     }
   };
-  auto lstore = [&]() {
+  // V^T rows are XOR-swizzled in 16-byte chunks by (row / 8) so the transposing
+  // 8-byte stores of a wave spread over all banks; reads stay conflict-free.
+  auto lstore = [&](int bf) {
 #pragma unroll
     for (int c = 0; c < KPT; ++c) {
       const int idx = threadIdx.x + c * kThreads;
       const int key = idx / CPR, ch = idx - key * CPR;
-      st16(&k_lds[key * KSTR + ch * 8], kbuf[c]);
+      st16(&k_lds[bf][key * KSTR + ch * 8], kbuf[c]);
     }
     if (threadIdx.x < VTASKS) {
       const int grp = threadIdx.x / CPR, ch = threadIdx.x - grp * CPR;
       const int slot = (4 * grp & ~15) + vt_slot(4 * grp & 15);
+      const int col = (((slot >> 3) ^ (ch & 7)) << 3) + (slot & 7);
       const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vbuf[0]);
       const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vbuf[1]);
       const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vbuf[2]);
@@ -139,78 +155,99 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
         const int sh = (dd & 1) * 16;
         const uint32_t a0 = (w0[dd >> 1] >> sh) & 0xffffu, a1 = (w1[dd >> 1] >> sh) & 0xffffu;
         const uint32_t a2 = (w2[dd >> 1] >> sh) & 0xffffu, a3 = (w3[dd >> 1] >> sh) & 0xffffu;
-        *reinterpret_cast<uint2*>(&v_lds[(ch * 8 + dd) * VSTR + slot]) =
+        *reinterpret_cast<uint2*>(&v_lds[bf][(ch * 8 + dd) * VSTR + col]) =
             make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
       }
     }
-    if (kPos && threadIdx.x < kKT) kpos_lds[threadIdx.x] = kpos_reg;
+    if (kPos && threadIdx.x < kKT) kpos_lds[bf][threadIdx.x] = kpos_reg;
   };
 
+  int bf = 0;
   if (kv_end > 0) {
     gload(0);
-    lstore();
+    lstore(0);
   }
   __syncthreads();
   for (int kt0 = 0; kt0 < kv_end; kt0 += kKT) {
     const bool has_next = kt0 + kKT < kv_end;
     if (has_next) gload(kt0 + kKT);
     if (kt0 < wave_end) {
+      const uint16_t* kl = k_lds[bf];
+      const uint16_t* vl = v_lds[bf];
       f32x16 s[2];
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
         s[blk] = f32x16{};
 #pragma unroll
         for (int st = 0; st < D / 16; ++st) {
-          const bf16x8 a = as_bf16x8(ld16(&k_lds[(blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
+          const bf16x8 a = as_bf16x8(ld16(&kl[(blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
           s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], s[blk], 0, 0, 0);
         }
       }
       const bool need_mask = kPos || kt0 + kKT > wmin || kt0 + kKT > nkv;
-      float mt = -INFINITY;
+      if (need_mask) {
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
+        for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          float x = s[blk][v] * scale2;
-          if (need_mask) {
+          for (int v = 0; v < 16; ++v) {
             const int jt = blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
             const int j = kt0 + jt;
-            const int kp = kPos ? kpos_lds[jt] : j;
-            if (j >= nkv || kp > qpos) x = -INFINITY;
+            const int kp = kPos ? kpos_lds[bf][jt] : j;
+            if (j >= nkv || kp > qpos) s[blk][v] = -INFINITY;
           }
-          s[blk][v] = x;
-          mt = fmaxf(mt, x);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float mn = fmaxf(m, mt);
-      const float alpha = (mn == -INFINITY) ? 1.f : exp2f(m - mn);
-      float psum = 0.f;
-      bf16x8 pb[4];
+      }
+      float mt = s[0][0];
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float p = (mn == -INFINITY) ? 0.f : exp2f(s[blk][v] - mn);
-          psum += p;
-          pb[blk * 2 + (v >> 3)][v & 7] = (__bf16)p;
-        }
-      ls = ls * alpha + psum;
-      m = mn;
+        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[blk][v]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * scale2;
+      // lazy rescale: keep a stale max unless some row's max grew by > 2^8
+      if (__ballot(mt > m + 8.f)) {
+        const float mn = fmaxf(m, mt);
+        const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m - mn);
+        ls *= alpha;
 #pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+        for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+        m = mn;
+      }
+      const float nm = -m;
+      float psum = 0.f;
+      bf16x8 pb[4];
+      if (need_mask) {
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float x = s[blk][v];
+            const float p = x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(fmaf(x, scale2, nm));
+            psum += p;
+            pb[blk * 2 + (v >> 3)][v & 7] = (__bf16)p;
+          }
+      } else {
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[blk][v], scale2, nm));
+            psum += p;
+            pb[blk * 2 + (v >> 3)][v & 7] = (__bf16)p;
+          }
+      }
+      ls += psum;
 #pragma unroll
       for (int s4 = 0; s4 < 4; ++s4)
 #pragma unroll
         for (int mb = 0; mb < D / 32; ++mb) {
-          const bf16x8 a = as_bf16x8(ld16(&v_lds[(32 * mb + lq) * VSTR + 16 * s4 + 8 * hi]));
+          const int d = 32 * mb + lq;
+          const int col = ((2 * s4 + hi) ^ ((d >> 3) & 7)) << 3;
+          const bf16x8 a = as_bf16x8(ld16(&vl[d * VSTR + col]));
           o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[s4], o[mb], 0, 0, 0);
         }
     }
+    if (has_next) lstore(bf ^ 1);
     __syncthreads();
-    if (has_next) {
-      lstore();
-      __syncthreads();
-    }
+    bf ^= 1;
   }
 
   const float lt = ls + __shfl_xor(ls, 32, 64);
@@ -298,12 +335,15 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
   while ((1 << lg) < s.hq / s.hkv) ++lg;
   if (bf16) {
     const int rpb = 128 >> lg;
-    dim3 grid((s.max_rows + rpb - 1) / rpb, s.hkv, s.batch);
+    const int max_tiles = (s.max_rows + rpb - 1) / rpb;
+    const int64_t nblocks = (int64_t)max_tiles * s.batch * s.hkv;
+    if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)nblocks);
 #define QCF_ATTN(D, P)                                                                            \
   attn_bf16_kernel<D, P><<<grid, kThreads, 0, stream>>>(                                          \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
-      kv_row_stride, cu_kv, kv_pos, s.hq, lg, scale2)
+      kv_row_stride, cu_kv, kv_pos, s.batch, max_tiles, s.hkv, s.hq, lg, scale2)
     if (kv_pos) {
       if (s.d == 64) QCF_ATTN(64, true); else QCF_ATTN(128, true);
     } else {

@@ -8,16 +8,17 @@
 //    the request times the G query heads that share the KV head (GQA
 //    packing), 32 vectors per wave;
 //  * the keys 0 .. max(row position in the block) stream through LDS in
-//    64-key tiles (K row-major, V transposed with a key order that matches the
-//    P operand), with the next tile prefetched into registers;
+//    64-key tiles that arrive by direct global->LDS DMA into a second buffer
+//    while the current tile is computed (one barrier per tile);
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (Q stays in registers as the B
 //    operand), so each lane holds 16 logits of ONE query vector: row max,
-//    rescale and row sum stay in the lane plus one exchange with lane ^ 32;
+//    rescale and row sum stay in the lane plus one lane^32 exchange;
 //  * O^T += V^T P^T on the same instruction: P^T comes straight from the
-//    logit registers (rounded to bf16), V^T from LDS;
-//  * online softmax in float32 (base-2 exponentials); the per-row causal
-//    limit masks only tiles that reach past the wave's smallest position, and
-//    waves skip tiles past their largest position.
+//    logit registers (rounded to bf16), V^T from row-major LDS through the
+//    gfx950 transposing LDS read, so V is never transposed in registers;
+//  * online softmax in float32 (base-2 exponentials) with a lazy rescale;
+//    the per-row causal limit masks only tiles that reach past the wave's
+//    smallest position, and waves skip tiles past their largest position.
 // fp32 path (vector ALUs): one wave per (row, head).
 #include <limits.h>
 #include <math.h>
@@ -33,13 +34,6 @@ constexpr int kKT = 64;  // keys per tile
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
 
-// position inside a 16-key group of the transposed V tile: bits 2 and 3 swap,
-// so lane half h of the P operand (keys {0-3, 8-11} or {4-7, 12-15}) reads one
-// contiguous 16-byte run
-__device__ __forceinline__ int vt_slot(int key) {
-  return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
-}
-
 template <int D, bool kPos>
 __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, const uint16_t* __restrict__ q,
@@ -47,13 +41,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, const int32_t* __restrict__ kv_pos,
     int batch, int max_tiles, int hkv, int hq, int lg, float scale2) {
-  constexpr int KSTR = D + 8;    // K tile row (bf16 elements), 16-byte pad
-  constexpr int VSTR = kKT + 8;  // V^T tile row (bf16 elements), 16-byte pad
-  constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
-  constexpr int KPT = kKT * CPR / kThreads;  // K chunks per thread per tile
-  constexpr int VTASKS = (kKT / 4) * CPR;    // (4-key group, chunk) tasks per tile
+  // LDS tiles, row-major, one key per row, filled by global->LDS DMA:
+  //  K rows hold D/8 16-byte chunks + 1 pad chunk, so the 16-byte fragment
+  //  reads of 8 consecutive keys hit distinct banks;
+  //  V rows hold D/8 chunks + 4 pad chunks (a 64-byte shift per row), so the
+  //  8-byte transposing reads of 8 rows x 64 bytes spread over all banks.
+  constexpr int KCH = D / 8 + 1, VCH = D / 8 + 4;  // 16-byte chunks per LDS row
+  constexpr int KSTR = KCH * 8, VSTR = VCH * 8;    // bf16 elements per LDS row
+  constexpr int KI = (KCH + 3) / 4, VI = VCH / 4;  // DMA instructions per wave
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKT * KSTR];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][D * VSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kKT * VSTR];
   __shared__ int kpos_lds[2][kPos ? kKT : 1];
   __shared__ int red[4];
 
@@ -105,27 +102,53 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   float m = valid ? -INFINITY : INFINITY;
   float ls = 0.f;
 
-  // Loads are clamped to the last key, so they never branch; keys past the
-  // end are masked out of the softmax.
-  uint4 kbuf[KPT], vbuf[4];
-  int kpos_reg = 0;
+  // DMA (global_load_lds_dwordx4: lane i of a wave writes 16 bytes at the
+  // wave's LDS base + 16 i).  Instruction i of a tile fills LDS chunks
+  // [64 i, 64 i + 64); wave w issues instructions w, w + 4, ...; the lane that
+  // fills chunk c of row r loads key r's chunk c (pad chunks reload chunk 0).
+  // Lane offsets are fixed; a full tile only moves a uniform base.  The tile
+  // that crosses the end of the keys clamps its rows to the last key.
   const uint16_t* kbase = kc + kv0 * kv_stride + (int64_t)g * D;
   const uint16_t* vbase = vc + kv0 * kv_stride + (int64_t)g * D;
   const int jmax = max(nkv - 1, 0);
-  auto gload = [&](int kt0) {
+  int koff[KI], voff[KI > VI ? KI : VI];
 #pragma unroll
-    for (int c = 0; c < KPT; ++c) {
-      const int idx = threadIdx.x + c * kThreads;
-      const int key = idx / CPR, ch = idx - key * CPR;
-      const int j = min(kt0 + key, jmax);
-      kbuf[c] = ld16(kbase + (int64_t)j * kv_stride + ch * 8);
-    }
-    if (threadIdx.x < VTASKS) {
-      const int grp = threadIdx.x / CPR, ch = threadIdx.x - grp * CPR;
+  for (int t = 0; t < KI; ++t) {
+    const int ci = (w + 4 * t) * 64 + l, r = ci / KCH, c = ci % KCH;
+    koff[t] = r * (int)kv_stride + (c < D / 8 ? c * 8 : 0);
+  }
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int j = min(kt0 + 4 * grp + e, jmax);
-        vbuf[e] = ld16(vbase + (int64_t)j * kv_stride + ch * 8);
+  for (int t = 0; t < VI; ++t) {
+    const int ci = (w + 4 * t) * 64 + l, r = ci / VCH, c = ci % VCH;
+    voff[t] = r * (int)kv_stride + (c < D / 8 ? c * 8 : 0);
+  }
+  int kpos_reg = 0;
+  auto dma = [&](const uint16_t* src, int off, uint16_t* dst) {
+    __builtin_amdgcn_global_load_lds((const void*)(src + off),
+                                     (void __attribute__((address_space(3)))*)dst, 16, 0, 0);
+  };
+  auto gload = [&](int kt0, int bfn) {
+    if (kt0 + kKT <= nkv) {
+      const uint16_t* kt = kbase + (int64_t)kt0 * kv_stride;
+      const uint16_t* vt = vbase + (int64_t)kt0 * kv_stride;
+#pragma unroll
+      for (int t = 0; t < KI; ++t)
+        if (w + 4 * t < KCH) dma(kt, koff[t], &k_lds[bfn][(w + 4 * t) * 512]);
+#pragma unroll
+      for (int t = 0; t < VI; ++t) dma(vt, voff[t], &v_lds[bfn][(w + 4 * t) * 512]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < KI; ++t) {
+        if (w + 4 * t >= KCH) continue;
+        const int ci = (w + 4 * t) * 64 + l, r = ci / KCH, c = ci % KCH;
+        const int j = min(kt0 + r, jmax);
+        dma(kbase, j * (int)kv_stride + (c < D / 8 ? c * 8 : 0), &k_lds[bfn][(w + 4 * t) * 512]);
+      }
+#pragma unroll
+      for (int t = 0; t < VI; ++t) {
+        const int ci = (w + 4 * t) * 64 + l, r = ci / VCH, c = ci % VCH;
+        const int j = min(kt0 + r, jmax);
+        dma(vbase, j * (int)kv_stride + (c < D / 8 ? c * 8 : 0), &v_lds[bfn][(w + 4 * t) * 512]);
       }
     }
     if (kPos && threadIdx.x < kKT) {
@@ -133,119 +156,114 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
       kpos_reg = j < nkv ? kv_pos[kv0 + j] : INT_MAX;
     }
   };
-  // V^T rows are XOR-swizzled in 16-byte chunks by (row / 8) so the transposing
-  // 8-byte stores of a wave spread over all banks; reads stay conflict-free.
-  auto lstore = [&](int bf) {
-#pragma unroll
-    for (int c = 0; c < KPT; ++c) {
-      const int idx = threadIdx.x + c * kThreads;
-      const int key = idx / CPR, ch = idx - key * CPR;
-      st16(&k_lds[bf][key * KSTR + ch * 8], kbuf[c]);
-    }
-    if (threadIdx.x < VTASKS) {
-      const int grp = threadIdx.x / CPR, ch = threadIdx.x - grp * CPR;
-      const int slot = (4 * grp & ~15) + vt_slot(4 * grp & 15);
-      const int col = (((slot >> 3) ^ (ch & 7)) << 3) + (slot & 7);
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vbuf[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vbuf[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vbuf[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vbuf[3]);
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const int sh = (dd & 1) * 16;
-        const uint32_t a0 = (w0[dd >> 1] >> sh) & 0xffffu, a1 = (w1[dd >> 1] >> sh) & 0xffffu;
-        const uint32_t a2 = (w2[dd >> 1] >> sh) & 0xffffu, a3 = (w3[dd >> 1] >> sh) & 0xffffu;
-        *reinterpret_cast<uint2*>(&v_lds[bf][(ch * 8 + dd) * VSTR + col]) =
-            make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
-      }
-    }
-    if (kPos && threadIdx.x < kKT) kpos_lds[bf][threadIdx.x] = kpos_reg;
+  auto kstore = [&](int bfn) {
+    if (kPos && threadIdx.x < kKT) kpos_lds[bfn][threadIdx.x] = kpos_reg;
   };
+  // Transposing V reads (ds_read_b64_tr_b16): inside each 16-lane group, lane
+  // j's element e comes from element (j & 3) of the 4-element segment that
+  // lane 16 g + 4 e + ((j & 15) >> 2) addresses.  Lane (g, e, qd) therefore
+  // addresses V row 4 (g >> 1) + e (+ 8 per read) at column 16 (g & 1) + 4 qd,
+  // which hands every lane the keys of its P-operand slots for its d column.
+  const int tg = l >> 4, te = (l >> 2) & 3, tq = l & 3;
+  const int vrd = (4 * (tg >> 1) + te) * VSTR + 16 * (tg & 1) + 4 * tq;
+  const int krd = lq * KSTR + 8 * hi;
 
   int bf = 0;
   if (kv_end > 0) {
-    gload(0);
-    lstore(0);
+    gload(0, 0);
+    kstore(0);
   }
   __syncthreads();
   for (int kt0 = 0; kt0 < kv_end; kt0 += kKT) {
     const bool has_next = kt0 + kKT < kv_end;
-    if (has_next) gload(kt0 + kKT);
     if (kt0 < wave_end) {
-      const uint16_t* kl = k_lds[bf];
-      const uint16_t* vl = v_lds[bf];
-      f32x16 s[2];
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        s[blk] = f32x16{};
-#pragma unroll
-        for (int st = 0; st < D / 16; ++st) {
-          const bf16x8 a = as_bf16x8(ld16(&kl[(blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
-          s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], s[blk], 0, 0, 0);
-        }
-      }
+      const uint16_t* kl = k_lds[bf] + krd;
+      const uint16_t* vl = v_lds[bf] + vrd;
       const bool need_mask = kPos || kt0 + kKT > wmin || kt0 + kKT > nkv;
-      if (need_mask) {
+      // two 32-key halves: S^T = K Q^T, softmax, O^T += V^T P^T
 #pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
+      for (int hb = 0; hb < 2; ++hb) {
+        bf16x8 kf[D / 16];
+#pragma unroll
+        for (int st = 0; st < D / 16; ++st) kf[st] = as_bf16x8(ld16(kl + hb * 32 * KSTR + 16 * st));
+        f32x16 s = f32x16{};
+#pragma unroll
+        for (int st = 0; st < D / 16; ++st)
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qreg[st], s, 0, 0, 0);
+        // V^T fragments of this half, read ahead of the softmax
+        bf16x8 vf[2 * (D / 32)];
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int mb = 0; mb < D / 32; ++mb) {
+            typedef short v4s __attribute__((ext_vector_type(4)));
+            typedef v4s __attribute__((address_space(3))) * lds_v4s;
+            const uint16_t* p0 = vl + (hb * 32 + 16 * k2) * VSTR + 32 * mb;
+            const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0));
+            const v4s hi8 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0 + 8 * VSTR));
+            vf[k2 * (D / 32) + mb] = __builtin_bit_cast(
+                bf16x8, __builtin_shufflevector(lo, hi8, 0, 1, 2, 3, 4, 5, 6, 7));
+          }
+        // the next tile's DMA flies while this tile's softmax and P.V run
+        if (hb == 0 && has_next) gload(kt0 + kKT, bf ^ 1);
+        if (need_mask) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int jt = blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
+            const int jt = hb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
             const int j = kt0 + jt;
             const int kp = kPos ? kpos_lds[bf][jt] : j;
-            if (j >= nkv || kp > qpos) s[blk][v] = -INFINITY;
+            if (j >= nkv || kp > qpos) s[v] = -INFINITY;
           }
-      }
-      float mt = s[0][0];
+        }
+        float mt = s[0];
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
+        for (int v = 1; v < 16; ++v) mt = fmaxf(mt, s[v]);
+        {
+          // lanes l and l ^ 32 hold the two halves of the same query vector's keys
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt),
+                                                           false, false);
+          mt = fmaxf(mt, fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]))) * scale2;
+        }
+        // lazy rescale: keep a stale max unless some row's max grew by > 2^8
+        if (__ballot(mt > m + 8.f)) {
+          const float mn = fmaxf(m, mt);
+          const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m - mn);
+          ls *= alpha;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[blk][v]);
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * scale2;
-      // lazy rescale: keep a stale max unless some row's max grew by > 2^8
-      if (__ballot(mt > m + 8.f)) {
-        const float mn = fmaxf(m, mt);
-        const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m - mn);
-        ls *= alpha;
-#pragma unroll
-        for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-        m = mn;
-      }
-      const float nm = -m;
-      float psum = 0.f;
-      bf16x8 pb[4];
-      if (need_mask) {
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
+          for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+          m = mn;
+        }
+        const float nm = -m;
+        float psum = 0.f;
+        bf16x8 pb[2];
+        if (need_mask) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const float x = s[blk][v];
+            const float x = s[v];
             const float p = x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(fmaf(x, scale2, nm));
             psum += p;
-            pb[blk * 2 + (v >> 3)][v & 7] = (__bf16)p;
+            pb[v >> 3][v & 7] = (__bf16)p;
           }
-      } else {
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
+        } else {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[blk][v], scale2, nm));
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[v], scale2, nm));
             psum += p;
-            pb[blk * 2 + (v >> 3)][v & 7] = (__bf16)p;
+            pb[v >> 3][v & 7] = (__bf16)p;
           }
-      }
-      ls += psum;
-#pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4)
-#pragma unroll
-        for (int mb = 0; mb < D / 32; ++mb) {
-          const int d = 32 * mb + lq;
-          const int col = ((2 * s4 + hi) ^ ((d >> 3) & 7)) << 3;
-          const bf16x8 a = as_bf16x8(ld16(&vl[d * VSTR + col]));
-          o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[s4], o[mb], 0, 0, 0);
         }
+        ls += psum;
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int mb = 0; mb < D / 32; ++mb)
+            o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k2 * (D / 32) + mb], pb[k2], o[mb],
+                                                            0, 0, 0);
+      }
+    } else if (has_next) {
+      gload(kt0 + kKT, bf ^ 1);
     }
-    if (has_next) lstore(bf ^ 1);
+    if (has_next) kstore(bf ^ 1);
     __syncthreads();
     bf ^= 1;
   }

@@ -8,8 +8,10 @@
 //    the request times the G query heads that share the KV head (GQA
 //    packing), 32 vectors per wave;
 //  * the keys 0 .. max(row position in the block) stream through LDS in
-//    64-key tiles that arrive by direct global->LDS DMA into a second buffer
-//    while the current tile is computed (one barrier per tile);
+//    64-key tiles that arrive by direct global->LDS DMA (K two tiles ahead, V
+//    one tile ahead; one barrier per tile), and the tile loop is software
+//    pipelined: tile t+1's S^T runs on the matrix cores while tile t's
+//    softmax runs on the vector ALUs;
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (Q stays in registers as the B
 //    operand), so each lane holds 16 logits of ONE query vector: row max,
 //    rescale and row sum stay in the lane plus one lane^32 exchange;
@@ -22,6 +24,7 @@
 // fp32 path (vector ALUs): one wave per (row, head).
 #include <limits.h>
 #include <math.h>
+#include <stdlib.h>
 
 #include "qcf_device.h"
 #include "qcf_launch.h"
@@ -40,7 +43,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
     const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, const int32_t* __restrict__ kv_pos,
-    int batch, int max_tiles, int hkv, int hq, int lg, float scale2) {
+    int batch, int max_tiles, int hkv, int hq, int lg, float scale2, int n_split_max,
+    int split_tiles, float* __restrict__ part_o, float2* __restrict__ part_ml) {
   // LDS tiles, row-major, one key per row, filled by global->LDS DMA:
   //  K rows hold D/8 16-byte chunks + 1 pad chunk, so the 16-byte fragment
   //  reads of 8 consecutive keys hit distinct banks;
@@ -55,13 +59,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   __shared__ int red[4];
 
   // Block order: consecutive block ids land on consecutive XCDs, so all
-  // blocks of one KV head share an XCD (and its L2); the tiles with the
-  // most keys (the last rows of each request) are dispatched first.
+  // blocks of one KV head share an XCD (and its L2); the splits of one row
+  // tile are adjacent; the tiles with the most keys (the last rows of each
+  // request) are dispatched first.
   const int L = blockIdx.x;
   const int g = L % hkv;
   const int rest = L / hkv;
-  const int b = rest % batch;
-  const int tile = max_tiles - 1 - rest / batch;
+  const int split = rest % n_split_max;
+  const int rest2 = rest / n_split_max;
+  const int b = rest2 % batch;
+  const int tile = max_tiles - 1 - rest2 / batch;
   const int G = 1 << lg;
   const int rpb = 128 >> lg;
   const int64_t r0 = cu_rows[b];
@@ -86,6 +93,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   const int bmax = max(max(red[0], red[1]), max(red[2], red[3]));
   const int kv_end = kPos ? nkv : min(nkv, bmax + 1);
   const int wave_end = kPos ? nkv : min(nkv, wmax + 1);
+  // split-K: this block covers keys [kt_lo, kt_hi) of the row tile's range;
+  // the last split also takes any remainder
+  const int span = split_tiles * kKT;
+  int nsp = (kv_end + span - 1) / span;
+  if (nsp > n_split_max) nsp = n_split_max;
+  const int kt_lo = split * span;
+  if (split > 0 && kt_lo >= kv_end) return;
+  const int kt_hi = split == nsp - 1 ? kv_end : min(kv_end, kt_lo + span);
 
   bf16x8 qreg[D / 16];
   {
@@ -97,9 +112,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   f32x16 o[D / 32];
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
-  // running max in log2 units; padding lanes start at +inf so they never
-  // trigger a rescale and produce p = 0
-  float m = valid ? -INFINITY : INFINITY;
+  // running max in log2 units.  It starts at -1e30 (not -inf) so that a
+  // masked logit (-inf) always gives p = exp2(-inf) = 0 without a guard;
+  // padding lanes start at +inf so they never trigger a rescale and give p = 0.
+  float m = valid ? -1e30f : INFINITY;
   float ls = 0.f;
 
   // DMA (global_load_lds_dwordx4: lane i of a wave writes 16 bytes at the
@@ -127,15 +143,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
     __builtin_amdgcn_global_load_lds((const void*)(src + off),
                                      (void __attribute__((address_space(3)))*)dst, 16, 0, 0);
   };
-  auto gload = [&](int kt0, int bfn) {
+  auto gload_k = [&](int kt0, int bfn) {
     if (kt0 + kKT <= nkv) {
       const uint16_t* kt = kbase + (int64_t)kt0 * kv_stride;
-      const uint16_t* vt = vbase + (int64_t)kt0 * kv_stride;
 #pragma unroll
       for (int t = 0; t < KI; ++t)
         if (w + 4 * t < KCH) dma(kt, koff[t], &k_lds[bfn][(w + 4 * t) * 512]);
-#pragma unroll
-      for (int t = 0; t < VI; ++t) dma(vt, voff[t], &v_lds[bfn][(w + 4 * t) * 512]);
     } else {
 #pragma unroll
       for (int t = 0; t < KI; ++t) {
@@ -144,6 +157,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
         const int j = min(kt0 + r, jmax);
         dma(kbase, j * (int)kv_stride + (c < D / 8 ? c * 8 : 0), &k_lds[bfn][(w + 4 * t) * 512]);
       }
+    }
+  };
+  auto gload_v = [&](int kt0, int bfn) {
+    if (kt0 + kKT <= nkv) {
+      const uint16_t* vt = vbase + (int64_t)kt0 * kv_stride;
+#pragma unroll
+      for (int t = 0; t < VI; ++t) dma(vt, voff[t], &v_lds[bfn][(w + 4 * t) * 512]);
+    } else {
 #pragma unroll
       for (int t = 0; t < VI; ++t) {
         const int ci = (w + 4 * t) * 64 + l, r = ci / VCH, c = ci % VCH;
@@ -168,120 +189,250 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   const int vrd = (4 * (tg >> 1) + te) * VSTR + 16 * (tg & 1) + 4 * tq;
   const int krd = lq * KSTR + 8 * hi;
 
-  int bf = 0;
-  if (kv_end > 0) {
-    gload(0, 0);
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  typedef v4s __attribute__((address_space(3))) * lds_v4s;
+  // V^T fragments of one 32-key half (2 k-steps x D/32 column blocks)
+  auto read_v = [&](const uint16_t* vl, int hb, bf16x8* vf) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb) {
+        const uint16_t* p0 = vl + (hb * 32 + 16 * k2) * VSTR + 32 * mb;
+        const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0));
+        const v4s up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0 + 8 * VSTR));
+        vf[k2 * (D / 32) + mb] =
+            __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+  };
+  // S^T = K Q^T of one 32-key half of the tile in LDS buffer kb
+  auto qk_half = [&](const uint16_t* kl, int hb, f32x16& sh) {
+    bf16x8 kf[D / 16];
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st) kf[st] = as_bf16x8(ld16(kl + hb * 32 * KSTR + 16 * st));
+    sh = f32x16{};
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st)
+      sh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qreg[st], sh, 0, 0, 0);
+  };
+  // masks and running max of one tile (lazy rescale of O)
+  auto softmax_pre = [&](f32x16 (&sc)[2], int kt0, int bfc) {
+    const bool need_mask = kPos || kt0 + kKT > wmin || kt0 + kKT > nkv;
+    if (need_mask) {
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int jt = hb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
+          const int j = kt0 + jt;
+          const int kp = kPos ? kpos_lds[bfc][jt] : j;
+          if (j >= nkv || kp > qpos) sc[hb][v] = -INFINITY;
+        }
+    }
+    float mt = sc[0][0];
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[hb][v]);
+    {
+      // lanes l and l ^ 32 hold the two halves of the same query vector's keys
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt),
+                                                       false, false);
+      mt = fmaxf(mt, fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]))) * scale2;
+    }
+    // lazy rescale: keep a stale max unless some row's max grew by > 2^8
+    if (__ballot(mt > m + 8.f)) {
+      const float mn = fmaxf(m, mt);
+      const float alpha = __builtin_amdgcn_exp2f(m - mn);
+      ls *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+      m = mn;
+    }
+  };
+  // P = exp2(S * scale2 - m) of one tile -> pb (straight-line code)
+  auto softmax_exp = [&](f32x16 (&sc)[2], bf16x8 (&pb)[2][2]) {
+    const float nm = -m;
+    float psum = 0.f;
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[hb][v], scale2, nm));
+        psum += p;
+        pb[hb][v >> 3][v & 7] = (__bf16)p;
+      }
+    ls += psum;
+  };
+  auto pv = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      bf16x8 vf[2 * (D / 32)];
+      read_v(vl, hb, vf);
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb)
+          o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k2 * (D / 32) + mb], pb[hb][k2],
+                                                          o[mb], 0, 0, 0);
+    }
+  };
+
+  // Software pipeline over the key tiles of [kt_lo, kt_hi): while tile t's
+  // softmax runs on the vector ALUs, tile t+1's S^T runs on the matrix cores.
+  // K is fetched two tiles ahead and V one tile ahead, so two LDS buffers of
+  // each and one barrier per tile suffice:
+  //   step t: DMA K(t+2) -> K[t%2], V(t+1) -> V[(t+1)%2];
+  //           S(t+1) from K[(t+1)%2] || softmax(t); O += P(t) V(t) from V[t%2];
+  //           barrier.
+  const int nt = kt_hi > kt_lo ? (kt_hi - kt_lo + kKT - 1) / kKT : 0;
+  f32x16 sa[2], sb[2];
+  if (nt > 0) {
+    gload_k(kt_lo, 0);
+    gload_v(kt_lo, 0);
     kstore(0);
   }
+  if (nt > 1) gload_k(kt_lo + kKT, 1);
   __syncthreads();
-  for (int kt0 = 0; kt0 < kv_end; kt0 += kKT) {
-    const bool has_next = kt0 + kKT < kv_end;
-    if (kt0 < wave_end) {
-      const uint16_t* kl = k_lds[bf] + krd;
-      const uint16_t* vl = v_lds[bf] + vrd;
-      const bool need_mask = kPos || kt0 + kKT > wmin || kt0 + kKT > nkv;
-      // two 32-key halves: S^T = K Q^T, softmax, O^T += V^T P^T
+  if (nt > 0 && kt_lo < wave_end) {
+    qk_half(k_lds[0] + krd, 0, sa[0]);
+    qk_half(k_lds[0] + krd, 1, sa[1]);
+  }
+  __syncthreads();
+  auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
+    const int cur = t & 1, nxt = cur ^ 1;
+    const int kt0 = kt_lo + t * kKT;
+    if (t + 2 < nt) gload_k(kt0 + 2 * kKT, cur);
+    if (t + 1 < nt) gload_v(kt0 + kKT, nxt);
+    const bool do_cur = kt0 < wave_end;
+    const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
+    bf16x8 pb[2][2];
+    if (do_cur) softmax_pre(sc, kt0, cur);
+    if (do_next) {
+      // one basic block: the next tile's MFMAs interleave with this tile's exponentials
+      qk_half(k_lds[nxt] + krd, 0, sn[0]);
+      qk_half(k_lds[nxt] + krd, 1, sn[1]);
+      softmax_exp(sc, pb);
 #pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        bf16x8 kf[D / 16];
-#pragma unroll
-        for (int st = 0; st < D / 16; ++st) kf[st] = as_bf16x8(ld16(kl + hb * 32 * KSTR + 16 * st));
-        f32x16 s = f32x16{};
-#pragma unroll
-        for (int st = 0; st < D / 16; ++st)
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qreg[st], s, 0, 0, 0);
-        // V^T fragments of this half, read ahead of the softmax
-        bf16x8 vf[2 * (D / 32)];
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-          for (int mb = 0; mb < D / 32; ++mb) {
-            typedef short v4s __attribute__((ext_vector_type(4)));
-            typedef v4s __attribute__((address_space(3))) * lds_v4s;
-            const uint16_t* p0 = vl + (hb * 32 + 16 * k2) * VSTR + 32 * mb;
-            const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0));
-            const v4s hi8 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0 + 8 * VSTR));
-            vf[k2 * (D / 32) + mb] = __builtin_bit_cast(
-                bf16x8, __builtin_shufflevector(lo, hi8, 0, 1, 2, 3, 4, 5, 6, 7));
-          }
-        // the next tile's DMA flies while this tile's softmax and P.V run
-        if (hb == 0 && has_next) gload(kt0 + kKT, bf ^ 1);
-        if (need_mask) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int jt = hb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
-            const int j = kt0 + jt;
-            const int kp = kPos ? kpos_lds[bf][jt] : j;
-            if (j >= nkv || kp > qpos) s[v] = -INFINITY;
-          }
-        }
-        float mt = s[0];
-#pragma unroll
-        for (int v = 1; v < 16; ++v) mt = fmaxf(mt, s[v]);
-        {
-          // lanes l and l ^ 32 hold the two halves of the same query vector's keys
-          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt),
-                                                           false, false);
-          mt = fmaxf(mt, fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]))) * scale2;
-        }
-        // lazy rescale: keep a stale max unless some row's max grew by > 2^8
-        if (__ballot(mt > m + 8.f)) {
-          const float mn = fmaxf(m, mt);
-          const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m - mn);
-          ls *= alpha;
-#pragma unroll
-          for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-          m = mn;
-        }
-        const float nm = -m;
-        float psum = 0.f;
-        bf16x8 pb[2];
-        if (need_mask) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float x = s[v];
-            const float p = x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(fmaf(x, scale2, nm));
-            psum += p;
-            pb[v >> 3][v & 7] = (__bf16)p;
-          }
-        } else {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[v], scale2, nm));
-            psum += p;
-            pb[v >> 3][v & 7] = (__bf16)p;
-          }
-        }
-        ls += psum;
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-          for (int mb = 0; mb < D / 32; ++mb)
-            o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k2 * (D / 32) + mb], pb[k2], o[mb],
-                                                            0, 0, 0);
+      for (int i = 0; i < D / 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);   // then vector ALU work
       }
-    } else if (has_next) {
-      gload(kt0 + kKT, bf ^ 1);
+    } else if (do_cur) {
+      softmax_exp(sc, pb);
     }
-    if (has_next) kstore(bf ^ 1);
+    if (do_cur) pv(v_lds[cur] + vrd, pb);
+    if (t + 1 < nt) kstore(nxt);
     __syncthreads();
-    bf ^= 1;
+  };
+  for (int t = 0; t < nt; t += 2) {
+    step(t, sa, sb);
+    if (t + 1 < nt) step(t + 1, sb, sa);
   }
 
   const float lt = ls + __shfl_xor(ls, 32, 64);
-  if (!valid) return;
-  const float inv = lt > 0.f ? 1.f / lt : 0.f;
   uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D;
+  if (nsp <= 1) {
+    if (!valid) return;
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d0 = 32 * mb + 8 * i + 4 * hi;
+        *reinterpret_cast<uint2*>(op + d0) =
+            make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
+                       pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
+      }
+    if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
+    return;
+  }
+  // Several splits: write this split's unnormalised O^T, its (stale) max and
+  // sum; attn_merge_kernel combines the splits after this kernel.
+  if (!valid) return;
+  const int64_t item = (((int64_t)b * max_tiles + tile) * hkv + g) * n_split_max + split;
+  float* po = part_o + (item * 128 + qv) * D;
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int d0 = 32 * mb + 8 * i + 4 * hi;
-      *reinterpret_cast<uint2*>(op + d0) =
-          make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
-                     pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<float4*>(po + 32 * mb + 8 * i + 4 * hi) =
+          make_float4(o[mb][4 * i], o[mb][4 * i + 1], o[mb][4 * i + 2], o[mb][4 * i + 3]);
+  if (hi == 0) part_ml[item * 128 + qv] = make_float2(m, lt);
+}
+
+// Combines the split-K partials of every row tile that was split, in split
+// order (deterministic).  One block per (row tile, KV head); 2 threads per
+// query vector, each owning half of its D outputs.
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_merge_kernel(
+    uint16_t* __restrict__ out, float* __restrict__ lse, const int32_t* __restrict__ row_pos,
+    int64_t n_rows, const int32_t* __restrict__ cu_rows, const int32_t* __restrict__ cu_kv,
+    int64_t n_kv_rows, int batch, int max_tiles, int hkv, int hq, int lg, int n_split_max,
+    int split_tiles, const float* __restrict__ part_o, const float2* __restrict__ part_ml) {
+  __shared__ int red[4];
+  const int L = blockIdx.x;
+  const int g = L % hkv;
+  const int rest = L / hkv;
+  const int b = rest % batch;
+  const int tile = max_tiles - 1 - rest / batch;
+  const int G = 1 << lg;
+  const int rpb = 128 >> lg;
+  const int64_t r0 = cu_rows[b];
+  const int nr = cu_rows[b + 1] - (int)r0;
+  const int rbase = tile * rpb;
+  if (rbase >= nr) return;
+  const int64_t kv0 = cu_kv[b];
+  int nkv = cu_kv[b + 1] - (int)kv0;
+  if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
+  // the same key range (and split count) as the attention kernel's blocks
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  {
+    const int qv = 32 * w + (l & 31);
+    const int rl = rbase + (qv >> lg);
+    const bool ok = rl < nr && r0 + rl < n_rows;
+    const int mx = wave_max_i(ok ? row_pos[r0 + rl] : -1);
+    if (l == 0) red[w] = mx;
+  }
+  __syncthreads();
+  const int kv_end = min(nkv, max(max(red[0], red[1]), max(red[2], red[3])) + 1);
+  const int span = split_tiles * kKT;
+  int nsp = (kv_end + span - 1) / span;
+  if (nsp > n_split_max) nsp = n_split_max;
+  if (nsp <= 1) return;
+  const int qv = threadIdx.x >> 1, half = threadIdx.x & 1;
+  const int rl = rbase + (qv >> lg);
+  const int64_t grow = r0 + rl;
+  if (rl >= nr || grow >= n_rows) return;
+  const int head = g * G + (qv & (G - 1));
+  const int64_t base = (((int64_t)b * max_tiles + tile) * hkv + g) * n_split_max;
+  float mx = -1e30f;
+  for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 128 + qv].x);
+  float acc[D / 2];
+#pragma unroll
+  for (int e = 0; e < D / 2; ++e) acc[e] = 0.f;
+  float lsum = 0.f;
+  for (int sp = 0; sp < nsp; ++sp) {
+    const float2 ml = part_ml[(base + sp) * 128 + qv];
+    const float wsp = __builtin_amdgcn_exp2f(ml.x - mx);
+    lsum += wsp * ml.y;
+    const float* po = part_o + ((base + sp) * 128 + qv) * D + half * (D / 2);
+#pragma unroll
+    for (int e = 0; e < D / 2; e += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(po + e);
+      acc[e] += wsp * x.x;
+      acc[e + 1] += wsp * x.y;
+      acc[e + 2] += wsp * x.z;
+      acc[e + 3] += wsp * x.w;
     }
-  if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
+  }
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D + half * (D / 2);
+#pragma unroll
+  for (int e = 0; e < D / 2; e += 8)
+    *reinterpret_cast<uint4*>(op + e) =
+        make_uint4(pack_bf16x2(acc[e] * inv, acc[e + 1] * inv), pack_bf16x2(acc[e + 2] * inv, acc[e + 3] * inv),
+                   pack_bf16x2(acc[e + 4] * inv, acc[e + 5] * inv), pack_bf16x2(acc[e + 6] * inv, acc[e + 7] * inv));
+  if (lse && half == 0) lse[grow * hq + head] = lsum > 0.f ? (mx + log2f(lsum)) * kLn2 : -INFINITY;
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -338,36 +489,100 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
   if (lse && l == 0) lse[r * hq + h] = ls > 0.f ? (m + log2f(ls)) * kLn2 : -INFINITY;
 }
 
+// Split-K plan of the bf16 kernel (explicit-position calls never split).
+// The estimate of the total work assumes row positions spread over each
+// request (a triangle of key tiles).  A split holds about as many key tiles
+// as one block slot of the chip gets on average (512 slots: 256 CUs x 2
+// resident blocks), at least 16, and at most 8 splits per row tile.
+struct SplitPlan {
+  int max_tiles, n_split, split_tiles;
+  size_t o_off, ml_off, bytes;
+};
+SplitPlan split_plan(const AttnShape& s, bool explicit_pos) {
+  SplitPlan p{};
+  int lg = 0;
+  while ((1 << lg) < s.hq / s.hkv) ++lg;
+  const int rpb = 128 >> lg;
+  p.max_tiles = (s.max_rows + rpb - 1) / rpb;
+  const int kv_tiles = (s.max_kv + kKT - 1) / kKT;
+  p.n_split = 1;
+  p.split_tiles = kv_tiles > 0 ? kv_tiles : 1;
+  const double est = 0.5 * (double)p.max_tiles * s.hkv * s.batch * kv_tiles;
+  // QCF_ATTN_SPLIT_TILES (read once) overrides the split size for tuning;
+  // 0 disables splitting
+  static const int forced = [] {
+    const char* e = getenv("QCF_ATTN_SPLIT_TILES");
+    return e ? atoi(e) : -1;
+  }();
+  if (!explicit_pos && forced > 0 && forced < kv_tiles) {
+    p.split_tiles = forced;
+    p.n_split = (kv_tiles + forced - 1) / forced;
+  } else if (!explicit_pos && forced < 0 && kv_tiles > 16) {
+    int st = (int)((est + 511.0) / 512.0);
+    st = st < 16 ? 16 : st;
+    const int min_st = (kv_tiles + 7) / 8;
+    st = st < min_st ? min_st : st;
+    if (st < kv_tiles) {
+      p.split_tiles = st;
+      p.n_split = (kv_tiles + st - 1) / st;
+    }
+  }
+  if (p.n_split > 1) {
+    const size_t groups = (size_t)p.max_tiles * s.hkv * s.batch;
+    const size_t items = groups * p.n_split;
+    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    p.o_off = 0;
+    p.ml_off = a256(items * 128 * s.d * sizeof(float));
+    p.bytes = p.ml_off + a256(items * 128 * sizeof(float2));
+  }
+  return p;
+}
+
 }  // namespace
 
-size_t attn_workspace(const AttnShape&, bool) { return 0; }
+size_t attn_workspace(const AttnShape& s, bool bf16) {
+  if (!bf16 || s.batch <= 0 || s.max_rows <= 0) return 0;
+  return split_plan(s, false).bytes;
+}
 
 hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
                               int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
                               const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
                               const int32_t* cu_kv, const int32_t* kv_pos, bool bf16,
-                              const AttnShape& s, float scale, void*, hipStream_t stream) {
+                              const AttnShape& s, float scale, void* ws, hipStream_t stream) {
   if (n_rows == 0 || s.batch == 0 || s.max_rows == 0) return hipSuccess;
   const float scale2 = scale * kLog2e;
   int lg = 0;
   while ((1 << lg) < s.hq / s.hkv) ++lg;
   if (bf16) {
-    const int rpb = 128 >> lg;
-    const int max_tiles = (s.max_rows + rpb - 1) / rpb;
-    const int64_t nblocks = (int64_t)max_tiles * s.batch * s.hkv;
+    const SplitPlan p = split_plan(s, kv_pos != nullptr);
+    char* wb = static_cast<char*>(ws);
+    float* part_o = p.n_split > 1 ? reinterpret_cast<float*>(wb + p.o_off) : nullptr;
+    float2* part_ml = p.n_split > 1 ? reinterpret_cast<float2*>(wb + p.ml_off) : nullptr;
+    const int64_t nblocks = (int64_t)p.max_tiles * s.batch * s.hkv * p.n_split;
     if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
     dim3 grid((unsigned)nblocks);
 #define QCF_ATTN(D, P)                                                                            \
   attn_bf16_kernel<D, P><<<grid, kThreads, 0, stream>>>(                                          \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
-      kv_row_stride, cu_kv, kv_pos, s.batch, max_tiles, s.hkv, s.hq, lg, scale2)
+      kv_row_stride, cu_kv, kv_pos, s.batch, p.max_tiles, s.hkv, s.hq, lg, scale2, p.n_split,     \
+      p.split_tiles, part_o, part_ml)
     if (kv_pos) {
       if (s.d == 64) QCF_ATTN(64, true); else QCF_ATTN(128, true);
     } else {
       if (s.d == 64) QCF_ATTN(64, false); else QCF_ATTN(128, false);
     }
 #undef QCF_ATTN
+    if (p.n_split > 1) {
+      dim3 mgrid((unsigned)((int64_t)p.max_tiles * s.batch * s.hkv));
+#define QCF_MERGE(D)                                                                              \
+  attn_merge_kernel<D><<<mgrid, kThreads, 0, stream>>>(                                           \
+      static_cast<uint16_t*>(out), lse, row_pos, n_rows, cu_rows, cu_kv, n_kv_rows, s.batch,       \
+      p.max_tiles, s.hkv, s.hq, lg, p.n_split, p.split_tiles, part_o, part_ml)
+      if (s.d == 64) QCF_MERGE(64); else QCF_MERGE(128);
+#undef QCF_MERGE
+    }
     return hipGetLastError();
   }
   dim3 grid((unsigned)n_rows, s.hq);

@@ -266,7 +266,7 @@ def qcf_sparse_prefill_attn(out, q, row_pos, cu_rows, k_cache, v_cache, cu_kv, m
     batch = cu_rows.numel() - 1
     need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, hq, hkv, d, q.dtype)
     if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = torch.zeros(need, dtype=torch.uint8, device=q.device)   # counters start at zero
     st = lib().qcf_sparse_prefill_attn(_ptr(out), _ptr(lse), _ptr(q), _ptr(row_pos), n, _ptr(cu_rows),
                                        _ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"),
                                        _ptr(cu_kv), _ptr(kv_pos), _dtype(q), batch, int(max_rows),

@@ -151,10 +151,12 @@ class FusionStep:
         self.scores = torch.zeros(T, dtype=torch.float32, device=dev)
         nws = qcf.qcf_probe_scores_workspace_size(w.batch, p.max_q, p.max_ctx, hq, hkv, d)
         self.ws_scores = torch.empty(max(nws, 256), dtype=torch.uint8, device=dev)
+        self.max_kv = int(np.diff(w.cu_kv).max()) if w.batch else 0
         nwa = qcf.qcf_sparse_prefill_attn_workspace_size(w.batch, max(p.max_R, p.max_probe),
-                                                         max(int(w.cu_kv.max() if w.batch else 0), 1),
-                                                         hq, hkv, d, dt)
-        self.ws_attn = torch.empty(max(nwa, 256), dtype=torch.uint8, device=dev)
+                                                         max(self.max_kv, 1), hq, hkv, d, dt)
+        # zero-filled once: the split-K counters inside start at zero and every call
+        # leaves them at zero
+        self.ws_attn = torch.zeros(max(nwa, 256), dtype=torch.uint8, device=dev)
 
     # -- stages ---------------------------------------------------------------
     def stage_rerope(self):
@@ -194,8 +196,8 @@ class FusionStep:
     def stage_attn(self):
         p = self.plan
         qcf.qcf_sparse_prefill_attn(self.o, self.q_R, self.R_pos, self.cu_R, self.k, self.v,
-                                    self.cu_kv, p.max_R, int(self.w.cu_kv.max() if self.w.batch else 0),
-                                    self.scale, workspace=self.ws_attn)
+                                    self.cu_kv, p.max_R, self.max_kv, self.scale,
+                                    workspace=self.ws_attn)
 
     STAGES = ("rerope", "query_rows", "anchor_gather", "probe_attn", "scores", "select", "scatter",
               "attn")

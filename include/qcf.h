@@ -121,6 +121,45 @@ qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
                           int n_kv_heads, int head_dim, double rope_theta, hipStream_t stream);
 
 /*
+ * qcf_assemble -- everything the query probe needs, in one launch (Section
+ * 3.5, first half): the request cache from the stored chunk caches (eq.
+ * pic_online), the user-query rows rotated at their positions, and the probe
+ * buffer [KV^A ; K/V of the query] with KV^A = Pi(KV^PIC[A]) (eq.
+ * anchor_cache).  Three independent parts, run side by side:
+ *  (1) segments, exactly as qcf_rerope with values:
+ *        k_cache[dst] = rope(k_pic[src], seg_delta[s]),  v_cache[dst] = v_pic[src]
+ *  (2) query rows i < n_query, with s = query_src ? query_src[i] : i and
+ *      p = query_pos[i]:
+ *        k_cache[query_row[i]] = rope(k_new[s], p),  v_cache[query_row[i]] = v_new[s]
+ *        q_u[i] = rope(q_new[s], p)
+ *        and, when query_slot != NULL and j = query_slot[i] >= 0:
+ *        probe_k[j] = rope(k_new[s], p),  probe_v[j] = v_new[s]
+ *  (3) probe slots j < n_probe with probe_src[j] >= 0:
+ *        probe_k[j] = rope(k_pic[probe_src[j]], probe_delta[j]),  probe_v[j] = v_pic[probe_src[j]]
+ *      slots with probe_src[j] < 0 are left to the query rows.
+ *   k_cache, v_cache [n_rows, row_stride]; k_pic, v_pic [n_pic_rows, row_stride]
+ *                    (read only; may not alias the outputs)
+ *   q_new [n_src_rows, n_q_heads * head_dim]; k_new, v_new [n_src_rows,
+ *   n_kv_heads * head_dim]; q_u [n_query, n_q_heads * head_dim];
+ *   probe_k, probe_v [n_probe, n_kv_heads * head_dim] (all dense)
+ *   max_seg_len >= every seg_len
+ * The parts must write disjoint places: no query_row inside a segment's
+ * destination rows, and each probe slot filled by (3) or by one query row.
+ * Results of overlapping writes are unspecified.
+ */
+qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t row_stride,
+                        const void* k_pic, const void* v_pic, int64_t n_pic_rows, int n_seg,
+                        const int32_t* seg_start, const int32_t* seg_len,
+                        const int32_t* seg_delta, const int32_t* src_start, int max_seg_len,
+                        const void* q_new, const void* k_new, const void* v_new,
+                        int64_t n_src_rows, int64_t n_query, const int32_t* query_row,
+                        const int32_t* query_pos, const int32_t* query_src,
+                        const int32_t* query_slot, void* q_u, void* probe_k, void* probe_v,
+                        int64_t n_probe, const int32_t* probe_src, const int32_t* probe_delta,
+                        qcf_dtype dtype, int n_q_heads, int n_kv_heads, int head_dim,
+                        double rope_theta, hipStream_t stream);
+
+/*
  * qcf_probe_scores -- per-token importance of one critical layer,
  * eq. single_layer_importance (Section 3.4.1); with accumulate != 0 the result
  * is added to `scores`, which sums it over the critical layers
@@ -135,7 +174,10 @@ qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
  *   k       [n_kv_rows, k_row_stride] keys at their request positions
  *   cu_q    [batch+1], cu_kv [batch+1], ctx_len [batch] device arrays;
  *   max_q_len >= max_b(cu_q[b+1]-cu_q[b]), max_ctx_len >= max_b ctx_len[b]
- *   workspace  >= qcf_probe_scores_workspace_size(...) bytes, 256-byte aligned
+ *   workspace  >= qcf_probe_scores_workspace_size(...) bytes, 256-byte aligned; it
+ *              holds the per-split softmax statistics between the two kernels and
+ *              needs no initialisation.  Calls that overlap in time need separate
+ *              workspaces.
  */
 size_t qcf_probe_scores_workspace_size(int batch, int max_q_len, int max_ctx_len,
                                        int n_q_heads, int n_kv_heads, int head_dim);
@@ -186,6 +228,8 @@ qcf_status qcf_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
  *        blocks (split-K); the workspace then holds the per-split partial results,
  *        which a second kernel merges in a fixed order (deterministic).  Its contents
  *        need no initialisation; calls that overlap in time need separate workspaces.
+ *        The size query is monotone: the size for (batch, max_rows, max_kv) covers
+ *        every call whose three values do not exceed them (other arguments equal).
  */
 size_t qcf_sparse_prefill_attn_workspace_size(int batch, int max_rows, int max_kv,
                                               int n_q_heads, int n_kv_heads, int head_dim,

@@ -121,6 +121,87 @@ qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
                                            n_kv_heads, head_dim, rope_theta, stream));
 }
 
+qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t row_stride,
+                        const void* k_pic, const void* v_pic, int64_t n_pic_rows, int n_seg,
+                        const int32_t* seg_start, const int32_t* seg_len,
+                        const int32_t* seg_delta, const int32_t* src_start, int max_seg_len,
+                        const void* q_new, const void* k_new, const void* v_new,
+                        int64_t n_src_rows, int64_t n_query, const int32_t* query_row,
+                        const int32_t* query_pos, const int32_t* query_src,
+                        const int32_t* query_slot, void* q_u, void* probe_k, void* probe_v,
+                        int64_t n_probe, const int32_t* probe_src, const int32_t* probe_delta,
+                        qcf_dtype dtype, int n_q_heads, int n_kv_heads, int head_dim,
+                        double rope_theta, hipStream_t stream) {
+  if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
+  qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != QCF_OK) return st;
+  if (n_rows < 0 || n_rows > INT32_MAX || n_pic_rows < 0 || n_pic_rows > INT32_MAX ||
+      n_src_rows < 0 || n_src_rows > INT32_MAX || n_query < 0 || n_query > INT32_MAX ||
+      n_probe < 0 || n_probe > INT32_MAX || n_seg < 0 || max_seg_len < 0)
+    return QCF_ERR_INVALID_ARG;
+  if (row_stride < (int64_t)n_kv_heads * head_dim || (row_stride * esize(dtype)) % 16 != 0)
+    return QCF_ERR_INVALID_ARG;
+  if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
+  const bool no_seg = n_seg == 0 || max_seg_len == 0;
+  const bool no_query = n_query == 0;
+  const bool no_probe = n_probe == 0;
+  const bool cache_used = !no_seg || !no_query;
+  const bool pic_used = !no_seg || !no_probe;
+  if (!tensor_ok(k_cache, !cache_used) || !tensor_ok(v_cache, !cache_used) ||
+      !tensor_ok(k_pic, !pic_used) || !tensor_ok(v_pic, !pic_used))
+    return QCF_ERR_INVALID_ARG;
+  if (!tensor_ok(q_new, no_query) || !tensor_ok(k_new, no_query) || !tensor_ok(v_new, no_query) ||
+      !tensor_ok(q_u, no_query))
+    return QCF_ERR_INVALID_ARG;
+  const bool probe_written = !no_probe || (query_slot != nullptr && !no_query);
+  if (!tensor_ok(probe_k, !probe_written) || !tensor_ok(probe_v, !probe_written))
+    return QCF_ERR_INVALID_ARG;
+  if (!index_ok(seg_start, no_seg) || !index_ok(seg_len, no_seg) || !index_ok(seg_delta, no_seg) ||
+      (src_start && !index_ok(src_start, false)))
+    return QCF_ERR_INVALID_ARG;
+  if (!index_ok(query_row, no_query) || !index_ok(query_pos, no_query) ||
+      (query_src && !index_ok(query_src, false)) || (query_slot && !index_ok(query_slot, false)))
+    return QCF_ERR_INVALID_ARG;
+  if (!index_ok(probe_src, no_probe) || !index_ok(probe_delta, no_probe)) return QCF_ERR_INVALID_ARG;
+  if (no_seg && no_query && no_probe) return QCF_OK;
+  qcf::AssembleShape s{};
+  s.n_rows = n_rows;
+  s.row_stride = row_stride;
+  s.n_pic_rows = n_pic_rows;
+  s.n_src_rows = n_src_rows;
+  s.n_query = n_query;
+  s.n_probe = n_probe;
+  s.n_seg = no_seg ? 0 : n_seg;
+  s.max_seg_len = no_seg ? 0 : max_seg_len;
+  s.hq = n_q_heads;
+  s.hkv = n_kv_heads;
+  s.d = head_dim;
+  s.bf16 = dtype == QCF_BF16;
+  s.theta = rope_theta;
+  qcf::AssemblePtrs p{};
+  p.k_cache = k_cache;
+  p.v_cache = v_cache;
+  p.k_pic = k_pic;
+  p.v_pic = v_pic;
+  p.seg_start = seg_start;
+  p.seg_len = seg_len;
+  p.seg_delta = seg_delta;
+  p.src_start = src_start;
+  p.q_new = q_new;
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.q_u = q_u;
+  p.query_row = query_row;
+  p.query_pos = query_pos;
+  p.query_src = query_src;
+  p.query_slot = query_slot;
+  p.probe_k = probe_k;
+  p.probe_v = probe_v;
+  p.probe_src = probe_src;
+  p.probe_delta = probe_delta;
+  return hip_status(qcf::launch_assemble(s, p, stream));
+}
+
 size_t qcf_probe_scores_workspace_size(int batch, int max_q_len, int max_ctx_len, int n_q_heads,
                                        int n_kv_heads, int head_dim) {
   if (batch < 0 || max_q_len < 0 || max_ctx_len < 0) return 0;

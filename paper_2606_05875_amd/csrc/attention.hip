@@ -26,6 +26,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "qcf_device.h"
 #include "qcf_launch.h"
 
@@ -361,8 +363,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
 }
 
 // Combines the split-K partials of every row tile that was split, in split
-// order (deterministic).  One block per (row tile, KV head); 2 threads per
-// query vector, each owning half of its D outputs.
+// order (deterministic).  One block per (row tile, KV head).  The first 128
+// threads turn each query vector's per-split (max, sum) into normalised split
+// weights in LDS; then the tile's partial outputs, one contiguous [128 x D]
+// float32 array per split, are streamed with consecutive threads on
+// consecutive 32-byte pieces.
+constexpr int kMaxSplit = 16;
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_merge_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, const int32_t* __restrict__ row_pos,
@@ -370,6 +377,7 @@ __global__ __launch_bounds__(kThreads) void attn_merge_kernel(
     int64_t n_kv_rows, int batch, int max_tiles, int hkv, int hq, int lg, int n_split_max,
     int split_tiles, const float* __restrict__ part_o, const float2* __restrict__ part_ml) {
   __shared__ int red[4];
+  __shared__ float wgt[kMaxSplit][128];
   const int L = blockIdx.x;
   const int g = L % hkv;
   const int rest = L / hkv;
@@ -399,40 +407,51 @@ __global__ __launch_bounds__(kThreads) void attn_merge_kernel(
   int nsp = (kv_end + span - 1) / span;
   if (nsp > n_split_max) nsp = n_split_max;
   if (nsp <= 1) return;
-  const int qv = threadIdx.x >> 1, half = threadIdx.x & 1;
-  const int rl = rbase + (qv >> lg);
-  const int64_t grow = r0 + rl;
-  if (rl >= nr || grow >= n_rows) return;
-  const int head = g * G + (qv & (G - 1));
   const int64_t base = (((int64_t)b * max_tiles + tile) * hkv + g) * n_split_max;
-  float mx = -1e30f;
-  for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 128 + qv].x);
-  float acc[D / 2];
-#pragma unroll
-  for (int e = 0; e < D / 2; ++e) acc[e] = 0.f;
-  float lsum = 0.f;
-  for (int sp = 0; sp < nsp; ++sp) {
-    const float2 ml = part_ml[(base + sp) * 128 + qv];
-    const float wsp = __builtin_amdgcn_exp2f(ml.x - mx);
-    lsum += wsp * ml.y;
-    const float* po = part_o + ((base + sp) * 128 + qv) * D + half * (D / 2);
-#pragma unroll
-    for (int e = 0; e < D / 2; e += 4) {
-      const float4 x = *reinterpret_cast<const float4*>(po + e);
-      acc[e] += wsp * x.x;
-      acc[e + 1] += wsp * x.y;
-      acc[e + 2] += wsp * x.z;
-      acc[e + 3] += wsp * x.w;
+  if (threadIdx.x < 128) {
+    const int qv = threadIdx.x;
+    float mx = -1e30f;
+    for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * 128 + qv].x);
+    float lsum = 0.f;
+    for (int sp = 0; sp < nsp; ++sp) {
+      const float2 ml = part_ml[(base + sp) * 128 + qv];
+      const float wsp = __builtin_amdgcn_exp2f(ml.x - mx);
+      wgt[sp][qv] = wsp;
+      lsum += wsp * ml.y;
     }
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+    for (int sp = 0; sp < nsp; ++sp) wgt[sp][qv] *= inv;
+    const int rl = rbase + (qv >> lg);
+    const int64_t grow = r0 + rl;
+    if (lse && rl < nr && grow < n_rows)
+      lse[grow * hq + g * G + (qv & (G - 1))] = lsum > 0.f ? (mx + log2f(lsum)) * kLn2 : -INFINITY;
   }
-  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-  uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D + half * (D / 2);
+  __syncthreads();
+  // 8 consecutive floats per thread and pass; a pass covers 2048 / D query vectors
+  constexpr int kPass = kThreads * 8;
+  const float* pbase = part_o + base * 128 * D;
+#pragma unroll 2
+  for (int e0 = 0; e0 < 128 * D; e0 += kPass) {
+    const int e = e0 + 8 * threadIdx.x;
+    const int qv = e / D, dd = e % D;
+    const int rl = rbase + (qv >> lg);
+    const int64_t grow = r0 + rl;
+    if (rl >= nr || grow >= n_rows) continue;
+    float acc[8];
 #pragma unroll
-  for (int e = 0; e < D / 2; e += 8)
-    *reinterpret_cast<uint4*>(op + e) =
-        make_uint4(pack_bf16x2(acc[e] * inv, acc[e + 1] * inv), pack_bf16x2(acc[e + 2] * inv, acc[e + 3] * inv),
-                   pack_bf16x2(acc[e + 4] * inv, acc[e + 5] * inv), pack_bf16x2(acc[e + 6] * inv, acc[e + 7] * inv));
-  if (lse && half == 0) lse[grow * hq + head] = lsum > 0.f ? (mx + log2f(lsum)) * kLn2 : -INFINITY;
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+    for (int sp = 0; sp < nsp; ++sp) {
+      const float wv = wgt[sp][qv];
+      const float4 x0 = *reinterpret_cast<const float4*>(pbase + (int64_t)sp * 128 * D + e);
+      const float4 x1 = *reinterpret_cast<const float4*>(pbase + (int64_t)sp * 128 * D + e + 4);
+      acc[0] += wv * x0.x; acc[1] += wv * x0.y; acc[2] += wv * x0.z; acc[3] += wv * x0.w;
+      acc[4] += wv * x1.x; acc[5] += wv * x1.y; acc[6] += wv * x1.z; acc[7] += wv * x1.w;
+    }
+    const int head = g * G + (qv & (G - 1));
+    *reinterpret_cast<uint4*>(out + grow * (int64_t)hq * D + (int64_t)head * D + dd) =
+        make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+                   pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
+  }
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -498,6 +517,16 @@ struct SplitPlan {
   int max_tiles, n_split, split_tiles;
   size_t o_off, ml_off, bytes;
 };
+// QCF_ATTN_SPLIT_TILES (read once) overrides the split size for tuning; 0
+// disables splitting, unset (-1) keeps the automatic plan.
+int forced_split_tiles() {
+  static const int forced = [] {
+    const char* e = getenv("QCF_ATTN_SPLIT_TILES");
+    return e ? atoi(e) : -1;
+  }();
+  return forced;
+}
+
 SplitPlan split_plan(const AttnShape& s, bool explicit_pos) {
   SplitPlan p{};
   int lg = 0;
@@ -508,15 +537,10 @@ SplitPlan split_plan(const AttnShape& s, bool explicit_pos) {
   p.n_split = 1;
   p.split_tiles = kv_tiles > 0 ? kv_tiles : 1;
   const double est = 0.5 * (double)p.max_tiles * s.hkv * s.batch * kv_tiles;
-  // QCF_ATTN_SPLIT_TILES (read once) overrides the split size for tuning;
-  // 0 disables splitting
-  static const int forced = [] {
-    const char* e = getenv("QCF_ATTN_SPLIT_TILES");
-    return e ? atoi(e) : -1;
-  }();
+  const int forced = forced_split_tiles();
   if (!explicit_pos && forced > 0 && forced < kv_tiles) {
-    p.split_tiles = forced;
-    p.n_split = (kv_tiles + forced - 1) / forced;
+    p.split_tiles = std::max(forced, (kv_tiles + kMaxSplit - 1) / kMaxSplit);
+    p.n_split = (kv_tiles + p.split_tiles - 1) / p.split_tiles;
   } else if (!explicit_pos && forced < 0 && kv_tiles > 16) {
     int st = (int)((est + 511.0) / 512.0);
     st = st < 16 ? 16 : st;
@@ -542,7 +566,18 @@ SplitPlan split_plan(const AttnShape& s, bool explicit_pos) {
 
 size_t attn_workspace(const AttnShape& s, bool bf16) {
   if (!bf16 || s.batch <= 0 || s.max_rows <= 0) return 0;
-  return split_plan(s, false).bytes;
+  // An upper bound over every call whose batch, max_rows and max_kv do not
+  // exceed these (the split count grows as the row count shrinks).  With G =
+  // max_tiles * hkv * batch row groups, a plan has n_split <= 8 and, since a
+  // split holds at least G * kv_tiles / 1024 tiles, n_split <= 1024 / G + 1.
+  const SplitPlan mx = split_plan(s, false);
+  const int kv_tiles = (s.max_kv + kKT - 1) / kKT;
+  if (kv_tiles <= 16 && mx.n_split <= 1) return 0;
+  const size_t G = (size_t)mx.max_tiles * s.hkv * s.batch;
+  size_t items = std::min(8 * G, 1024 + G);
+  if (forced_split_tiles() > 0) items = G * kMaxSplit;  // a forced split size
+  auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  return a256(items * 128 * s.d * sizeof(float)) + a256(items * 128 * sizeof(float2));
 }
 
 hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
@@ -556,6 +591,7 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
   while ((1 << lg) < s.hq / s.hkv) ++lg;
   if (bf16) {
     const SplitPlan p = split_plan(s, kv_pos != nullptr);
+    if (p.n_split > kMaxSplit) return hipErrorInvalidConfiguration;
     char* wb = static_cast<char*>(ws);
     float* part_o = p.n_split > 1 ? reinterpret_cast<float*>(wb + p.o_off) : nullptr;
     float2* part_ml = p.n_split > 1 ? reinterpret_cast<float2*>(wb + p.ml_off) : nullptr;

@@ -3,22 +3,28 @@
 //
 // I(t) = sum_{i,h} softmax_t(q_{i,h} . k_{t,g(h)} * scale) needs every query
 // row's softmax denominator over all N context keys before any column can be
-// summed, so the bf16 path runs in two passes over the keys:
-//   stats   : grid (query tile, KV head x key split, request).  Each wave holds
-//             32 query vectors of one KV-head group in registers, streams 64-key
-//             tiles of K through LDS and keeps an online (max, sum) per row.
-//   merge   : per query vector, combines the key splits -> (max, 1/sum).
-//   columns : grid (128-key chunk, KV head, request).  Each wave keeps its 32
-//             keys in registers, streams 64-row tiles of the group's queries
-//             (and their stats) through LDS, recomputes the logits and
-//             accumulates probabilities per key; one butterfly across the
-//             wave's lanes finishes the per-key sums.
-//   finish  : sums the KV-head partials in a fixed order and writes (or adds
-//             to) the score vector.
-// QK^T runs on the matrix cores as S^T = K Q^T with v_mfma_f32_32x32x16_bf16:
-// A = 32 keys x 16 d (a 16-byte row slice of K per lane), B = 16 d x 32 query
-// vectors (a 16-byte row slice of Q per lane).  The fp32 path uses the vector
-// ALUs.  Every reduction has a fixed order, so results are deterministic.
+// summed, so the bf16 path runs in two launches:
+//   stats   : grid (128-query-vector tile, KV head x key split, request), at
+//             most 16 key splits.  Each wave holds 32 query vectors of one
+//             KV-head group in registers; the split's keys pass through LDS in
+//             128-key sub-tiles (the next one prefetched into registers while
+//             the current one is in use) and every row keeps an online
+//             (max, sum); the split's base-2 log-sum-exp is written.  The
+//             first split's blocks also store their Q registers in MFMA
+//             operand order, so the column pass reads them contiguously.
+//   columns : grid (32-key chunk, request).  The block's eight waves share out
+//             the (KV head, 32-query-vector) items of the request, one head at
+//             a time per wave; for each item a wave merges the query vectors'
+//             split log-sum-exps in a fixed order, recomputes the logits
+//             against its keys (held in registers per head) and adds the
+//             probabilities 2^(logit - lse) per key.  The waves' per-key sums are added in wave order in LDS and
+//             written (or added) to the scores.
+// No block waits for another: the two launches are the only global
+// synchronisation.  QK^T runs on the matrix cores as S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16: A = 32 keys x 16 d (a 16-byte row slice of K per
+// lane), B = 16 d x 32 query vectors (a 16-byte row slice of Q per lane).  The
+// fp32 path uses the vector ALUs.  Every reduction has a fixed order, so
+// results are deterministic.
 #include <math.h>
 
 #include "qcf_device.h"
@@ -29,13 +35,13 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kQvPerBlock = 128;  // stats pass: 4 waves x 32 query vectors
-constexpr int kKeyTile = 64;      // stats pass K tile
-constexpr int kKeysPerBlock = 128;  // column pass: 4 waves x 32 keys
-constexpr int kQTile = 64;          // column pass Q tile
+constexpr int kSubKeys = 128;     // stats pass: keys per LDS sub-tile
+constexpr int kMaxSplits = 16;    // stats pass: key splits per query tile
+constexpr int kColKeys = 32;      // column pass: keys per block
 
 struct WsLayout {
-  size_t part_off, stats_off, cols_off, total;
-  int n_splits, keys_per_split, max_qv;
+  size_t part_off, frag_off, total;
+  int n_splits, n_sub, max_qv, n_qt;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -44,23 +50,18 @@ WsLayout ws_layout(const ProbeShape& s) {
   WsLayout w{};
   const int grp = s.hq / s.hkv;
   w.max_qv = s.max_q_len * grp;
-  const int row_tiles = (w.max_qv + kQvPerBlock - 1) / kQvPerBlock;
-  const int64_t blocks = (int64_t)row_tiles * s.hkv * s.batch;
-  int want = (int)((1024 + blocks - 1) / (blocks > 0 ? blocks : 1));
-  int cap = (s.max_ctx_len + 511) / 512;
-  if (cap < 1) cap = 1;
-  const int grid_cap = 65535 / (s.hkv > 0 ? s.hkv : 1);
-  if (cap > grid_cap) cap = grid_cap;
-  if (cap < 1) cap = 1;
-  w.n_splits = want < 1 ? 1 : (want > cap ? cap : want);
-  int kps = (s.max_ctx_len + w.n_splits - 1) / w.n_splits;
-  w.keys_per_split = ((kps + kKeyTile - 1) / kKeyTile) * kKeyTile;
-  if (w.keys_per_split == 0) w.keys_per_split = kKeyTile;
+  w.n_qt = (w.max_qv + kQvPerBlock - 1) / kQvPerBlock;
+  const int sub_tiles = (s.max_ctx_len + kSubKeys - 1) / kSubKeys;
+  w.n_sub = (sub_tiles + kMaxSplits - 1) / kMaxSplits;
+  if (w.n_sub < 1) w.n_sub = 1;
+  w.n_splits = (sub_tiles + w.n_sub - 1) / w.n_sub;
+  if (w.n_splits < 1) w.n_splits = 1;
   const size_t nb = (size_t)s.batch * s.hkv;
   w.part_off = 0;
-  w.stats_off = align256(nb * w.n_splits * w.max_qv * sizeof(float2));
-  w.cols_off = w.stats_off + align256(nb * w.max_qv * sizeof(float2));
-  w.total = w.cols_off + align256(nb * (size_t)s.max_ctx_len * sizeof(float));
+  w.frag_off = align256(nb * w.n_splits * w.max_qv * sizeof(float));
+  // Q in MFMA B-fragment order: per (request, head, 32-vector item, 16-wide k
+  // step), the 64 lanes' 16-byte slices back to back
+  w.total = w.frag_off + nb * (size_t)w.n_qt * 4 * (s.d / 16) * 64 * 16;
   return w;
 }
 
@@ -75,29 +76,45 @@ __device__ __forceinline__ float2 combine_ml(float2 a, float2 b) {
 // ---------------------------------------------------------------- bf16 stats
 template <int D>
 __global__ __launch_bounds__(kThreads) void probe_stats_bf16(
-    float2* __restrict__ part, const uint16_t* __restrict__ q, int64_t n_q_rows,
+    float* __restrict__ part, uint16_t* __restrict__ qfrag, const uint16_t* __restrict__ q,
+    int64_t n_q_rows,
     const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
-    const int32_t* __restrict__ ctx_len, int hq, int hkv, int lg, int n_splits,
-    int keys_per_split, int max_qv, float scale2) {
+    const int32_t* __restrict__ ctx_len, int hq, int hkv, int lg, int n_splits, int n_sub,
+    int max_qv, float scale2) {
   constexpr int KSTR = D + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKeyTile * KSTR];
+  constexpr int CPR = D / 8;                        // 16-byte chunks per K row
+  constexpr int PER = kSubKeys * CPR / kThreads;    // chunks per thread per sub-tile
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kSubKeys * KSTR];
 
   const int tile = blockIdx.x;
   const int g = blockIdx.y % hkv, split = blockIdx.y / hkv, b = blockIdx.z;
   const int64_t q0 = cu_q[b];
-  const int nqv = (cu_q[b + 1] - (int)q0) << lg;
+  const int nqv = min((cu_q[b + 1] - (int)q0) << lg, max_qv);
   if (tile * kQvPerBlock >= nqv) return;
   const int64_t k0 = cu_kv[b];
   const int N = ctx_len[b];
-  const int key_lo = split * keys_per_split;
-  const int key_hi = min(N, key_lo + keys_per_split);
+  const int key_lo = split * n_sub * kSubKeys;
+  const int key_hi = min(N, key_lo + n_sub * kSubKeys);
+  const int n_here = key_hi > key_lo ? (key_hi - key_lo + kSubKeys - 1) / kSubKeys : 0;
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
   const int qv = tile * kQvPerBlock + 32 * w + lq;
   const int64_t qrow = q0 + (qv >> lg);
-  const bool valid = qv < nqv && qv < max_qv && qrow < n_q_rows;
+  const bool valid = qv < nqv && qrow < n_q_rows;
   const int head = g * (1 << lg) + (qv & ((1 << lg) - 1));
 
+  uint4 buf[PER];
+  auto fetch = [&](int sub) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * kThreads;
+      const int key = key_lo + sub * kSubKeys + c / CPR, ch = c % CPR;
+      const int64_t row = k0 + key;
+      buf[i] = (key < key_hi && row < n_kv_rows) ? ld16(k + row * k_stride + (int64_t)g * D + ch * 8)
+                                                 : make_uint4(0, 0, 0, 0);
+    }
+  };
+  if (n_here > 0) fetch(0);
   bf16x8 qreg[D / 16];
   {
     const uint16_t* qp = q + qrow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
@@ -105,166 +122,204 @@ __global__ __launch_bounds__(kThreads) void probe_stats_bf16(
     for (int st = 0; st < D / 16; ++st)
       qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
   }
+  if (split == 0) {  // one block per (tile, head, request) stores the fragments
+    const int item = tile * 4 + w;
+    uint16_t* fp = qfrag + ((((int64_t)(b * hkv + g) * gridDim.x * 4 + item) * (D / 16)) * 64 + l) * 8;
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st) st16(fp + st * 64 * 8, __builtin_bit_cast(uint4, qreg[st]));
+  }
   float m = -INFINITY, ls = 0.f;
-  constexpr int CPR = D / 8;  // 16-byte chunks per K row
-  for (int kt0 = key_lo; kt0 < key_hi; kt0 += kKeyTile) {
-    for (int c = threadIdx.x; c < kKeyTile * CPR; c += kThreads) {
-      const int key = c / CPR, ch = c - key * CPR;
-      const int64_t row = k0 + kt0 + key;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kt0 + key < key_hi && row < n_kv_rows) v = ld16(k + row * k_stride + (int64_t)g * D + ch * 8);
-      st16(&k_lds[key * KSTR + ch * 8], v);
+  for (int sub = 0; sub < n_here; ++sub) {
+    if (sub > 0) __syncthreads();  // the previous sub-tile is no longer read
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * kThreads;
+      st16(&k_lds[(c / CPR) * KSTR + (c % CPR) * 8], buf[i]);
     }
     __syncthreads();
-    f32x16 s[2];
+    if (sub + 1 < n_here) fetch(sub + 1);  // in flight during this sub-tile's work
+    // two halves of 64 keys, each folded into the running (max, sum); logits are
+    // scaled into the log2 domain, masked only in the split's last sub-tile
+    const bool tail = key_lo + (sub + 1) * kSubKeys > key_hi;
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-      s[blk] = f32x16{};
+    for (int half = 0; half < kSubKeys / 64; ++half) {
+      const int kt0 = key_lo + sub * kSubKeys + half * 64;
+      f32x16 sacc[2];
 #pragma unroll
-      for (int st = 0; st < D / 16; ++st) {
-        const bf16x8 a = as_bf16x8(ld16(&k_lds[(blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
-        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], s[blk], 0, 0, 0);
+      for (int blk = 0; blk < 2; ++blk) {
+        sacc[blk] = f32x16{};
+#pragma unroll
+        for (int st = 0; st < D / 16; ++st) {
+          const bf16x8 a =
+              as_bf16x8(ld16(&k_lds[(half * 64 + blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
+          sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], sacc[blk], 0, 0, 0);
+        }
       }
-    }
-    float mt = -INFINITY;
+      if (tail) {
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
+        for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kt0 + blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
-        float x = s[blk][v] * scale2;
-        if (key >= key_hi) x = -INFINITY;
-        s[blk][v] = x;
-        mt = fmaxf(mt, x);
+          for (int v = 0; v < 16; ++v)
+            if (kt0 + blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3) >= key_hi) sacc[blk][v] = -INFINITY;
       }
-    const float mn = fmaxf(m, mt);
-    if (mn != -INFINITY) {
-      float acc = 0.f;
+      float mt = -INFINITY;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc += exp2f(s[blk][v] - mn);
-      ls = ls * exp2f(m - mn) + acc;
-      m = mn;
+        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[blk][v]);
+      const float mn = fmaxf(m, mt * scale2);
+      if (mn != -INFINITY) {
+        float acc = 0.f;
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc += __builtin_amdgcn_exp2f(fmaf(sacc[blk][v], scale2, -mn));
+        ls = ls * __builtin_amdgcn_exp2f(m - mn) + acc;
+        m = mn;
+      }
     }
-    __syncthreads();
   }
-  // lanes l and l^32 hold disjoint keys of the same query vector
-  float2 ml = combine_ml(make_float2(m, ls), make_float2(__shfl_xor(m, 32, 64), __shfl_xor(ls, 32, 64)));
+  // lanes l and l^32 hold disjoint keys of the same query vector; the split's
+  // base-2 log-sum-exp log2(sum_t 2^(logit_t)) = max + log2(sum) (-inf: no keys)
+  const float2 ml = combine_ml(make_float2(m, ls), make_float2(__shfl_xor(m, 32, 64), __shfl_xor(ls, 32, 64)));
   if (valid && hi == 0)
-    part[((int64_t)(b * hkv + g) * n_splits + split) * max_qv + qv] = ml;
-}
-
-// ---------------------------------------------------------------- merge
-__global__ __launch_bounds__(kThreads) void probe_merge(const float2* __restrict__ part,
-                                                        float2* __restrict__ stats,
-                                                        const int32_t* __restrict__ cu_q, int hkv,
-                                                        int lg, int n_splits, int max_qv) {
-  const int qv = blockIdx.x * kThreads + threadIdx.x;
-  const int g = blockIdx.y, b = blockIdx.z;
-  const int nqv = (cu_q[b + 1] - cu_q[b]) << lg;
-  if (qv >= nqv || qv >= max_qv) return;
-  const float2* p = part + (int64_t)(b * hkv + g) * n_splits * max_qv + qv;
-  float2 ml = make_float2(-INFINITY, 0.f);
-  for (int s = 0; s < n_splits; ++s) ml = combine_ml(ml, p[(int64_t)s * max_qv]);
-  stats[(int64_t)(b * hkv + g) * max_qv + qv] = make_float2(ml.x, ml.y > 0.f ? 1.f / ml.y : 0.f);
+    part[((int64_t)(b * hkv + g) * n_splits + split) * max_qv + qv] =
+        ml.y > 0.f ? ml.x + __builtin_amdgcn_logf(ml.y) : -INFINITY;
 }
 
 // ---------------------------------------------------------------- bf16 columns
+constexpr int kColWaves = 8;
+
+// Operands of one (KV head, 32-query-vector) item of the column pass: the Q
+// slice (B operand) of the lane's query vector and its per-split log-sum-exps
+// (even splits in lanes 0-31, odd splits in lanes 32-63).
 template <int D>
-__global__ __launch_bounds__(kThreads) void probe_cols_bf16(
-    float* __restrict__ cols, const float2* __restrict__ stats, const uint16_t* __restrict__ q,
-    int64_t n_q_rows, const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
+struct ColItem {
+  bf16x8 q[D / 16];
+  float p[kMaxSplits / 2];
+  bool live;
+};
+
+template <int D>
+__global__ __launch_bounds__(kColWaves * 64) void probe_cols_bf16(
+    float* __restrict__ scores, int accumulate, const float* __restrict__ part,
+    const uint16_t* __restrict__ qfrag, int n_items_max, int64_t n_q_rows,
+    const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
-    const int32_t* __restrict__ ctx_len, int hq, int hkv, int lg, int max_qv, int max_ctx,
+    const int32_t* __restrict__ ctx_len, int hkv, int lg, int n_splits, int max_qv,
     float scale2) {
-  constexpr int QSTR = D + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t q_lds[kQTile * QSTR];
-  __shared__ float2 st_lds[kQTile];
-
-  const int g = blockIdx.y, b = blockIdx.z;
+  __shared__ float red[kColWaves][kColKeys];
+  const int chunk = blockIdx.x, b = blockIdx.y;
   const int N = ctx_len[b];
-  const int kc0 = blockIdx.x * kKeysPerBlock;
-  if (kc0 >= N) return;
-  const int64_t q0 = cu_q[b];
-  const int nqv = (cu_q[b + 1] - (int)q0) << lg;
+  const int kc0 = chunk * kColKeys;
   const int64_t k0 = cu_kv[b];
+  if (kc0 >= N || k0 + kc0 >= n_kv_rows) return;
+  const int64_t q0 = cu_q[b];
+  // query vectors whose rows exist (the rest of a 32-wide item is padding)
+  const int nqv = min(min((cu_q[b + 1] - (int)q0) << lg, max_qv), (int)max<int64_t>(0, n_q_rows - q0) << lg);
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
-  const int kw = kc0 + 32 * w;
+  const int nsub = (nqv + 31) >> 5;
+  // waves per KV head (heads beyond the waves are taken in turns), and this
+  // wave's share of the head's 32-query-vector items
+  const int wpg = hkv >= kColWaves ? 1 : kColWaves / hkv;
+  const int spw = (nsub + wpg - 1) / wpg;
+  const int part_w = w % wpg;
+  const int s0 = part_w * spw, s1 = min(nsub, s0 + spw);
+  // keys past the context (or the tensor) read the last real row; their sums are dropped
+  const int64_t krow = min(k0 + min(kc0 + lq, N - 1), n_kv_rows - 1);
 
-  bf16x8 kreg[D / 16];
-  {
-    const int key = kw + lq;
-    const bool ok = key < N && k0 + key < n_kv_rows;
-    const uint16_t* kp = k + (k0 + key) * k_stride + (int64_t)g * D + 8 * hi;
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st)
-      kreg[st] = as_bf16x8(ok ? ld16(kp + 16 * st) : make_uint4(0, 0, 0, 0));
-  }
-  const float2* stg = stats + (int64_t)(b * hkv + g) * max_qv;
   float col[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) col[v] = 0.f;
 
-  constexpr int CPR = D / 8;
-  for (int qt0 = 0; qt0 < nqv; qt0 += kQTile) {
-    for (int c = threadIdx.x; c < kQTile * CPR; c += kThreads) {
-      const int r = c / CPR, ch = c - r * CPR;
-      const int qv = qt0 + r;
-      const int64_t qrow = q0 + (qv >> lg);
-      const int head = g * (1 << lg) + (qv & ((1 << lg) - 1));
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (qv < nqv && qrow < n_q_rows) v = ld16(q + qrow * (int64_t)hq * D + (int64_t)head * D + ch * 8);
-      st16(&q_lds[r * QSTR + ch * 8], v);
-    }
-    if (threadIdx.x < kQTile) {
-      const int qv = qt0 + threadIdx.x;
-      st_lds[threadIdx.x] = (qv < nqv && qv < max_qv) ? stg[qv] : make_float2(0.f, 0.f);
-    }
-    __syncthreads();
+  if (w < hkv * wpg && s0 < s1) {
+    for (int g = w / wpg; g < hkv; g += kColWaves / wpg) {
+      bf16x8 kreg[D / 16];
+      {
+        const uint16_t* kp = k + krow * k_stride + (int64_t)g * D + 8 * hi;
 #pragma unroll
-    for (int sub = 0; sub < kQTile / 32; ++sub) {
-      f32x16 s = f32x16{};
-#pragma unroll
-      for (int st = 0; st < D / 16; ++st) {
-        const bf16x8 bq = as_bf16x8(ld16(&q_lds[(sub * 32 + lq) * QSTR + 8 * hi + 16 * st]));
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kreg[st], bq, s, 0, 0, 0);
+        for (int st = 0; st < D / 16; ++st) kreg[st] = as_bf16x8(ld16(kp + 16 * st));
       }
-      const float2 ml = st_lds[sub * 32 + lq];  // (max, 1/sum); 1/sum == 0 for padding
+      const float* pg = part + ((int64_t)(b * hkv + g) * n_splits) * max_qv;
+      const uint16_t* fg = qfrag + (int64_t)(b * hkv + g) * n_items_max * (D / 16) * 64 * 8 + l * 8;
+      // every load below is unconditional (indices clamped), so the hardware's
+      // in-order load counter lets two items stay in flight while one is used
+      auto load_item = [&](int sub, ColItem<D>& c) {
+        const int qv_raw = sub * 32 + lq;
+        c.live = sub < s1 && qv_raw < nqv;
+        const int qv = min(qv_raw, nqv - 1);
+        const uint16_t* fp = fg + (int64_t)min(sub, nsub - 1) * (D / 16) * 64 * 8;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) col[v] += exp2f(s[v] * scale2 - ml.x) * ml.y;
+        for (int st = 0; st < D / 16; ++st) c.q[st] = as_bf16x8(ld16(fp + st * 64 * 8));
+#pragma unroll
+        for (int j = 0; j < kMaxSplits / 2; ++j)
+          c.p[j] = pg[(int64_t)min(2 * j + hi, n_splits - 1) * max_qv + qv];
+      };
+      auto use_item = [&](const ColItem<D>& c) {
+        // the query vector's log-sum-exp over all keys from the splits', in a
+        // fixed order: global max, then the even and odd splits' sums (lanes
+        // 0-31 / 32-63), even + odd; copies past the last split are masked
+        float pv[kMaxSplits / 2];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kMaxSplits / 2; ++j) {
+          pv[j] = 2 * j + hi < n_splits ? c.p[j] : -INFINITY;
+          mx = fmaxf(mx, pv[j]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        float ls = 0.f;
+        if (mx != -INFINITY) {
+#pragma unroll
+          for (int j = 0; j < kMaxSplits / 2; ++j) ls += __builtin_amdgcn_exp2f(pv[j] - mx);
+        }
+        const float lo = __shfl_xor(ls, 32, 64);
+        const float lsum = hi == 0 ? ls + lo : lo + ls;
+        // padding (and a request without keys) get a reference that sends every
+        // exponential to 0
+        const float lse = (c.live && lsum > 0.f) ? mx + __builtin_amdgcn_logf(lsum) : 1e30f;
+        f32x16 sacc = f32x16{};
+#pragma unroll
+        for (int st = 0; st < D / 16; ++st)
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kreg[st], c.q[st], sacc, 0, 0, 0);
+        // S^T layout: value v of this lane is key 8(v>>2)+4hi+(v&3) of query vector
+        // lq, whose log-sum-exp this lane holds: probability = 2^(logit - lse)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) col[v] += __builtin_amdgcn_exp2f(fmaf(sacc[v], scale2, -lse));
+      };
+      ColItem<D> ca, cb, cc;
+      load_item(s0, ca);
+      load_item(s0 + 1, cb);
+      for (int sub = s0; sub < s1; sub += 3) {
+        load_item(sub + 2, cc);
+        use_item(ca);
+        load_item(sub + 3, ca);
+        if (sub + 1 < s1) use_item(cb);
+        load_item(sub + 4, cb);
+        if (sub + 2 < s1) use_item(cc);
+      }
     }
-    __syncthreads();
   }
+  // per-key sums over the wave's 32 query-vector columns (lanes with the same hi)
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
 #pragma unroll
     for (int o = 1; o < 32; o <<= 1) col[v] += __shfl_xor(col[v], o, 64);
   }
   if (lq == 0) {
-    float* cg = cols + (int64_t)(b * hkv + g) * max_ctx;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int key = kw + 8 * (v >> 2) + 4 * hi + (v & 3);
-      if (key < N && key < max_ctx) cg[key] = col[v];
+    for (int v = 0; v < 16; ++v) red[w][8 * (v >> 2) + 4 * hi + (v & 3)] = col[v];
+  }
+  __syncthreads();
+  if (threadIdx.x < kColKeys) {
+    const int t = kc0 + threadIdx.x;
+    const int64_t row = k0 + t;
+    if (t < N && row < n_kv_rows) {
+      float acc = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < kColWaves; ++ww) acc += red[ww][threadIdx.x];
+      scores[row] = accumulate ? scores[row] + acc : acc;
     }
   }
-}
-
-// ---------------------------------------------------------------- finish
-__global__ __launch_bounds__(kThreads) void probe_finish(float* __restrict__ scores, int accumulate,
-                                                         const float* __restrict__ cols,
-                                                         const int32_t* __restrict__ cu_kv,
-                                                         const int32_t* __restrict__ ctx_len,
-                                                         int64_t n_kv_rows, int hkv, int max_ctx) {
-  const int t = blockIdx.x * kThreads + threadIdx.x;
-  const int b = blockIdx.y;
-  if (t >= ctx_len[b] || t >= max_ctx) return;
-  const int64_t row = (int64_t)cu_kv[b] + t;
-  if (row >= n_kv_rows) return;
-  float acc = 0.f;
-  for (int g = 0; g < hkv; ++g) acc += cols[(int64_t)(b * hkv + g) * max_ctx + t];
-  scores[row] = accumulate ? scores[row] + acc : acc;
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -385,39 +440,28 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
     return hipGetLastError();
   }
   const WsLayout w = ws_layout(s);
-  char* base = static_cast<char*>(ws);
-  float2* part = reinterpret_cast<float2*>(base + w.part_off);
-  float2* stats = reinterpret_cast<float2*>(base + w.stats_off);
-  float* cols = reinterpret_cast<float*>(base + w.cols_off);
+  if ((int64_t)s.hkv * w.n_splits > 65535) return hipErrorInvalidConfiguration;
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + w.part_off);
+  uint16_t* qfrag = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + w.frag_off);
   const uint16_t* qb = static_cast<const uint16_t*>(q);
   const uint16_t* kb = static_cast<const uint16_t*>(k);
   if (w.max_qv > 0) {
-    dim3 ga((w.max_qv + kQvPerBlock - 1) / kQvPerBlock, s.hkv * w.n_splits, s.batch);
-    if (s.d == 64)
-      probe_stats_bf16<64><<<ga, kThreads, 0, stream>>>(part, qb, n_q_rows, kb, n_kv_rows,
-                                                        k_row_stride, cu_q, cu_kv, ctx_len, s.hq,
-                                                        s.hkv, lg, w.n_splits, w.keys_per_split,
-                                                        w.max_qv, scale2);
-    else
-      probe_stats_bf16<128><<<ga, kThreads, 0, stream>>>(part, qb, n_q_rows, kb, n_kv_rows,
-                                                         k_row_stride, cu_q, cu_kv, ctx_len, s.hq,
-                                                         s.hkv, lg, w.n_splits, w.keys_per_split,
-                                                         w.max_qv, scale2);
-    dim3 gm((w.max_qv + kThreads - 1) / kThreads, s.hkv, s.batch);
-    probe_merge<<<gm, kThreads, 0, stream>>>(part, stats, cu_q, s.hkv, lg, w.n_splits, w.max_qv);
+    dim3 ga(w.n_qt, s.hkv * w.n_splits, s.batch);
+#define QCF_STATS(D)                                                                             \
+  probe_stats_bf16<D><<<ga, kThreads, 0, stream>>>(part, qfrag, qb, n_q_rows, kb, n_kv_rows,     \
+                                                   k_row_stride, cu_q, cu_kv, ctx_len, s.hq,     \
+                                                   s.hkv, lg, w.n_splits, w.n_sub, w.max_qv, scale2)
+    if (s.d == 64) QCF_STATS(64); else QCF_STATS(128);
+#undef QCF_STATS
   }
-  dim3 gc((s.max_ctx_len + kKeysPerBlock - 1) / kKeysPerBlock, s.hkv, s.batch);
-  if (s.d == 64)
-    probe_cols_bf16<64><<<gc, kThreads, 0, stream>>>(cols, stats, qb, n_q_rows, kb, n_kv_rows,
-                                                     k_row_stride, cu_q, cu_kv, ctx_len, s.hq,
-                                                     s.hkv, lg, w.max_qv, s.max_ctx_len, scale2);
-  else
-    probe_cols_bf16<128><<<gc, kThreads, 0, stream>>>(cols, stats, qb, n_q_rows, kb, n_kv_rows,
-                                                      k_row_stride, cu_q, cu_kv, ctx_len, s.hq,
-                                                      s.hkv, lg, w.max_qv, s.max_ctx_len, scale2);
-  dim3 gf((s.max_ctx_len + kThreads - 1) / kThreads, s.batch);
-  probe_finish<<<gf, kThreads, 0, stream>>>(scores, accumulate, cols, cu_kv, ctx_len, n_kv_rows,
-                                            s.hkv, s.max_ctx_len);
+  dim3 gc((s.max_ctx_len + kColKeys - 1) / kColKeys, s.batch);
+#define QCF_COLS(D)                                                                             \
+  probe_cols_bf16<D><<<gc, kColWaves * 64, 0, stream>>>(scores, accumulate, part, qfrag,       \
+                                                  w.n_qt * 4, n_q_rows, kb, n_kv_rows,           \
+                                                  k_row_stride, cu_q, cu_kv, ctx_len, s.hkv, lg,  \
+                                                  w.n_splits, w.max_qv, scale2)
+  if (s.d == 64) QCF_COLS(64); else QCF_COLS(128);
+#undef QCF_COLS
   return hipGetLastError();
 }
 

@@ -32,6 +32,24 @@ hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
                               const int32_t* seg_k, const int32_t* out_start,
                               const int32_t* pos_base, int max_seg_len, hipStream_t stream);
 
+struct AssembleShape {
+  int64_t n_rows, row_stride, n_pic_rows, n_src_rows, n_query, n_probe;
+  int n_seg, max_seg_len, hq, hkv, d;
+  bool bf16;
+  double theta;
+};
+struct AssemblePtrs {
+  void *k_cache, *v_cache;
+  const void *k_pic, *v_pic;
+  const int32_t *seg_start, *seg_len, *seg_delta, *src_start;
+  const void *q_new, *k_new, *v_new;
+  void* q_u;
+  const int32_t *query_row, *query_pos, *query_src, *query_slot;
+  void *probe_k, *probe_v;
+  const int32_t *probe_src, *probe_delta;
+};
+hipError_t launch_assemble(const AssembleShape& s, const AssemblePtrs& p, hipStream_t stream);
+
 struct ProbeShape {
   int batch, max_q_len, max_ctx_len, hq, hkv, d;
 };

@@ -15,7 +15,7 @@ import torch
 
 __all__ = [
     "QcfError", "lib", "lib_path", "qcf_version", "qcf_status_string", "qcf_rerope",
-    "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
+    "qcf_assemble", "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
     "qcf_select_topk", "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
     "EXPORTS",
 ]
@@ -34,6 +34,9 @@ EXPORTS = {
     "qcf_status_string": (ctypes.c_char_p, [_I]),
     "qcf_rerope": (_I, [_P, _P, _P, _P, _I, _I64, _I64, _I, _I, _I64, _I, _P, _P, _P, _P, _I,
                         ctypes.c_double, _P]),
+    "qcf_assemble": (_I, [_P, _P, _I64, _I64, _P, _P, _I64, _I, _P, _P, _P, _P, _I, _P, _P, _P, _I64,
+                          _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I, _I, _I, _I,
+                          ctypes.c_double, _P]),
     "qcf_gather_rows": (_I, [_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _P]),
     "qcf_scatter_kv": (_I, [_P, _P, _I64, _I64, _P, _P, _P, _P, _I64, _P, _I, _I64, _P, _P, _I, _I,
                             _I, ctypes.c_double, _P]),
@@ -144,6 +147,51 @@ def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_the
                           _ptr(seg_start), _ptr(seg_len), _ptr(seg_delta), _ptr(src_start),
                           int(max_seg_len), float(rope_theta), _stream())
     _check(st, "qcf_rerope")
+
+
+def qcf_assemble(k_cache, v_cache, k_pic, v_pic, seg_start, seg_len, seg_delta, max_seg_len,
+                 q_new, k_new, v_new, query_row, query_pos, q_u, probe_k, probe_v, probe_src,
+                 probe_delta, rope_theta, src_start=None, query_src=None, query_slot=None):
+    """One launch: chunk remap + stitch into the cache, query rows rotated into the cache and
+    q_u (and probe slots), anchor rows remapped from the stored chunks into the probe buffer."""
+    dt = k_pic.dtype
+    for n, t in (("k_cache", k_cache), ("v_cache", v_cache), ("k_pic", k_pic), ("v_pic", v_pic),
+                 ("q_new", q_new), ("k_new", k_new), ("v_new", v_new), ("q_u", q_u),
+                 ("probe_k", probe_k), ("probe_v", probe_v)):
+        _dev(t, n, dt)
+    for n, t in (("seg_start", seg_start), ("seg_len", seg_len), ("seg_delta", seg_delta),
+                 ("src_start", src_start), ("query_row", query_row), ("query_pos", query_pos),
+                 ("query_src", query_src), ("query_slot", query_slot), ("probe_src", probe_src),
+                 ("probe_delta", probe_delta)):
+        _i32(t, n)
+    T, hkv, d = k_cache.shape
+    rs = _rows(k_cache, "k_cache")
+    if (v_cache.shape != k_cache.shape or v_cache.stride(0) != rs or k_pic.shape[1:] != (hkv, d)
+            or v_pic.shape != k_pic.shape or k_pic.stride(0) != rs or v_pic.stride(0) != rs):
+        raise QcfError("k_cache/v_cache/k_pic/v_pic must share the row shape and row stride")
+    for n, t in (("q_new", q_new), ("k_new", k_new), ("v_new", v_new), ("q_u", q_u),
+                 ("probe_k", probe_k), ("probe_v", probe_v)):
+        if not t.is_contiguous():
+            raise QcfError(f"{n} must be dense")
+    hq = q_new.shape[1]
+    nq = query_row.numel()
+    if (k_new.shape[1:] != (hkv, d) or v_new.shape != k_new.shape or q_new.shape[0] != k_new.shape[0]
+            or q_new.shape[2] != d or q_u.shape != (nq, hq, d) or query_pos.numel() != nq
+            or (query_src is not None and query_src.numel() != nq)
+            or (query_slot is not None and query_slot.numel() != nq)):
+        raise QcfError("query tensors: q_new [S, H_q, d], k_new/v_new [S, H_kv, d], q_u [n_query, H_q, d]")
+    npb = probe_src.numel()
+    if (probe_k.shape != (npb, hkv, d) or probe_v.shape != probe_k.shape
+            or probe_delta.numel() != npb):
+        raise QcfError("probe_k/probe_v must be [len(probe_src), H_kv, d]")
+    st = lib().qcf_assemble(_ptr(k_cache), _ptr(v_cache), T, rs, _ptr(k_pic), _ptr(v_pic),
+                            k_pic.shape[0], seg_start.numel(), _ptr(seg_start), _ptr(seg_len),
+                            _ptr(seg_delta), _ptr(src_start), int(max_seg_len), _ptr(q_new),
+                            _ptr(k_new), _ptr(v_new), k_new.shape[0], nq, _ptr(query_row),
+                            _ptr(query_pos), _ptr(query_src), _ptr(query_slot), _ptr(q_u),
+                            _ptr(probe_k), _ptr(probe_v), npb, _ptr(probe_src), _ptr(probe_delta),
+                            _dtype(k_pic), hq, hkv, d, float(rope_theta), _stream())
+    _check(st, "qcf_assemble")
 
 
 def qcf_gather_rows(dst, src, idx):
@@ -266,7 +314,7 @@ def qcf_sparse_prefill_attn(out, q, row_pos, cu_rows, k_cache, v_cache, cu_kv, m
     batch = cu_rows.numel() - 1
     need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, hq, hkv, d, q.dtype)
     if workspace is None and need > 0:
-        workspace = torch.zeros(need, dtype=torch.uint8, device=q.device)   # counters start at zero
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     st = lib().qcf_sparse_prefill_attn(_ptr(out), _ptr(lse), _ptr(q), _ptr(row_pos), n, _ptr(cu_rows),
                                        _ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"),
                                        _ptr(cu_kv), _ptr(kv_pos), _dtype(q), batch, int(max_rows),

@@ -10,15 +10,16 @@ synchronisation inside the step.
 
 Sequence of one step (Section 3.5, selective token localization followed by
 one layer of cache fusion):
-  1. qcf_rerope          stored chunk caches -> request cache: keys re-positioned,
-                         values stitched (eq. pic_online)
-  2. qcf_scatter_kv      user-query rows: rotate q/k at N+i, write K/V into the cache
-  3. qcf_gather_rows x2  anchor cache [KV^A ; query K/V] (eq. anchor_cache)
-  4. qcf_sparse_prefill_attn  query probe over the anchor cache (eq. anchor_query_state)
-  5. qcf_probe_scores    I(t) over the context keys (eq. single_layer_importance)
-  6. qcf_select_topk     per-chunk top-k -> P (eq. critical_mask)
-  7. qcf_scatter_kv      rows R = P + query: rotate fresh q/k, write fresh K/V (eq. fuse_cache)
-  8. qcf_sparse_prefill_attn  causal attention of R over the fused cache (Section 2.1.3)
+  1. qcf_assemble        stored chunk caches -> request cache (keys re-positioned,
+                         values stitched, eq. pic_online); user-query rows rotated
+                         at N+i into the cache and q_u; probe buffer
+                         [KV^A ; query K/V] (eq. anchor_cache)
+  2. qcf_sparse_prefill_attn  query probe over the anchor cache (eq. anchor_query_state)
+  3. qcf_probe_scores    I(t) over the context keys (eq. single_layer_importance)
+  4. qcf_select_topk     per-chunk top-k -> P (eq. critical_mask)
+  5. qcf_scatter_kv      rows R = P + query: rotate fresh q/k, write fresh K/V (eq. fuse_cache)
+  6. qcf_sparse_prefill_attn  causal attention of R over the fused cache (Section 2.1.3)
+Step 1 can also run as qcf_rerope + qcf_scatter_kv + two qcf_gather_rows.
 """
 from __future__ import annotations
 
@@ -46,8 +47,11 @@ class FusionPlan:
     pos_base: np.ndarray     # [n_chunks] first cache row of the chunk's request
     u_idx: np.ndarray        # [n_q] cache rows of all query tokens
     u_pos: np.ndarray        # [n_q] positions N_b + i
-    probe_idx: np.ndarray    # [n_probe] cache rows gathered into the probe buffer
+    probe_idx: np.ndarray    # [n_probe] cache rows held by the probe buffer
     probe_pos: np.ndarray    # [n_probe] request positions of those rows
+    probe_src: np.ndarray    # [n_probe] stored-chunk row of an anchor slot, -1 for a query slot
+    probe_delta: np.ndarray  # [n_probe] chunk offset of an anchor slot (0 for a query slot)
+    query_slot: np.ndarray   # [n_q] probe slot of each query token
     cu_probe: np.ndarray     # [B+1]
     max_q: int
     max_ctx: int
@@ -72,6 +76,7 @@ class FusionPlan:
         R_idx = np.full(int(cu_R[-1]), -1, np.int64)
         R_pos = np.full(int(cu_R[-1]), -1, np.int64)
         u_idx, u_pos, probe_idx, probe_pos, cu_probe = [], [], [], [], [0]
+        probe_src, probe_delta, query_slot = [], [], []
         for b in range(B):
             base, N, nq = int(w.cu_kv[b]), int(w.ctx_len[b]), int(w.q_lens[b])
             rows = np.arange(base + N, base + N + nq)
@@ -83,9 +88,14 @@ class FusionPlan:
             u_pos.append(pos)
             segs = np.nonzero(w.seg_req == b)[0]
             arows = [w.seg_start[s] + w.anchor_local[s] for s in segs]
+            adelta = [np.full(len(w.anchor_local[s]), w.seg_delta[s]) for s in segs]
             arows = np.concatenate(arows) if arows else np.zeros(0, np.int64)
+            adelta = np.concatenate(adelta) if adelta else np.zeros(0, np.int64)
             probe_idx += [arows, rows]
             probe_pos += [arows - base, pos]
+            probe_src += [arows, np.full(nq, -1)]
+            probe_delta += [adelta, np.zeros(nq)]
+            query_slot.append(cu_probe[-1] + arows.size + np.arange(nq))
             cu_probe.append(cu_probe[-1] + arows.size + nq)
         cat = lambda xs: np.concatenate(xs).astype(np.int32) if xs else np.zeros(0, np.int32)
         pos_base = w.cu_kv[w.seg_req].astype(np.int32)
@@ -94,6 +104,7 @@ class FusionPlan:
             cu_R=cu_R.astype(np.int32), n_P=n_P, R_idx_init=R_idx.astype(np.int32),
             R_pos_init=R_pos.astype(np.int32), pos_base=pos_base, u_idx=cat(u_idx),
             u_pos=cat(u_pos), probe_idx=cat(probe_idx), probe_pos=cat(probe_pos),
+            probe_src=cat(probe_src), probe_delta=cat(probe_delta), query_slot=cat(query_slot),
             cu_probe=np.array(cu_probe, np.int32), max_q=int(max(w.q_lens) if B else 0),
             max_ctx=int(w.ctx_len.max() if B else 0),
             max_R=int(np.diff(cu_R).max() if B else 0),
@@ -104,7 +115,7 @@ class FusionPlan:
 class FusionStep:
     """Device buffers and the call chain of one layer's fusion step for workload ``w``.
 
-    ``run()`` enqueues the eight stages on the current stream.  The stored
+    ``run()`` enqueues the stages on the current stream.  The stored
     chunk caches (``k_pic``, ``v_pic``) are never modified: re-positioning
     writes the request cache (``k``, ``v``), which then receives the recomputed
     rows, so ``run()`` can be repeated with identical results.
@@ -135,6 +146,8 @@ class FusionStep:
         self.cu_R, self.cu_probe = t(p.cu_R), t(p.cu_probe)
         self.u_idx, self.u_pos = t(p.u_idx), t(p.u_pos)
         self.probe_idx, self.probe_pos = t(p.probe_idx), t(p.probe_pos)
+        self.probe_src, self.probe_delta = t(p.probe_src), t(p.probe_delta)
+        self.query_slot = t(p.query_slot)
         self.R_idx_init, self.R_pos_init = t(p.R_idx_init), t(p.R_pos_init)
         # working state and outputs
         self.k = torch.zeros_like(self.k_pic)
@@ -152,13 +165,30 @@ class FusionStep:
         nws = qcf.qcf_probe_scores_workspace_size(w.batch, p.max_q, p.max_ctx, hq, hkv, d)
         self.ws_scores = torch.empty(max(nws, 256), dtype=torch.uint8, device=dev)
         self.max_kv = int(np.diff(w.cu_kv).max()) if w.batch else 0
-        nwa = qcf.qcf_sparse_prefill_attn_workspace_size(w.batch, max(p.max_R, p.max_probe),
-                                                         max(self.max_kv, 1), hq, hkv, d, dt)
-        # zero-filled once: the split-K counters inside start at zero and every call
-        # leaves them at zero
-        self.ws_attn = torch.zeros(max(nwa, 256), dtype=torch.uint8, device=dev)
+        nwa = qcf.qcf_sparse_prefill_attn_workspace_size(w.batch, p.max_R, max(self.max_kv, 1), hq,
+                                                         hkv, d, dt)
+        self.ws_attn = torch.empty(max(nwa, 256), dtype=torch.uint8, device=dev)
+        nwp = qcf.qcf_sparse_prefill_attn_workspace_size(w.batch, p.max_q, max(p.max_probe, 1), hq,
+                                                         hkv, d, dt)
+        self.ws_probe = torch.empty(max(nwp, 256), dtype=torch.uint8, device=dev)
+        # the anchor probe depends only on the assembled buffers and nothing later in the
+        # step reads its output, so it runs on a second stream (default priority) beside
+        # the score -> select -> scatter chain and is joined at the end of the step
+        self.side = torch.cuda.Stream(device=dev)
+        self.ev_assembled = torch.cuda.Event()
+        self.ev_probed = torch.cuda.Event()
 
     # -- stages ---------------------------------------------------------------
+    def stage_assemble(self):
+        """Request cache (chunks re-positioned, values stitched), query rows, probe buffer."""
+        w, p = self.w, self.plan
+        qcf.qcf_assemble(self.k, self.v, self.k_pic, self.v_pic, self.seg_start, self.seg_len,
+                         self.seg_delta, p.max_seg, self.q_new, self.k_new, self.v_new, self.u_idx,
+                         self.u_pos, self.q_u, self.k_probe, self.v_probe, self.probe_src,
+                         self.probe_delta, w.rope_theta, query_src=self.u_idx,
+                         query_slot=self.query_slot)
+
+    # the same work as three separate calls (kept for the stage-by-stage tests)
     def stage_rerope(self):
         w, p = self.w, self.plan
         qcf.qcf_rerope(self.k, self.k_pic, self.seg_start, self.seg_len, self.seg_delta, p.max_seg,
@@ -176,7 +206,7 @@ class FusionStep:
         p = self.plan
         qcf.qcf_sparse_prefill_attn(self.o_probe, self.q_u, self.u_pos, self.cu_q, self.k_probe,
                                     self.v_probe, self.cu_probe, p.max_q, p.max_probe, self.scale,
-                                    kv_pos=self.probe_pos, workspace=self.ws_attn)
+                                    kv_pos=self.probe_pos, workspace=self.ws_probe)
 
     def stage_scores(self, accumulate=False):
         p = self.plan
@@ -199,18 +229,38 @@ class FusionStep:
                                     self.cu_kv, p.max_R, self.max_kv, self.scale,
                                     workspace=self.ws_attn)
 
-    STAGES = ("rerope", "query_rows", "anchor_gather", "probe_attn", "scores", "select", "scatter",
-              "attn")
+    STAGES = ("assemble", "probe_attn", "scores", "select", "scatter", "attn")
 
-    def run(self):
-        self.stage_rerope()
-        self.stage_query_rows()
-        self.stage_anchor_gather()
-        self.stage_probe_attn()
+    def run_front(self, separate_assembly=False, overlap=True):
+        """Everything before the recomputed-row attention; the probe forks to the side stream."""
+        if separate_assembly:
+            self.stage_rerope()
+            self.stage_query_rows()
+            self.stage_anchor_gather()
+        else:
+            self.stage_assemble()
+        if overlap:
+            main = torch.cuda.current_stream(self.device)
+            self.ev_assembled.record(main)
+            self.side.wait_event(self.ev_assembled)
+            with torch.cuda.stream(self.side):
+                self.stage_probe_attn()
+            self.ev_probed.record(self.side)
+        else:
+            self.stage_probe_attn()
         self.stage_scores()
         self.stage_select()
         self.stage_scatter()
+
+    def join(self, overlap=True):
+        """Make the current stream wait for the probe (before anything reuses its buffers)."""
+        if overlap:
+            torch.cuda.current_stream(self.device).wait_event(self.ev_probed)
+
+    def run(self, separate_assembly=False, overlap=True):
+        self.run_front(separate_assembly, overlap)
         self.stage_attn()
+        self.join(overlap)
 
     # -- results on the host ----------------------------------------------------
     def results(self):

@@ -36,7 +36,8 @@ def L():
 
 def test_every_declared_symbol_is_exported(L):
     decl = _declared()
-    assert set(decl) == {"qcf_version", "qcf_status_string", "qcf_rerope", "qcf_gather_rows",
+    assert set(decl) == {"qcf_version", "qcf_status_string", "qcf_rerope", "qcf_assemble",
+                         "qcf_gather_rows",
                          "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
                          "qcf_select_topk", "qcf_sparse_prefill_attn_workspace_size",
                          "qcf_sparse_prefill_attn"}
@@ -71,6 +72,29 @@ def test_rerope_validation(L):
     # nothing to do: OK without touching the device
     assert L.qcf_rerope(None, None, None, None, BF16, 0, 0, 8, 128, 1024, 0, None, None, None, None,
                         0, 1e4, s) == OK
+
+
+def test_assemble_validation(L):
+    def a(**kw):
+        g = kw.get
+        return [g("kc", A), A, 100, g("stride", 1024), g("kp", A), A, 100, g("nseg", 2), A, A, A,
+                None, 50, g("qn", A), A, A, 100, g("nq", 4), A, A, None, g("slot", None), g("qu", A),
+                g("pk", A), A, g("np_", 8), A, A, g("dt", BF16), g("hq", 32), 8, g("d", 128),
+                g("theta", 1e4), None]
+    assert L.qcf_assemble(*a(dt=7)) == UNSUPPORTED
+    assert L.qcf_assemble(*a(d=96)) == UNSUPPORTED
+    assert L.qcf_assemble(*a(hq=36)) == INVALID
+    assert L.qcf_assemble(*a(stride=1000)) == INVALID
+    assert L.qcf_assemble(*a(theta=0.0)) == INVALID
+    assert L.qcf_assemble(*a(kc=None)) == INVALID                 # cache written by segments
+    assert L.qcf_assemble(*a(kp=MIS)) == INVALID
+    assert L.qcf_assemble(*a(qu=None)) == INVALID                 # query rows need q_u
+    assert L.qcf_assemble(*a(pk=None)) == INVALID                 # probe slots to fill
+    assert L.qcf_assemble(*a(nq=-1)) == INVALID
+    # nothing to do: every pointer may be null
+    assert L.qcf_assemble(None, None, 0, 1024, None, None, 0, 0, None, None, None, None, 0, None,
+                          None, None, 0, 0, None, None, None, None, None, None, None, 0, None, None,
+                          BF16, 32, 8, 128, 1e4, None) == OK
 
 
 def test_gather_validation(L):

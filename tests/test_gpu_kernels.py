@@ -97,6 +97,75 @@ def test_rerope_from_chunk_store():
     assert np.all(gk[-16:] == 0)
 
 
+@pytest.mark.parametrize("dtype,hq,hkv,d", [("bf16", 32, 8, 128), ("bf16", 16, 2, 64), ("f32", 8, 4, 128)])
+def test_assemble(dtype, hq, hkv, d):
+    """One launch: chunk remap + value stitch, query rows, probe buffer (anchors from the store)."""
+    say("assemble", dtype, hq, hkv, d)
+    rng = np.random.default_rng(21)
+    theta = 5e5
+    store_lens = np.array([513, 1, 300, 77, 1024])
+    store_start = np.concatenate([[0], np.cumsum(store_lens + 2)[:-1]])   # gaps in the store
+    S_rows = int(store_start[-1] + store_lens[-1] + 3)
+    pool_k, pool_v = draw(rng, (S_rows, hkv, d), dtype), draw(rng, (S_rows, hkv, d), dtype)
+    order = np.array([4, 1, 0, 3])
+    lens = store_lens[order]
+    seg_start = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    N = int(lens.sum())
+    nq = 37
+    T = N + nq + 5
+    src_start = store_start[order]
+    delta = seg_start.copy()                 # chunk stored at local positions 0..n-1
+    # fresh projections for every cache row (only the query rows are read)
+    kn, vn = draw(rng, (T, hkv, d), dtype), draw(rng, (T, hkv, d), dtype)
+    qn = draw(rng, (T, hq, d), dtype, 3.0)
+    qrow = np.arange(N, N + nq)
+    qpos = qrow.copy()
+    # probe buffer: 3 anchors of each chunk (1 for the 1-row chunk), then the query rows
+    anc_src, anc_delta, anc_req = [], [], []
+    for s_ in range(len(order)):
+        loc = np.sort(rng.choice(lens[s_], min(3, lens[s_]), replace=False))
+        anc_src.append(src_start[s_] + loc)
+        anc_delta.append(np.full(loc.size, delta[s_]))
+        anc_req.append(seg_start[s_] + loc)
+    anc_src, anc_delta, anc_req = map(np.concatenate, (anc_src, anc_delta, anc_req))
+    na = anc_src.size
+    probe_src = np.concatenate([anc_src, np.full(nq, -1)])
+    probe_delta = np.concatenate([anc_delta, np.zeros(nq)])
+    slot = na + np.arange(nq)
+    t = DT[dtype]
+    i32 = lambda a: dev(np.asarray(a, np.int32))
+    kc = torch.full((T, hkv, d), 7.0, dtype=t, device="cuda")
+    vc = torch.full_like(kc, 7.0)
+    qu = torch.empty((nq, hq, d), dtype=t, device="cuda")
+    pk = torch.empty((na + nq, hkv, d), dtype=t, device="cuda")
+    pv = torch.empty_like(pk)
+    qcf.qcf_assemble(kc, vc, dev(pool_k, t), dev(pool_v, t), i32(seg_start), i32(lens), i32(delta),
+                     int(lens.max()), dev(qn, t), dev(kn, t), dev(vn, t), i32(qrow), i32(qpos), qu, pk, pv,
+                     i32(probe_src), i32(probe_delta), theta, src_start=i32(src_start),
+                     query_src=i32(qrow), query_slot=i32(slot))
+    gk, gv = host(kc), host(vc)
+    for s_ in range(len(order)):
+        a, n, src = int(seg_start[s_]), int(lens[s_]), int(src_start[s_])
+        want = Q.rerope(pool_k[src:src + n], [0], [n], [a], theta, dtype)
+        assert_ulp(gk[a:a + n], want, dtype, f"chunk {s_}")
+        np.testing.assert_array_equal(gv[a:a + n], pool_v[src:src + n])
+    wk = Q.round_storage(Q.rope(kn[qrow], qpos, theta), dtype)
+    wq = Q.round_storage(Q.rope(qn[qrow], qpos, theta), dtype)
+    assert_ulp(gk[qrow], wk, dtype, "query K")
+    np.testing.assert_array_equal(gv[qrow], vn[qrow])
+    assert_ulp(host(qu), wq, dtype, "q_u")
+    assert np.all(gk[N + nq:] == 7.0) and np.all(gv[N + nq:] == 7.0)     # untouched rows
+    # probe buffer: anchors = re-positioned stored rows, equal to their cache rows; then the query
+    gpk, gpv = host(pk), host(pv)
+    for j in range(na):
+        wj = Q.rerope(pool_k[anc_src[j]:anc_src[j] + 1], [0], [1], [anc_delta[j]], theta, dtype)
+        assert_ulp(gpk[j:j + 1], wj, dtype, f"anchor {j}")
+    np.testing.assert_array_equal(gpk[:na], gk[anc_req])                    # same bits as the cache rows
+    np.testing.assert_array_equal(gpv[:na], pool_v[anc_src])
+    np.testing.assert_array_equal(gpk[na:], gk[qrow])
+    np.testing.assert_array_equal(gpv[na:], gv[qrow])
+
+
 def test_gather_rows_exact():
     say("gather")
     rng = np.random.default_rng(2)
@@ -170,6 +239,7 @@ def test_select_topk_exact(lens, ks):
     ("bf16", [17, 1, 128], [700, 3000, 129], 32, 8, 128),
     ("bf16", [9], [1000], 8, 8, 64),
     ("bf16", [40], [2500], 64, 8, 128),
+    ("bf16", [8, 3], [20000, 9000], 32, 8, 128),      # several 128-key sub-tiles per split
     ("f32", [32], [512], 8, 2, 64),
 ])
 def test_probe_scores(dtype, nqs, ctxs, hq, hkv, d):
@@ -195,6 +265,30 @@ def test_probe_scores(dtype, nqs, ctxs, hq, hkv, d):
     # accumulate mode adds a second layer's scores; runs are bit-identical
     qcf.qcf_probe_scores(sc, *args, accumulate=True)
     np.testing.assert_array_equal(sc.double().cpu().numpy()[:ctxs[0]], 2 * got[:ctxs[0]])
+
+
+def test_probe_scores_workspace_reuse_across_shapes():
+    """One workspace serves calls of different shapes with results identical to fresh
+    workspaces (nothing in it carries over from call to call)."""
+    say("probe_scores workspace reuse")
+    rng = np.random.default_rng(7)
+    hq, hkv, d = 32, 8, 128
+    shapes = [([64], [5120]), ([5, 33], [300, 2000]), ([128], [777]), ([64], [5120])]
+    big = max(qcf.qcf_probe_scores_workspace_size(len(n), max(n), max(c), hq, hkv, d) for n, c in shapes)
+    ws = torch.full((big,), 0x5A, dtype=torch.uint8, device="cuda")      # garbage to start
+    for nqs, ctxs in shapes:
+        rows = [c + q for c, q in zip(ctxs, nqs)]
+        cu_kv = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+        cu_q = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+        k = draw(rng, (int(cu_kv[-1]), hkv, d), "bf16", 1 / math.sqrt(d))
+        q = draw(rng, (int(cu_q[-1]), hq, d), "bf16", 1.5 * math.sqrt(d))
+        args = (dev(q, torch.bfloat16), dev(k, torch.bfloat16), dev(cu_q), dev(cu_kv),
+                dev(np.array(ctxs, np.int32)), max(nqs), max(ctxs), 1 / math.sqrt(d))
+        a = torch.zeros(int(cu_kv[-1]), device="cuda")
+        b = torch.zeros_like(a)
+        qcf.qcf_probe_scores(a, *args, workspace=ws)
+        qcf.qcf_probe_scores(b, *args)                       # a fresh workspace
+        assert torch.equal(a, b)
 
 
 @pytest.mark.parametrize("dtype,hq,hkv,d,n_kv,n_rows", [

@@ -100,3 +100,19 @@ def test_untouched_rows_bit_identical_and_deterministic():
     g2 = step.results()
     for key in ("k_fuse", "v_fuse", "scores", "R", "o", "o_probe"):
         np.testing.assert_array_equal(g1[key], g2[key])
+
+
+@pytest.mark.parametrize("name", ["c2", "c5"])
+def test_fused_assembly_matches_separate_calls(name):
+    """qcf_assemble gives the same bits as qcf_rerope + qcf_scatter_kv + qcf_gather_rows."""
+    w = make_workload(name)
+    say(name, "fused vs separate assembly")
+    a = FusionStep(w)
+    a.run(separate_assembly=True)
+    g1 = a.results()
+    b = FusionStep(w)
+    b.run()
+    g2 = b.results()
+    for key in ("k_fuse", "v_fuse", "scores", "R", "o", "o_probe", "q_u"):
+        np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)
+    assert torch.equal(a.k_probe, b.k_probe) and torch.equal(a.v_probe, b.v_probe)

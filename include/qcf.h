@@ -224,12 +224,14 @@ qcf_status qcf_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
  *   k_cache, v_cache [n_kv_rows, kv_row_stride]
  *   cu_rows [batch+1], cu_kv [batch+1]; max_rows / max_kv bound the per-request counts
  *   workspace >= qcf_sparse_prefill_attn_workspace_size(...) bytes (may be 0), 256-byte
- *        aligned.  bf16 calls without kv_pos may split long rows' keys over several
- *        blocks (split-K); the workspace then holds the per-split partial results,
- *        which a second kernel merges in a fixed order (deterministic).  Its contents
- *        need no initialisation; calls that overlap in time need separate workspaces.
- *        The size query is monotone: the size for (batch, max_rows, max_kv) covers
- *        every call whose three values do not exceed them (other arguments equal).
+ *        aligned.  A bf16 call without kv_pos that has few row tiles shares the key
+ *        steps of all its row tiles evenly over a fixed grid of blocks; the
+ *        workspace then holds the work plan and the partial results of row tiles
+ *        cut between two blocks, which a second kernel merges in a fixed order
+ *        (deterministic).  Its contents need no initialisation; calls that overlap
+ *        in time need separate workspaces.  The size query is monotone: the size
+ *        for (batch, max_rows, max_kv) covers every call whose three values do
+ *        not exceed them (other arguments equal).
  */
 size_t qcf_sparse_prefill_attn_workspace_size(int batch, int max_rows, int max_kv,
                                               int n_q_heads, int n_kv_heads, int head_dim,

@@ -3,15 +3,12 @@
 // itself included) and, with explicit key positions, the anchor-conditioned
 // query probe (Section 3.3.2, eq. anchor_query_state).
 //
-// bf16 path (matrix cores, flash-style, one pass over the keys):
-//  * a block owns 128 query vectors of one KV head: 128/G consecutive rows of
-//    the request times the G query heads that share the KV head (GQA
-//    packing), 32 vectors per wave;
-//  * the keys 0 .. max(row position in the block) stream through LDS in
-//    64-key tiles that arrive by direct global->LDS DMA (K two tiles ahead, V
-//    one tile ahead; one barrier per tile), and the tile loop is software
-//    pipelined: tile t+1's S^T runs on the matrix cores while tile t's
-//    softmax runs on the vector ALUs;
+// bf16 path (matrix cores, flash-style, one pass over the keys).  Per wave:
+//  * 32 query vectors of one KV head: consecutive rows of the request times
+//    the G query heads that share the KV head (GQA packing);
+//  * the keys stream through LDS in 64-key tiles, and the tile loop is
+//    software pipelined: tile t+1's S^T runs on the matrix cores while tile
+//    t's softmax runs on the vector ALUs;
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (Q stays in registers as the B
 //    operand), so each lane holds 16 logits of ONE query vector: row max,
 //    rescale and row sum stay in the lane plus one lane^32 exchange;
@@ -19,8 +16,12 @@
 //    logit registers (rounded to bf16), V^T from row-major LDS through the
 //    gfx950 transposing LDS read, so V is never transposed in registers;
 //  * online softmax in float32 (base-2 exponentials) with a lazy rescale;
-//    the per-row causal limit masks only tiles that reach past the wave's
-//    smallest position, and waves skip tiles past their largest position.
+//    the causal limit masks only tiles that reach past the wave's smallest
+//    position, and waves skip tiles past their largest position.
+// Recomputed rows run on attn_w8_kernel (8 waves, 256 query vectors, a
+// 4-stage K/V ring filled by buffer loads; a persistent "stream" grid when the
+// row tiles are few and unequal), the probe on attn_pos_kernel (4 waves, K/V
+// by global->LDS loads two and one tiles ahead, key positions from a table).
 // fp32 path (vector ALUs): one wave per (row, head).
 #include <limits.h>
 #include <math.h>
@@ -39,14 +40,13 @@ constexpr int kKT = 64;  // keys per tile
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <int D, bool kPos>
-__global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void attn_pos_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, const uint16_t* __restrict__ q,
     const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, const int32_t* __restrict__ kv_pos,
-    int batch, int max_tiles, int hkv, int hq, int lg, float scale2, int n_split_max,
-    int split_tiles, float* __restrict__ part_o, float2* __restrict__ part_ml) {
+    int batch, int max_tiles, int hkv, int hq, int lg, float scale2) {
   // LDS tiles, row-major, one key per row, filled by global->LDS DMA:
   //  K rows hold D/8 16-byte chunks + 1 pad chunk, so the 16-byte fragment
   //  reads of 8 consecutive keys hit distinct banks;
@@ -57,20 +57,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   constexpr int KI = (KCH + 3) / 4, VI = VCH / 4;  // DMA instructions per wave
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKT * KSTR];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kKT * VSTR];
-  __shared__ int kpos_lds[2][kPos ? kKT : 1];
-  __shared__ int red[4];
+  __shared__ int kpos_lds[2][kKT];
 
   // Block order: consecutive block ids land on consecutive XCDs, so all
-  // blocks of one KV head share an XCD (and its L2); the splits of one row
-  // tile are adjacent; the tiles with the most keys (the last rows of each
-  // request) are dispatched first.
+  // blocks of one KV head share an XCD (and its L2); the tiles with the most
+  // rows are dispatched first.
   const int L = blockIdx.x;
   const int g = L % hkv;
   const int rest = L / hkv;
-  const int split = rest % n_split_max;
-  const int rest2 = rest / n_split_max;
-  const int b = rest2 % batch;
-  const int tile = max_tiles - 1 - rest2 / batch;
+  const int b = rest % batch;
+  const int tile = max_tiles - 1 - rest / batch;
   const int G = 1 << lg;
   const int rpb = 128 >> lg;
   const int64_t r0 = cu_rows[b];
@@ -88,22 +84,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   const bool valid = rl < nr && grow < n_rows;
   const int qpos = valid ? row_pos[grow] : INT_MIN;
 
-  const int wmax = wave_max_i(valid ? qpos : -1);
-  const int wmin = wave_min_i(valid ? qpos : INT_MAX);
-  if (l == 0) red[w] = wmax;
-  __syncthreads();
-  const int bmax = max(max(red[0], red[1]), max(red[2], red[3]));
-  const int kv_end = kPos ? nkv : min(nkv, bmax + 1);
-  const int wave_end = kPos ? nkv : min(nkv, wmax + 1);
-  // split-K: this block covers keys [kt_lo, kt_hi) of the row tile's range;
-  // the last split also takes any remainder
-  const int span = split_tiles * kKT;
-  int nsp = (kv_end + span - 1) / span;
-  if (nsp > n_split_max) nsp = n_split_max;
-  const int kt_lo = split * span;
-  if (split > 0 && kt_lo >= kv_end) return;
-  const int kt_hi = split == nsp - 1 ? kv_end : min(kv_end, kt_lo + span);
-
+  // every key is visited; the mask compares key positions with row positions
+  const int kt_lo = 0, kt_hi = nkv;
+  const int wave_end = nkv;
   bf16x8 qreg[D / 16];
   {
     const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
@@ -174,13 +157,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
         dma(vbase, j * (int)kv_stride + (c < D / 8 ? c * 8 : 0), &v_lds[bfn][(w + 4 * t) * 512]);
       }
     }
-    if (kPos && threadIdx.x < kKT) {
+    if (threadIdx.x < kKT) {
       const int j = kt0 + threadIdx.x;
       kpos_reg = j < nkv ? kv_pos[kv0 + j] : INT_MAX;
     }
   };
   auto kstore = [&](int bfn) {
-    if (kPos && threadIdx.x < kKT) kpos_lds[bfn][threadIdx.x] = kpos_reg;
+    if (threadIdx.x < kKT) kpos_lds[bfn][threadIdx.x] = kpos_reg;
   };
   // Transposing V reads (ds_read_b64_tr_b16): inside each 16-lane group, lane
   // j's element e comes from element (j & 3) of the 4-element segment that
@@ -218,15 +201,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   };
   // masks and running max of one tile (lazy rescale of O)
   auto softmax_pre = [&](f32x16 (&sc)[2], int kt0, int bfc) {
-    const bool need_mask = kPos || kt0 + kKT > wmin || kt0 + kKT > nkv;
-    if (need_mask) {
+    {
 #pragma unroll
       for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int jt = hb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
           const int j = kt0 + jt;
-          const int kp = kPos ? kpos_lds[bfc][jt] : j;
+          const int kp = kpos_lds[bfc][jt];
           if (j >= nkv || kp > qpos) sc[hb][v] = -INFINITY;
         }
     }
@@ -332,40 +314,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
   }
 
   const float lt = ls + __shfl_xor(ls, 32, 64);
-  uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D;
-  if (nsp <= 1) {
-    if (!valid) return;
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-#pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d0 = 32 * mb + 8 * i + 4 * hi;
-        *reinterpret_cast<uint2*>(op + d0) =
-            make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
-                       pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
-      }
-    if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
-    return;
-  }
-  // Several splits: write this split's unnormalised O^T, its (stale) max and
-  // sum; attn_merge_kernel combines the splits after this kernel.
   if (!valid) return;
-  const int64_t item = (((int64_t)b * max_tiles + tile) * hkv + g) * n_split_max + split;
-  float* po = part_o + (item * 128 + qv) * D;
+  uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D;
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<float4*>(po + 32 * mb + 8 * i + 4 * hi) =
-          make_float4(o[mb][4 * i], o[mb][4 * i + 1], o[mb][4 * i + 2], o[mb][4 * i + 3]);
-  if (hi == 0) part_ml[item * 128 + qv] = make_float2(m, lt);
+    for (int i = 0; i < 4; ++i) {
+      const int d0 = 32 * mb + 8 * i + 4 * hi;
+      *reinterpret_cast<uint2*>(op + d0) =
+          make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
+                     pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
+    }
+  if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
 }
 
 // ---------------------------------------------------------------- 8-wave kernel
 // The recomputed-row attention (no explicit key positions) on 8-wave blocks:
 // 256 query vectors per block (256/G rows x the G heads of one KV head), 32
-// per wave, with the same per-wave tile step as attn_bf16_kernel.  One block
+// per wave, with the same per-wave tile step as attn_pos_kernel.  One block
 // fills a CU (two waves per SIMD), which leaves LDS for a 4-stage ring of
 // K/V tiles: K is fetched three tiles ahead and V two tiles ahead, and a step
 // ends by waiting only for the tiles fetched one step earlier, so every
@@ -376,7 +343,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(
 constexpr int kW8 = 8;                // waves per block
 constexpr int kW8Qv = 32 * kW8;       // query vectors per block
 constexpr int kStages = 4;            // LDS ring depth
-constexpr int kW8Slots = 256;         // resident blocks: one per CU
 constexpr uint32_t kOob = 0x80000000u;  // a buffer offset past every descriptor's range
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -406,14 +372,25 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
 }
 
-template <int D>
+// Work of an 8-wave block.  Plain mode: block -> (KV head g, request b, row
+// tile), the tile's whole key range.  Stream mode (few, unequal tiles): a
+// persistent grid of nbg blocks per KV head; the head's key steps -- the
+// 64-key tiles of every row tile of every request, in (request, row tile)
+// order -- are cut into nbg equal contiguous ranges, one per block, so every
+// block does the same amount of work whatever the row positions.  A row tile
+// cut by a range boundary leaves partial results (at most two per block:
+// its first and its last segment) that attn_stream_merge_kernel combines.
+constexpr int kMaxStreamTiles = 256;  // row tiles (requests x tiles) of a stream-mode call
+constexpr int kStreamBlocks = 256;    // persistent blocks (one per CU of MI355X)
+
+template <int D, bool kStream>
 __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, const uint16_t* __restrict__ q,
     const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, int batch, int max_tiles, int hkv,
-    int hq, int lg, float scale2, int n_split_max, int split_tiles, float* __restrict__ part_o,
-    float2* __restrict__ part_ml) {
+    int hq, int lg, float scale2, int nbg, int32_t* __restrict__ plan_out,
+    float* __restrict__ part_o, float2* __restrict__ part_ml) {
   constexpr int KCH = D / 8 + 1, VCH = D / 8 + 4;  // 16-byte chunks per LDS row (padded)
   constexpr int KSTR = KCH * 8, VSTR = VCH * 8;    // bf16 elements per LDS row
   constexpr int KST = kKT * KSTR, VST = kKT * VSTR;  // elements per stage
@@ -423,365 +400,464 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kStages * KST];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[kStages * VST];
   __shared__ int red[kW8];
+  __shared__ int plan_cum[kStream ? kMaxStreamTiles + 1 : 1];
+  __shared__ int plan_end[kStream ? kMaxStreamTiles : 1];
 
-  const int L = blockIdx.x;
-  const int g = L % hkv;
-  const int rest = L / hkv;
-  const int split = rest % n_split_max;
-  const int rest2 = rest / n_split_max;
-  const int b = rest2 % batch;
-  const int tile = max_tiles - 1 - rest2 / batch;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
   const int G = 1 << lg;
   const int rpb = kW8Qv >> lg;
-  const int64_t r0 = cu_rows[b];
-  const int nr = cu_rows[b + 1] - (int)r0;
-  const int rbase = tile * rpb;
-  if (rbase >= nr) return;
-  const int64_t kv0 = cu_kv[b];
-  int nkv = cu_kv[b + 1] - (int)kv0;
-  if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
   const int qv = 32 * w + lq;
-  const int rl = rbase + (qv >> lg);
-  const int head = g * G + (qv & (G - 1));
-  const int64_t grow = r0 + rl;
-  const bool valid = rl < nr && grow < n_rows;
-  const int qpos = valid ? row_pos[grow] : INT_MIN;
+  const int g = blockIdx.x % hkv;
 
-  const int wmax = wave_max_i(valid ? qpos : -1);
-  const int wmin = wave_min_i(valid ? qpos : INT_MAX);
-  if (l == 0) red[w] = wmax;
-  __syncthreads();
-  int bmax = red[0];
-#pragma unroll
-  for (int i = 1; i < kW8; ++i) bmax = max(bmax, red[i]);
-  const int kv_end = min(nkv, bmax + 1);
-  const int wave_end = min(nkv, wmax + 1);
-  const int span = split_tiles * kKT;
-  int nsp = (kv_end + span - 1) / span;
-  if (nsp > n_split_max) nsp = n_split_max;
-  const int kt_lo = split * span;
-  if (split > 0 && kt_lo >= kv_end) return;
-  const int kt_hi = split == nsp - 1 ? kv_end : min(kv_end, kt_lo + span);
-
-  bf16x8 qreg[D / 16];
-  {
-    const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st)
-      qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
-  }
-  f32x16 o[D / 32];
-#pragma unroll
-  for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
-  float m = valid ? -1e30f : INFINITY;
-  float ls = 0.f;
-
-  // descriptors over this request's rows of KV head g: the last byte in range
-  // is the end of the last key's head slice
   const uint32_t row_b = (uint32_t)(kv_stride * 2);
-  const uint32_t range = nkv > 0 ? (uint32_t)(nkv - 1) * row_b + D * 2 : 0u;
-  const i32x4 rk = make_rsrc(kc + kv0 * kv_stride + (int64_t)g * D, range);
-  const i32x4 rv = make_rsrc(vc + kv0 * kv_stride + (int64_t)g * D, range);
-  // this wave's transfer slots j = w + 8 i: slot j < KCH fills K chunks
-  // [64 j, 64 j + 64) of a stage, the others V chunks; lane l of a slot fills
-  // chunk 64 j + l = (row, column) of the padded tile
-  uint32_t soff[SPW];
-#pragma unroll
-  for (int i = 0; i < SPW; ++i) {
-    const int j = w + kW8 * i;
-    const bool isk = j < KCH;
-    const int ci = (isk ? j : j - KCH) * 64 + l;
-    const int ch = isk ? KCH : VCH;
-    const int r = ci / ch, c = ci % ch;
-    soff[i] = (j < NSLOT && c < D / 8) ? (uint32_t)r * row_b + c * 16 : kOob;
-  }
-  const int nslots = w < NFULL ? SPW : SPW - 1;
-  // the transfers of one step: tile r (relative to this split's first tile)
-  // into stage r % 4, K and V; a tile past the split's end reads zeros
-  const int t0 = kt_lo / kKT;
-  const int nt = kt_hi > kt_lo ? (kt_hi - kt_lo + kKT - 1) / kKT : 0;
-  auto issue = [&](int r) {
-    const int sg = r & (kStages - 1);
-    const uint32_t toff = (uint32_t)((t0 + r) * kKT) * row_b;
-#pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      if (i >= nslots) break;
-      const int j = w + kW8 * i;
-      const uint32_t off = r < nt ? soff[i] + toff : kOob;
-      if (j < KCH)
-        dma16(rk, off, k_lds + sg * KST + j * 512);
-      else
-        dma16(rv, off, v_lds + sg * VST + (j - KCH) * 512);
-    }
-  };
-  // end of a step: this step's transfers may stay in flight, all older ones
-  // (and every LDS read) are complete, then the block meets
-  auto step_barrier = [&]() {
-    asm volatile("" ::: "memory");
-    if (w < NFULL) wait_vm_lgkm0<SPW>();
-    else wait_vm_lgkm0<SPW - 1>();
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-  };
-
   const int tg = l >> 4, te = (l >> 2) & 3, tq = l & 3;
   const int vrd = (4 * (tg >> 1) + te) * VSTR + 16 * (tg & 1) + 4 * tq;
   const int krd = lq * KSTR + 8 * hi;
   typedef short v4s __attribute__((ext_vector_type(4)));
   typedef v4s __attribute__((address_space(3))) * lds_v4s;
-  auto read_v = [&](const uint16_t* vl, int hb, bf16x8* vf) {
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) {
-        const uint16_t* p0 = vl + (hb * 32 + 16 * k2) * VSTR + 32 * mb;
-        const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0));
-        const v4s up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0 + 8 * VSTR));
-        vf[k2 * (D / 32) + mb] =
-            __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
-      }
-  };
-  auto qk_half = [&](const uint16_t* kl, int hb, f32x16& sh) {
-    bf16x8 kf[D / 16];
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st) kf[st] = as_bf16x8(ld16(kl + hb * 32 * KSTR + 16 * st));
-    sh = f32x16{};
-#pragma unroll
-    for (int st = 0; st < D / 16; ++st)
-      sh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qreg[st], sh, 0, 0, 0);
-  };
-  auto softmax_pre = [&](f32x16 (&sc)[2], int kt0) {
-    if (kt0 + kKT > wmin || kt0 + kKT > nkv) {
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int j = kt0 + hb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
-          if (j >= nkv || j > qpos) sc[hb][v] = -INFINITY;
-        }
-    }
-    float mt = sc[0][0];
-#pragma unroll
-    for (int hb = 0; hb < 2; ++hb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[hb][v]);
-    {
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt),
-                                                       false, false);
-      mt = fmaxf(mt, fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]))) * scale2;
-    }
-    if (__ballot(mt > m + 8.f)) {
-      const float mn = fmaxf(m, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m - mn);
-      ls *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-      m = mn;
-    }
-  };
   typedef float f32x2_t __attribute__((ext_vector_type(2)));
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-  auto softmax_exp = [&](f32x16 (&sc)[2], bf16x8 (&pb)[2][2]) {
-    const float nm = -m;
-    float psum = 0.f;
+
+  // One segment: keys [kt_lo, kt_hi) of row tile `tile` of request b; the
+  // result is final (slot < 0) or partial slot `slot` of the workspace.
+  auto segment = [&](int b, int tile, int kt_lo, int kt_hi, int64_t slot) {
+    const int64_t r0 = cu_rows[b];
+    const int nr = cu_rows[b + 1] - (int)r0;
+    const int rbase = tile * rpb;
+    const int64_t kv0 = cu_kv[b];
+    int nkv = cu_kv[b + 1] - (int)kv0;
+    if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
+    const int rl = rbase + (qv >> lg);
+    const int head = g * G + (qv & (G - 1));
+    const int64_t grow = r0 + rl;
+    const bool valid = rl < nr && grow < n_rows;
+    const int qpos = valid ? row_pos[grow] : INT_MIN;
+    const int wmax = wave_max_i(valid ? qpos : -1);
+    const int wmin = wave_min_i(valid ? qpos : INT_MAX);
+    const int wave_end = min(nkv, wmax + 1);
+
+    bf16x8 qreg[D / 16];
+    {
+      const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
 #pragma unroll
-    for (int hb = 0; hb < 2; ++hb)
+      for (int st = 0; st < D / 16; ++st)
+        qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
+    }
+    f32x16 o[D / 32];
 #pragma unroll
-      for (int v = 0; v < 16; v += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[hb][v], scale2, nm));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[hb][v + 1], scale2, nm));
-        psum += p0;
-        psum += p1;
-        const bf16x2_t pk = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
-        pb[hb][v >> 3][v & 7] = pk[0];
-        pb[hb][v >> 3][(v & 7) + 1] = pk[1];
+    for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
+    float m = valid ? -1e30f : INFINITY;
+    float ls = 0.f;
+
+    // descriptors over this request's rows of KV head g: the last byte in range
+    // is the end of the last key's head slice
+    const uint32_t range = nkv > 0 ? (uint32_t)(nkv - 1) * row_b + D * 2 : 0u;
+    const i32x4 rk = make_rsrc(kc + kv0 * kv_stride + (int64_t)g * D, range);
+    const i32x4 rv = make_rsrc(vc + kv0 * kv_stride + (int64_t)g * D, range);
+    // this wave's transfer slots j = w + 8 i: slot j < KCH fills K chunks
+    // [64 j, 64 j + 64) of a stage, the others V chunks; lane l of a slot fills
+    // chunk 64 j + l = (row, column) of the padded tile
+    uint32_t soff[SPW];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int j = w + kW8 * i;
+      const bool isk = j < KCH;
+      const int ci = (isk ? j : j - KCH) * 64 + l;
+      const int ch = isk ? KCH : VCH;
+      const int r = ci / ch, c = ci % ch;
+      soff[i] = (j < NSLOT && c < D / 8) ? (uint32_t)r * row_b + c * 16 : kOob;
+    }
+    const int nslots = w < NFULL ? SPW : SPW - 1;
+    // the transfers of one step: tile r (relative to the segment's first tile)
+    // into stage r % 4, K and V; a tile past the segment's end reads zeros
+    const int t0 = kt_lo / kKT;
+    const int nt = kt_hi > kt_lo ? (kt_hi - kt_lo + kKT - 1) / kKT : 0;
+    auto issue = [&](int r) {
+      const int sg = r & (kStages - 1);
+      const uint32_t toff = (uint32_t)((t0 + r) * kKT) * row_b;
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        if (i >= nslots) break;
+        const int j = w + kW8 * i;
+        const uint32_t off = r < nt ? soff[i] + toff : kOob;
+        if (j < KCH)
+          dma16(rk, off, k_lds + sg * KST + j * 512);
+        else
+          dma16(rv, off, v_lds + sg * VST + (j - KCH) * 512);
       }
-    ls += psum;
-  };
-  auto pv = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
-#pragma unroll
-    for (int hb = 0; hb < 2; ++hb) {
-      bf16x8 vf[2 * (D / 32)];
-      read_v(vl, hb, vf);
+    };
+    // end of a step: this step's transfers may stay in flight, all older ones
+    // (and every LDS read) are complete, then the block meets
+    auto step_barrier = [&]() {
+      asm volatile("" ::: "memory");
+      if (w < NFULL) wait_vm_lgkm0<SPW>();
+      else wait_vm_lgkm0<SPW - 1>();
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    };
+    auto read_v = [&](const uint16_t* vl, int hb, bf16x8* vf) {
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-        for (int mb = 0; mb < D / 32; ++mb)
-          o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k2 * (D / 32) + mb], pb[hb][k2],
-                                                          o[mb], 0, 0, 0);
-    }
-  };
-
-  // Ring: K(t) and V(t) live in stage t % 4.  Step t issues tile t+3 into the
-  // stage of tile t-1 (its K was last read in step t-2, its V in step t-1),
-  // computes S(t+1) while the softmax of tile t runs, then O += P(t) V(t); at
-  // its end everything issued before step t -- K(t+2) and V(t+1) among it --
-  // has landed.  Past the last tile the transfers still go out (zeros, no
-  // memory traffic), so every step issues the same number of them.
-  f32x16 sa[2], sb[2];
-  issue(0);
-  issue(1);
-  issue(2);
-  asm volatile("" ::: "memory");
-  wait_vm_lgkm0<0>();
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-  if (nt > 0 && kt_lo < wave_end) {
-    qk_half(k_lds + krd, 0, sa[0]);
-    qk_half(k_lds + krd, 1, sa[1]);
-  }
-  auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
-    const int kt0 = kt_lo + t * kKT;
-    issue(t + 3);
-    const bool do_cur = kt0 < wave_end;
-    const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
-    bf16x8 pb[2][2];
-    if (do_cur) softmax_pre(sc, kt0);
-    if (do_next) {
-      const uint16_t* kn = k_lds + ((t + 1) & 3) * KST + krd;
-      qk_half(kn, 0, sn[0]);
-      qk_half(kn, 1, sn[1]);
-      softmax_exp(sc, pb);
+        for (int mb = 0; mb < D / 32; ++mb) {
+          const uint16_t* p0 = vl + (hb * 32 + 16 * k2) * VSTR + 32 * mb;
+          const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0));
+          const v4s up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0 + 8 * VSTR));
+          vf[k2 * (D / 32) + mb] =
+              __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+    };
+    auto qk_half = [&](const uint16_t* kl, int hb, f32x16& sh) {
+      bf16x8 kf[D / 16];
 #pragma unroll
-      for (int i = 0; i < D / 8; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+      for (int st = 0; st < D / 16; ++st) kf[st] = as_bf16x8(ld16(kl + hb * 32 * KSTR + 16 * st));
+      sh = f32x16{};
+#pragma unroll
+      for (int st = 0; st < D / 16; ++st)
+        sh = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qreg[st], sh, 0, 0, 0);
+    };
+    auto softmax_pre = [&](f32x16 (&sc)[2], int kt0) {
+      if (kt0 + kKT > wmin || kt0 + kKT > nkv) {
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int j = kt0 + hb * 32 + 8 * (v >> 2) + 4 * hi + (v & 3);
+            if (j >= nkv || j > qpos) sc[hb][v] = -INFINITY;
+          }
       }
-    } else if (do_cur) {
-      softmax_exp(sc, pb);
-    }
-    if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
-    step_barrier();
-  };
-  for (int t = 0; t < nt; t += 2) {
-    step(t, sa, sb);
-    if (t + 1 < nt) step(t + 1, sb, sa);
-  }
-  // drain the last (zero-row) transfers before the block's LDS can be reused
-  asm volatile("" ::: "memory");
-  wait_vm_lgkm0<0>();
+      float mt = sc[0][0];
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[hb][v]);
+      {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt),
+                                                         false, false);
+        mt = fmaxf(mt, fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]))) * scale2;
+      }
+      if (__ballot(mt > m + 8.f)) {
+        const float mn = fmaxf(m, mt);
+        const float alpha = __builtin_amdgcn_exp2f(m - mn);
+        ls *= alpha;
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+        m = mn;
+      }
+    };
+    auto softmax_exp = [&](f32x16 (&sc)[2], bf16x8 (&pb)[2][2]) {
+      const float nm = -m;
+      float psum = 0.f;
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int v = 0; v < 16; v += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[hb][v], scale2, nm));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[hb][v + 1], scale2, nm));
+          psum += p0;
+          psum += p1;
+          const bf16x2_t pk = __builtin_convertvector((f32x2_t){p0, p1}, bf16x2_t);
+          pb[hb][v >> 3][v & 7] = pk[0];
+          pb[hb][v >> 3][(v & 7) + 1] = pk[1];
+        }
+      ls += psum;
+    };
+    auto pv = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        bf16x8 vf[2 * (D / 32)];
+        read_v(vl, hb, vf);
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int mb = 0; mb < D / 32; ++mb)
+            o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k2 * (D / 32) + mb], pb[hb][k2],
+                                                            o[mb], 0, 0, 0);
+      }
+    };
 
-  const float lt = ls + __shfl_xor(ls, 32, 64);
-  uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D;
-  if (nsp <= 1) {
+    // Ring: K(t) and V(t) live in stage t % 4.  Step t issues tile t+3 into the
+    // stage of tile t-1 (its K was last read in step t-2, its V in step t-1),
+    // computes S(t+1) while the softmax of tile t runs, then O += P(t) V(t); at
+    // its end everything issued before step t -- K(t+2) and V(t+1) among it --
+    // has landed.  Past the last tile the transfers still go out (zeros, no
+    // memory traffic), so every step issues the same number of them.
+    f32x16 sa[2], sb[2];
+    issue(0);
+    issue(1);
+    issue(2);
+    asm volatile("" ::: "memory");
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (nt > 0 && kt_lo < wave_end) {
+      qk_half(k_lds + krd, 0, sa[0]);
+      qk_half(k_lds + krd, 1, sa[1]);
+    }
+    auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
+      const int kt0 = kt_lo + t * kKT;
+      issue(t + 3);
+      const bool do_cur = kt0 < wave_end;
+      const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
+      bf16x8 pb[2][2];
+      if (do_cur) softmax_pre(sc, kt0);
+      if (do_next) {
+        const uint16_t* kn = k_lds + ((t + 1) & 3) * KST + krd;
+        qk_half(kn, 0, sn[0]);
+        qk_half(kn, 1, sn[1]);
+        softmax_exp(sc, pb);
+#pragma unroll
+        for (int i = 0; i < D / 8; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        }
+      } else if (do_cur) {
+        softmax_exp(sc, pb);
+      }
+      if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
+      step_barrier();
+    };
+    for (int t = 0; t < nt; t += 2) {
+      step(t, sa, sb);
+      if (t + 1 < nt) step(t + 1, sb, sa);
+    }
+    // drain the last (zero-row) transfers before the LDS is refilled or released
+    asm volatile("" ::: "memory");
+    wait_vm_lgkm0<0>();
+
+    const float lt = ls + __shfl_xor(ls, 32, 64);
     if (!valid) return;
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    if (slot < 0) {
+      uint16_t* op = out + grow * (int64_t)hq * D + (int64_t)head * D;
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d0 = 32 * mb + 8 * i + 4 * hi;
+          *reinterpret_cast<uint2*>(op + d0) =
+              make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
+                         pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
+        }
+      if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
+      return;
+    }
+    // partials bypass the L2 (non-temporal): they are read once, by the
+    // merge kernel, and would otherwise evict the K/V tiles other blocks of
+    // this head are still streaming
+    float* po = part_o + (slot * kW8Qv + qv) * D;
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int d0 = 32 * mb + 8 * i + 4 * hi;
-        *reinterpret_cast<uint2*>(op + d0) =
-            make_uint2(pack_bf16x2(o[mb][4 * i] * inv, o[mb][4 * i + 1] * inv),
-                       pack_bf16x2(o[mb][4 * i + 2] * inv, o[mb][4 * i + 3] * inv));
+        f32x4 v4 = {o[mb][4 * i], o[mb][4 * i + 1], o[mb][4 * i + 2], o[mb][4 * i + 3]};
+        __builtin_nontemporal_store(v4, reinterpret_cast<f32x4*>(po + 32 * mb + 8 * i + 4 * hi));
       }
-    if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
+    if (hi == 0) {
+      __builtin_nontemporal_store(m, &part_ml[slot * kW8Qv + qv].x);
+      __builtin_nontemporal_store(lt, &part_ml[slot * kW8Qv + qv].y);
+    }
+  };
+
+  if (!kStream) {
+    // plain: this block's row tile, all of its keys (up to its largest row position)
+    const int rest = blockIdx.x / hkv;
+    const int b = rest % batch;
+    const int tile = max_tiles - 1 - rest / batch;
+    const int64_t r0 = cu_rows[b];
+    const int nr = cu_rows[b + 1] - (int)r0;
+    if (tile * rpb >= nr) return;
+    const int64_t kv0 = cu_kv[b];
+    int nkv = cu_kv[b + 1] - (int)kv0;
+    if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
+    const int rl = tile * rpb + (qv >> lg);
+    const int mx = wave_max_i(rl < nr && r0 + rl < n_rows ? row_pos[r0 + rl] : -1);
+    if (l == 0) red[w] = mx;
+    __syncthreads();
+    int bmax = red[0];
+#pragma unroll
+    for (int i = 1; i < kW8; ++i) bmax = max(bmax, red[i]);
+    segment(b, tile, 0, min(nkv, bmax + 1), -1);
     return;
   }
-  if (!valid) return;
-  const int64_t item = (((int64_t)b * max_tiles + tile) * hkv + g) * n_split_max + split;
-  float* po = part_o + (item * kW8Qv + qv) * D;
+
+  // stream: the plan (key end and step count of every row tile), built by
+  // each block in LDS: wave w takes tiles w, w+8, ...; its lanes split the rows
+  const int n_tiles = batch * max_tiles;
+  for (int i = w; i < n_tiles; i += kW8) {
+    const int b = i / max_tiles, tile = i - b * max_tiles;
+    const int64_t r0 = cu_rows[b];
+    const int nr = cu_rows[b + 1] - (int)r0;
+    const int64_t kv0 = cu_kv[b];
+    int nkv = cu_kv[b + 1] - (int)kv0;
+    if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
+    int mx = -1;
+    for (int rr = tile * rpb + l; rr < min(nr, (tile + 1) * rpb); rr += 64)
+      if (r0 + rr < n_rows) mx = max(mx, row_pos[r0 + rr]);
+    mx = wave_max_i(mx);
+    if (l == 0) plan_end[i] = max(0, min(nkv, mx + 1));
+  }
+  __syncthreads();
+  if (w == 0) {
+    // exclusive scan of the step counts (kMaxStreamTiles / 64 tiles per lane)
+    constexpr int PL = kMaxStreamTiles / 64;
+    int loc[PL], sum = 0;
 #pragma unroll
-  for (int mb = 0; mb < D / 32; ++mb)
+    for (int k = 0; k < PL; ++k) {
+      const int i = l * PL + k;
+      loc[k] = i < n_tiles ? (plan_end[i] + kKT - 1) / kKT : 0;
+      sum += loc[k];
+    }
+    int incl = sum;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<float4*>(po + 32 * mb + 8 * i + 4 * hi) =
-          make_float4(o[mb][4 * i], o[mb][4 * i + 1], o[mb][4 * i + 2], o[mb][4 * i + 3]);
-  if (hi == 0) part_ml[item * kW8Qv + qv] = make_float2(m, lt);
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (l >= o) incl += y;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int k = 0; k < PL; ++k) {
+      const int i = l * PL + k;
+      if (i < n_tiles) plan_cum[i] = run;
+      run += loc[k];
+    }
+    if (l == 63) plan_cum[n_tiles] = incl;
+  }
+  __syncthreads();
+  if (blockIdx.x == 0) {  // the merge kernel reads the same plan
+    for (int i = threadIdx.x; i <= n_tiles; i += kW8 * 64) plan_out[i] = plan_cum[i];
+    for (int i = threadIdx.x; i < n_tiles; i += kW8 * 64) plan_out[kMaxStreamTiles + 1 + i] = plan_end[i];
+  }
+  const int r = blockIdx.x / hkv;
+  const int64_t S = plan_cum[n_tiles];
+  int lo = (int)(r * S / nbg);
+  const int hi_s = (int)((r + 1) * S / nbg);
+  int i = 0;
+  bool first = true;
+  while (lo < hi_s) {
+    while (plan_cum[i + 1] <= lo) ++i;  // skip tiles without steps
+    const int c0 = plan_cum[i], c1 = plan_cum[i + 1];
+    const int seg_end = min(hi_s, c1);
+    const int b = i / max_tiles, tile = i - b * max_tiles;
+    const bool whole = lo == c0 && seg_end == c1;
+    const int64_t slot = whole ? -1 : ((int64_t)(g * nbg + r) * 2 + (first ? 0 : 1));
+    segment(b, tile, (lo - c0) * kKT, min(plan_end[i], (seg_end - c0) * kKT), slot);
+    lo = seg_end;
+    first = false;
+  }
 }
 
-// Combines the split-K partials of every row tile that was split, in split
-// order (deterministic).  One block per (row tile, KV head), QV query vectors
-// per tile.  The block first turns each query vector's per-split (max, sum)
-// into normalised split weights in LDS; then the tile's partial outputs, one
-// contiguous [QV x D] float32 array per split, are streamed with consecutive
-// threads on consecutive 32-byte pieces.
-constexpr int kMaxSplit = 16;
-
-template <int D, int QV>
-__global__ __launch_bounds__(kThreads) void attn_merge_kernel(
-    uint16_t* __restrict__ out, float* __restrict__ lse, const int32_t* __restrict__ row_pos,
-    int64_t n_rows, const int32_t* __restrict__ cu_rows, const int32_t* __restrict__ cu_kv,
-    int64_t n_kv_rows, int batch, int max_tiles, int hkv, int hq, int lg, int n_split_max,
-    int split_tiles, const float* __restrict__ part_o, const float2* __restrict__ part_ml) {
-  static_assert(QV == 128 || QV == 256, "tile width");
-  __shared__ int red[4];
-  __shared__ float wgt[kMaxSplit][QV];
-  const int L = blockIdx.x;
-  const int g = L % hkv;
-  const int rest = L / hkv;
-  const int b = rest % batch;
-  const int tile = max_tiles - 1 - rest / batch;
+// Combines the stream-mode partials of each row tile that a range boundary
+// cut: the blocks r_first .. r_last of the tile's KV head each hold one
+// segment (in slot 0 if the segment is the block's first, else slot 1); they
+// are combined in block order (deterministic).  One block per (row tile, KV
+// head).
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
+    uint16_t* __restrict__ out, float* __restrict__ lse, int64_t n_rows,
+    const int32_t* __restrict__ cu_rows, int batch, int max_tiles, int hkv, int hq, int lg,
+    int nbg, const int32_t* __restrict__ plan, const float* __restrict__ part_o,
+    const float2* __restrict__ part_ml) {
+  constexpr int QV = kW8Qv;
+  constexpr int QQ = QV / 4;  // query vectors per merge block (a quarter of the tile)
+  constexpr int WS = 8;       // split weights kept in LDS; later ones are recomputed
+  __shared__ float wgt[WS][QQ];
+  __shared__ float mxq[QQ], invq[QQ];
+  __shared__ int64_t slot_l[kStreamBlocks];
+  __shared__ int nsp_l;
+  const int quarter = blockIdx.x & 3;
+  const int i = (blockIdx.x >> 2) / hkv, g = (blockIdx.x >> 2) % hkv;
+  const int n_tiles = batch * max_tiles;
+  if (i >= n_tiles) return;
+  const int64_t S = plan[n_tiles];
+  const int c0 = plan[i], c1 = plan[i + 1];
+  if (c1 <= c0 || S == 0) return;
+  // block holding step x: the largest r with floor(r S / nbg) <= x
+  auto owner = [&](int x) {
+    int a = 0, z = nbg - 1;
+    while (a < z) {
+      const int mid = (a + z + 1) >> 1;
+      if ((int)((int64_t)mid * S / nbg) <= x) a = mid; else z = mid - 1;
+    }
+    return a;
+  };
+  const int rf = owner(c0), rlst = owner(c1 - 1);
+  if (rf == rlst) return;  // one block did the whole tile
+  // the blocks with a non-empty range between them, in order (with fewer steps
+  // than blocks some ranges are empty); the first block's segment sits in its
+  // slot 1 when its range began before this tile, every other one's in slot 0
+  if (threadIdx.x == 0) {
+    int n = 0;
+    for (int rr = rf; rr <= rlst; ++rr) {
+      const int lo_r = (int)((int64_t)rr * S / nbg), hi_r = (int)((int64_t)(rr + 1) * S / nbg);
+      if (hi_r <= lo_r) continue;
+      slot_l[n++] = (int64_t)(g * nbg + rr) * 2 + (lo_r < c0 ? 1 : 0);
+    }
+    nsp_l = n;
+  }
+  __syncthreads();
+  const int nsp = nsp_l;
+  const int b = i / max_tiles, tile = i - b * max_tiles;
   const int G = 1 << lg;
   const int rpb = QV >> lg;
   const int64_t r0 = cu_rows[b];
   const int nr = cu_rows[b + 1] - (int)r0;
   const int rbase = tile * rpb;
-  if (rbase >= nr) return;
-  const int64_t kv0 = cu_kv[b];
-  int nkv = cu_kv[b + 1] - (int)kv0;
-  if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
-  // the same key range (and split count) as the attention kernel's blocks
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  {
-    int mx = -1;
-    for (int qv = 64 * w + l; qv < QV; qv += kThreads) {
-      const int rl = rbase + (qv >> lg);
-      if (rl < nr && r0 + rl < n_rows) mx = max(mx, row_pos[r0 + rl]);
-    }
-    mx = wave_max_i(mx);
-    if (l == 0) red[w] = mx;
-  }
-  __syncthreads();
-  const int kv_end = min(nkv, max(max(red[0], red[1]), max(red[2], red[3])) + 1);
-  const int span = split_tiles * kKT;
-  int nsp = (kv_end + span - 1) / span;
-  if (nsp > n_split_max) nsp = n_split_max;
-  if (nsp <= 1) return;
-  const int64_t base = (((int64_t)b * max_tiles + tile) * hkv + g) * n_split_max;
-  for (int qv = threadIdx.x; qv < QV; qv += kThreads) {
+  const int qv0 = quarter * QQ;
+  if (threadIdx.x < QQ) {
+    const int qv = qv0 + threadIdx.x;
     float mx = -1e30f;
-    for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[(base + sp) * QV + qv].x);
+    for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[slot_l[sp] * QV + qv].x);
     float lsum = 0.f;
     for (int sp = 0; sp < nsp; ++sp) {
-      const float2 ml = part_ml[(base + sp) * QV + qv];
+      const float2 ml = part_ml[slot_l[sp] * QV + qv];
       const float wsp = __builtin_amdgcn_exp2f(ml.x - mx);
-      wgt[sp][qv] = wsp;
+      if (sp < WS) wgt[sp][threadIdx.x] = wsp;
       lsum += wsp * ml.y;
     }
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    for (int sp = 0; sp < nsp; ++sp) wgt[sp][qv] *= inv;
+    for (int sp = 0; sp < nsp && sp < WS; ++sp) wgt[sp][threadIdx.x] *= inv;
+    mxq[threadIdx.x] = mx;
+    invq[threadIdx.x] = inv;
     const int rl = rbase + (qv >> lg);
     const int64_t grow = r0 + rl;
     if (lse && rl < nr && grow < n_rows)
       lse[grow * hq + g * G + (qv & (G - 1))] = lsum > 0.f ? (mx + log2f(lsum)) * kLn2 : -INFINITY;
   }
   __syncthreads();
-  // 8 consecutive floats per thread and pass; a pass covers 2048 / D query vectors
+  // QQ x D outputs, 8 consecutive ones per thread and pass, all passes in flight
   constexpr int kPass = kThreads * 8;
-  const float* pbase = part_o + base * QV * D;
-#pragma unroll 2
-  for (int e0 = 0; e0 < QV * D; e0 += kPass) {
-    const int e = e0 + 8 * threadIdx.x;
-    const int qv = e / D, dd = e % D;
+  constexpr int NP = QQ * D / kPass;
+  float acc[NP][8];
+#pragma unroll
+  for (int p = 0; p < NP; ++p)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[p][k] = 0.f;
+  for (int sp = 0; sp < nsp; ++sp) {
+    const float* pp = part_o + (slot_l[sp] * QV + qv0) * D;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int e = p * kPass + 8 * threadIdx.x;
+      const int ql = e / D;
+      const float wv = sp < WS ? wgt[sp][ql]
+                               : __builtin_amdgcn_exp2f(part_ml[slot_l[sp] * QV + qv0 + ql].x - mxq[ql]) * invq[ql];
+      const float4 x0 = *reinterpret_cast<const float4*>(pp + e);
+      const float4 x1 = *reinterpret_cast<const float4*>(pp + e + 4);
+      acc[p][0] += wv * x0.x; acc[p][1] += wv * x0.y; acc[p][2] += wv * x0.z; acc[p][3] += wv * x0.w;
+      acc[p][4] += wv * x1.x; acc[p][5] += wv * x1.y; acc[p][6] += wv * x1.z; acc[p][7] += wv * x1.w;
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int e = p * kPass + 8 * threadIdx.x;
+    const int qv = qv0 + e / D, dd = e % D;
     const int rl = rbase + (qv >> lg);
     const int64_t grow = r0 + rl;
     if (rl >= nr || grow >= n_rows) continue;
-    float acc[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-    for (int sp = 0; sp < nsp; ++sp) {
-      const float wv = wgt[sp][qv];
-      const float4 x0 = *reinterpret_cast<const float4*>(pbase + (int64_t)sp * QV * D + e);
-      const float4 x1 = *reinterpret_cast<const float4*>(pbase + (int64_t)sp * QV * D + e + 4);
-      acc[0] += wv * x0.x; acc[1] += wv * x0.y; acc[2] += wv * x0.z; acc[3] += wv * x0.w;
-      acc[4] += wv * x1.x; acc[5] += wv * x1.y; acc[6] += wv * x1.z; acc[7] += wv * x1.w;
-    }
     const int head = g * G + (qv & (G - 1));
     *reinterpret_cast<uint4*>(out + grow * (int64_t)hq * D + (int64_t)head * D + dd) =
-        make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
-                   pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
+        make_uint4(pack_bf16x2(acc[p][0], acc[p][1]), pack_bf16x2(acc[p][2], acc[p][3]),
+                   pack_bf16x2(acc[p][4], acc[p][5]), pack_bf16x2(acc[p][6], acc[p][7]));
   }
 }
 
@@ -839,78 +915,41 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(
   if (lse && l == 0) lse[r * hq + h] = ls > 0.f ? (m + log2f(ls)) * kLn2 : -INFINITY;
 }
 
-// Split-K plan of the bf16 kernels (explicit-position calls never split).
-// The estimate of the total work assumes row positions spread over each
-// request (a triangle of key tiles).  A split holds about as many key tiles
-// as one block slot of the chip gets on average (256 slots for the 8-wave
-// kernel: one block per CU), at least 16, and at most 8 splits per row tile.
-struct SplitPlan {
-  int max_tiles, n_split, split_tiles;
-  size_t o_off, ml_off, bytes;
-};
-// QCF_ATTN_SPLIT_TILES (read once) overrides the split size for tuning; 0
-// disables splitting, unset (-1) keeps the automatic plan.
-int forced_split_tiles() {
-  static const int forced = [] {
-    const char* e = getenv("QCF_ATTN_SPLIT_TILES");
-    return e ? atoi(e) : -1;
-  }();
-  return forced;
+// Stream mode is used when the plain grid would not fill the chip twice over
+// and the row tiles fit the block's plan.  Its workspace: the plan (step
+// prefix sums and key ends of up to kMaxStreamTiles row tiles) and two
+// partial slots per block.
+
+bool use_stream(const AttnShape& s, int max_tiles) {
+  const int64_t plain_blocks = (int64_t)max_tiles * s.batch * s.hkv;
+  return plain_blocks < 2 * kStreamBlocks && (int64_t)max_tiles * s.batch <= kMaxStreamTiles &&
+         s.max_kv > kKT;
 }
 
-// qv: query vectors per block; slots: blocks the chip holds at once
-SplitPlan split_plan(const AttnShape& s, bool explicit_pos, int qv, int slots) {
-  SplitPlan p{};
-  int lg = 0;
-  while ((1 << lg) < s.hq / s.hkv) ++lg;
-  const int rpb = qv >> lg;
-  p.max_tiles = (s.max_rows + rpb - 1) / rpb;
-  const int kv_tiles = (s.max_kv + kKT - 1) / kKT;
-  p.n_split = 1;
-  p.split_tiles = kv_tiles > 0 ? kv_tiles : 1;
-  const double est = 0.5 * (double)p.max_tiles * s.hkv * s.batch * kv_tiles;
-  const int forced = forced_split_tiles();
-  if (!explicit_pos && forced > 0 && forced < kv_tiles) {
-    p.split_tiles = std::max(forced, (kv_tiles + kMaxSplit - 1) / kMaxSplit);
-    p.n_split = (kv_tiles + p.split_tiles - 1) / p.split_tiles;
-  } else if (!explicit_pos && forced < 0 && kv_tiles > 16) {
-    int st = (int)((est + slots - 1.0) / slots);
-    st = st < 16 ? 16 : st;
-    const int min_st = (kv_tiles + 7) / 8;
-    st = st < min_st ? min_st : st;
-    if (st < kv_tiles) {
-      p.split_tiles = st;
-      p.n_split = (kv_tiles + st - 1) / st;
-    }
-  }
-  if (p.n_split > 1) {
-    const size_t groups = (size_t)p.max_tiles * s.hkv * s.batch;
-    const size_t items = groups * p.n_split;
-    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    p.o_off = 0;
-    p.ml_off = a256(items * qv * s.d * sizeof(float));
-    p.bytes = p.ml_off + a256(items * qv * sizeof(float2));
-  }
-  return p;
+struct StreamLayout {
+  int nbg;
+  size_t plan_off, o_off, ml_off, bytes;
+};
+
+StreamLayout stream_layout(const AttnShape& s) {
+  StreamLayout L{};
+  L.nbg = std::max(1, kStreamBlocks / s.hkv);
+  const size_t slots = (size_t)L.nbg * s.hkv * 2;
+  auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  L.plan_off = 0;
+  L.o_off = a256((2 * kMaxStreamTiles + 1) * sizeof(int32_t));
+  L.ml_off = L.o_off + a256(slots * kW8Qv * s.d * sizeof(float));
+  L.bytes = L.ml_off + a256(slots * kW8Qv * sizeof(float2));
+  return L;
 }
 
 }  // namespace
 
 size_t attn_workspace(const AttnShape& s, bool bf16) {
-  if (!bf16 || s.batch <= 0 || s.max_rows <= 0) return 0;
-  // An upper bound over every call whose batch, max_rows and max_kv do not
-  // exceed these (the split count grows as the row count shrinks).  With G =
-  // max_tiles * hkv * batch row groups, a plan has n_split <= 8 and, since a
-  // split holds at least G * kv_tiles / (2 * slots) tiles, n_split <=
-  // 2 * slots / G + 1.
-  const SplitPlan mx = split_plan(s, false, kW8Qv, kW8Slots);
-  const int kv_tiles = (s.max_kv + kKT - 1) / kKT;
-  if (kv_tiles <= 16 && mx.n_split <= 1) return 0;
-  const size_t G = (size_t)mx.max_tiles * s.hkv * s.batch;
-  size_t items = std::min(8 * G, 2 * (size_t)kW8Slots + G);
-  if (forced_split_tiles() > 0) items = G * kMaxSplit;  // a forced split size
-  auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  return a256(items * kW8Qv * s.d * sizeof(float)) + a256(items * kW8Qv * sizeof(float2));
+  // Every call that could choose stream mode needs the same layout (it only
+  // depends on the heads and head_dim), so the size covers all smaller shapes.
+  if (!bf16 || s.batch <= 0 || s.max_rows <= 0 || s.max_kv <= kKT) return 0;
+  return stream_layout(s).bytes;
 }
 
 hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
@@ -925,64 +964,54 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
   if (bf16 && !kv_pos) {
     // recomputed rows: the 8-wave kernel (buffer offsets of one request's rows are 32-bit)
     if ((double)s.max_kv * (double)kv_row_stride * 2.0 >= 2147483648.0) return hipErrorInvalidConfiguration;
-    const SplitPlan p = split_plan(s, false, kW8Qv, kW8Slots);
-    if (p.n_split > kMaxSplit) return hipErrorInvalidConfiguration;
-    char* wb = static_cast<char*>(ws);
-    float* part_o = p.n_split > 1 ? reinterpret_cast<float*>(wb + p.o_off) : nullptr;
-    float2* part_ml = p.n_split > 1 ? reinterpret_cast<float2*>(wb + p.ml_off) : nullptr;
-    const int64_t nblocks = (int64_t)p.max_tiles * s.batch * s.hkv * p.n_split;
+    const int max_tiles = (s.max_rows + (kW8Qv >> lg) - 1) / (kW8Qv >> lg);
+    if (use_stream(s, max_tiles)) {
+      const StreamLayout L = stream_layout(s);
+      char* wb = static_cast<char*>(ws);
+      int32_t* plan = reinterpret_cast<int32_t*>(wb + L.plan_off);
+      float* part_o = reinterpret_cast<float*>(wb + L.o_off);
+      float2* part_ml = reinterpret_cast<float2*>(wb + L.ml_off);
+      dim3 grid((unsigned)(L.nbg * s.hkv));
+#define QCF_W8S(D)                                                                                \
+  attn_w8_kernel<D, true><<<grid, kW8 * 64, 0, stream>>>(                                         \
+      static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
+      static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
+      kv_row_stride, cu_kv, s.batch, max_tiles, s.hkv, s.hq, lg, scale2, L.nbg, plan, part_o,     \
+      part_ml);                                                                                   \
+  attn_stream_merge_kernel<D><<<dim3((unsigned)(4 * max_tiles * s.batch * s.hkv)), kThreads, 0,   \
+                                 stream>>>(static_cast<uint16_t*>(out), lse, n_rows, cu_rows,      \
+                                           s.batch, max_tiles, s.hkv, s.hq, lg, L.nbg, plan,       \
+                                           part_o, part_ml)
+      if (s.d == 64) { QCF_W8S(64); } else { QCF_W8S(128); }
+#undef QCF_W8S
+      return hipGetLastError();
+    }
+    const int64_t nblocks = (int64_t)max_tiles * s.batch * s.hkv;
     if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
     dim3 grid((unsigned)nblocks);
 #define QCF_W8(D)                                                                                 \
-  attn_w8_kernel<D><<<grid, kW8 * 64, 0, stream>>>(                                               \
+  attn_w8_kernel<D, false><<<grid, kW8 * 64, 0, stream>>>(                                        \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
-      kv_row_stride, cu_kv, s.batch, p.max_tiles, s.hkv, s.hq, lg, scale2, p.n_split,             \
-      p.split_tiles, part_o, part_ml)
+      kv_row_stride, cu_kv, s.batch, max_tiles, s.hkv, s.hq, lg, scale2, 0, nullptr, nullptr,     \
+      nullptr)
     if (s.d == 64) QCF_W8(64); else QCF_W8(128);
 #undef QCF_W8
-    if (p.n_split > 1) {
-      dim3 mgrid((unsigned)((int64_t)p.max_tiles * s.batch * s.hkv));
-#define QCF_MERGE(D)                                                                              \
-  attn_merge_kernel<D, kW8Qv><<<mgrid, kThreads, 0, stream>>>(                                    \
-      static_cast<uint16_t*>(out), lse, row_pos, n_rows, cu_rows, cu_kv, n_kv_rows, s.batch,       \
-      p.max_tiles, s.hkv, s.hq, lg, p.n_split, p.split_tiles, part_o, part_ml)
-      if (s.d == 64) QCF_MERGE(64); else QCF_MERGE(128);
-#undef QCF_MERGE
-    }
     return hipGetLastError();
   }
   if (bf16) {
-    // explicit key positions (the anchor probe): the 4-wave kernel, never split
-    const SplitPlan p = split_plan(s, true, 128, 512);
-    if (p.n_split > kMaxSplit) return hipErrorInvalidConfiguration;
-    char* wb = static_cast<char*>(ws);
-    float* part_o = p.n_split > 1 ? reinterpret_cast<float*>(wb + p.o_off) : nullptr;
-    float2* part_ml = p.n_split > 1 ? reinterpret_cast<float2*>(wb + p.ml_off) : nullptr;
-    const int64_t nblocks = (int64_t)p.max_tiles * s.batch * s.hkv * p.n_split;
+    // explicit key positions (the anchor probe): the 4-wave kernel
+    const int max_tiles = (s.max_rows + (128 >> lg) - 1) / (128 >> lg);
+    const int64_t nblocks = (int64_t)max_tiles * s.batch * s.hkv;
     if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
     dim3 grid((unsigned)nblocks);
-#define QCF_ATTN(D, P)                                                                            \
-  attn_bf16_kernel<D, P><<<grid, kThreads, 0, stream>>>(                                          \
+#define QCF_POS(D)                                                                                \
+  attn_pos_kernel<D><<<grid, kThreads, 0, stream>>>(                                              \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
-      kv_row_stride, cu_kv, kv_pos, s.batch, p.max_tiles, s.hkv, s.hq, lg, scale2, p.n_split,     \
-      p.split_tiles, part_o, part_ml)
-    if (kv_pos) {
-      if (s.d == 64) QCF_ATTN(64, true); else QCF_ATTN(128, true);
-    } else {
-      if (s.d == 64) QCF_ATTN(64, false); else QCF_ATTN(128, false);
-    }
-#undef QCF_ATTN
-    if (p.n_split > 1) {
-      dim3 mgrid((unsigned)((int64_t)p.max_tiles * s.batch * s.hkv));
-#define QCF_MERGE(D)                                                                              \
-  attn_merge_kernel<D, 128><<<mgrid, kThreads, 0, stream>>>(                                      \
-      static_cast<uint16_t*>(out), lse, row_pos, n_rows, cu_rows, cu_kv, n_kv_rows, s.batch,       \
-      p.max_tiles, s.hkv, s.hq, lg, p.n_split, p.split_tiles, part_o, part_ml)
-      if (s.d == 64) QCF_MERGE(64); else QCF_MERGE(128);
-#undef QCF_MERGE
-    }
+      kv_row_stride, cu_kv, kv_pos, s.batch, max_tiles, s.hkv, s.hq, lg, scale2)
+    if (s.d == 64) QCF_POS(64); else QCF_POS(128);
+#undef QCF_POS
     return hipGetLastError();
   }
   dim3 grid((unsigned)n_rows, s.hq);

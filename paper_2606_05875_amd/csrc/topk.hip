@@ -45,6 +45,62 @@ __device__ __forceinline__ uint32_t block_prefix(bool pred, uint32_t* wave_tot, 
   return before + below;
 }
 
+// Most-significant-digit radix select over the keys key_at(i), i < n: the key
+// tau of the k-th largest (1 <= k < n) and how many of the keys equal to tau
+// belong to the top k.  NT threads; hist has 256 entries.
+template <int NT, typename KeyAt>
+__device__ void radix_select(KeyAt key_at, int n, int k, uint32_t* hist, uint32_t* sh,
+                             uint32_t& tau, int& remaining) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0u, mask = 0u;
+  remaining = k;  // how many of the keys matching `prefix` are still to be taken
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += NT) hist[i] = 0u;
+    __syncthreads();
+    for (int i = tid; i < n; i += NT) {
+      const uint32_t key = key_at(i);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid < 64) {
+      // lane l owns digits 255-4l .. 252-4l (descending digit order)
+      uint32_t c[4];
+      uint32_t own = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c[e] = hist[255 - 4 * tid - e];
+        own += c[e];
+      }
+      // exclusive prefix over lanes = keys with a larger digit
+      uint32_t incl = own;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = __shfl_up(incl, off, 64);
+        if (tid >= off) incl += t;
+      }
+      uint32_t above = incl - own;
+      if (above < (uint32_t)remaining && (uint32_t)remaining <= incl) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (above + c[e] >= (uint32_t)remaining) {
+            sh[0] = 255u - 4u * tid - e;
+            sh[1] = above;
+            break;
+          }
+          above += c[e];
+        }
+      }
+    }
+    __syncthreads();
+    const uint32_t digit = sh[0];
+    remaining -= (int)sh[1];
+    prefix |= digit << shift;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  tau = prefix;
+}
+
 template <bool kLds>
 __global__ __launch_bounds__(kThreads) void select_topk_kernel(
     int32_t* __restrict__ out_idx, int32_t* __restrict__ out_pos, int64_t n_out,
@@ -54,7 +110,7 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(
   __shared__ uint32_t keys[kLds ? kLdsKeys : 1];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t wave_tot[kWaves];
-  __shared__ uint32_t sh_digit, sh_above;
+  __shared__ uint32_t sh[2];
 
   const int s = blockIdx.x;
   const int64_t start = seg_start[s];
@@ -76,55 +132,9 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(
   auto key_at = [&](int i) -> uint32_t { return kLds ? keys[i] : order_key(sc[i]); };
 
   const bool take_all = (k == n);
-  uint32_t prefix = 0u, mask = 0u;
-  int remaining = k;  // how many of the keys matching `prefix` are still to be taken
-  if (!take_all) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      hist[tid] = 0u;  // kThreads == 256 bins
-      __syncthreads();
-      for (int i = tid; i < n; i += kThreads) {
-        const uint32_t key = key_at(i);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      if (tid < 64) {
-        // lane l owns digits 255-4l .. 252-4l (descending digit order)
-        uint32_t c[4];
-        uint32_t own = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          c[e] = hist[255 - 4 * tid - e];
-          own += c[e];
-        }
-        // exclusive prefix over lanes = keys with a larger digit
-        uint32_t incl = own;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const uint32_t t = __shfl_up(incl, off, 64);
-          if (tid >= off) incl += t;
-        }
-        uint32_t above = incl - own;
-        if (above < (uint32_t)remaining && (uint32_t)remaining <= incl) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (above + c[e] >= (uint32_t)remaining) {
-              sh_digit = 255u - 4u * tid - e;
-              sh_above = above;
-              break;
-            }
-            above += c[e];
-          }
-        }
-      }
-      __syncthreads();
-      const uint32_t digit = sh_digit;
-      remaining -= (int)sh_above;
-      prefix |= digit << shift;
-      mask |= 255u << shift;
-      __syncthreads();
-    }
-  }
-  const uint32_t tau = prefix;
+  uint32_t tau = 0u;
+  int remaining = k;
+  if (!take_all) radix_select<kThreads>(key_at, n, k, hist, sh, tau, remaining);
 
   // ordered compaction: keys > tau, then the `remaining` lowest-index keys == tau
   uint32_t eq_base = 0, sel_base = 0;
@@ -166,3 +176,4 @@ hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
 }
 
 }  // namespace qcf
+

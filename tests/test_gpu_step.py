@@ -113,6 +113,6 @@ def test_fused_assembly_matches_separate_calls(name):
     b = FusionStep(w)
     b.run()
     g2 = b.results()
-    for key in ("k_fuse", "v_fuse", "scores", "R", "o", "o_probe", "q_u"):
+    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u", "q_R"):
         np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)
     assert torch.equal(a.k_probe, b.k_probe) and torch.equal(a.v_probe, b.v_probe)

@@ -71,6 +71,8 @@ def main():
     ap.add_argument("--sets", type=int, default=0, help="buffer sets rotated (0: enough for 512 MB)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 256 MiB device-to-device copy 20 times (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -78,6 +80,16 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.calibrate_copy:
+        # a plain copy of known size: 256 MiB read + 256 MiB written per launch
+        x = torch.empty(64 << 20, dtype=torch.float32, device="cuda").uniform_()
+        y = torch.empty_like(x)
+        for _ in range(20):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read": x.numel() * 4, "bytes_written": y.numel() * 4,
+                          "launches": 20}), flush=True)
+        return
     from paper_2606_05875_amd.step import FusionStep
     from paper_2606_05875_amd.workloads import make_workload
 

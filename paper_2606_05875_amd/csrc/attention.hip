@@ -390,7 +390,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, int batch, int max_tiles, int hkv,
     int hq, int lg, float scale2, int nbg, int32_t* __restrict__ plan_out,
-    float* __restrict__ part_o, float2* __restrict__ part_ml) {
+    uint16_t* __restrict__ part_o, float2* __restrict__ part_ml) {
   constexpr int KCH = D / 8 + 1, VCH = D / 8 + 4;  // 16-byte chunks per LDS row (padded)
   constexpr int KSTR = KCH * 8, VSTR = VCH * 8;    // bf16 elements per LDS row
   constexpr int KST = kKT * KSTR, VST = kKT * VSTR;  // elements per stage
@@ -642,21 +642,20 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       if (lse && hi == 0) lse[grow * hq + head] = lt > 0.f ? (m + log2f(lt)) * kLn2 : -INFINITY;
       return;
     }
-    // partials bypass the L2 (non-temporal): they are read once, by the
-    // merge kernel, and would otherwise evict the K/V tiles other blocks of
-    // this head are still streaming
-    float* po = part_o + (slot * kW8Qv + qv) * D;
+    // partial: this segment's O normalised by its own sum, in bf16 (half the
+    // traffic of float32; |O / sum| <= max |v|, so one bf16 rounding of the
+    // output scale), and its (max, sum) in float32.  Lanes l and l^32 write
+    // the two halves of each 16-byte piece; the L2 joins them into full lines.
+    uint16_t* po = part_o + (slot * kW8Qv + qv) * D;
+    const float pinv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x4 v4 = {o[mb][4 * i], o[mb][4 * i + 1], o[mb][4 * i + 2], o[mb][4 * i + 3]};
-        __builtin_nontemporal_store(v4, reinterpret_cast<f32x4*>(po + 32 * mb + 8 * i + 4 * hi));
-      }
-    if (hi == 0) {
-      __builtin_nontemporal_store(m, &part_ml[slot * kW8Qv + qv].x);
-      __builtin_nontemporal_store(lt, &part_ml[slot * kW8Qv + qv].y);
-    }
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<uint2*>(po + 32 * mb + 8 * i + 4 * hi) =
+            make_uint2(pack_bf16x2(o[mb][4 * i] * pinv, o[mb][4 * i + 1] * pinv),
+                       pack_bf16x2(o[mb][4 * i + 2] * pinv, o[mb][4 * i + 3] * pinv));
+    if (hi == 0) part_ml[slot * kW8Qv + qv] = make_float2(m, lt);
   };
 
   if (!kStream) {
@@ -756,7 +755,7 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, int64_t n_rows,
     const int32_t* __restrict__ cu_rows, int batch, int max_tiles, int hkv, int hq, int lg,
-    int nbg, const int32_t* __restrict__ plan, const float* __restrict__ part_o,
+    int nbg, const int32_t* __restrict__ plan, const uint16_t* __restrict__ part_o,
     const float2* __restrict__ part_ml) {
   constexpr int QV = kW8Qv;
   constexpr int QQ = QV / 4;  // query vectors per merge block (a quarter of the tile)
@@ -808,12 +807,13 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
     const int qv = qv0 + threadIdx.x;
     float mx = -1e30f;
     for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[slot_l[sp] * QV + qv].x);
+    // split sp's weight on its normalised partial: sum_sp 2^(m_sp - max) / total
     float lsum = 0.f;
     for (int sp = 0; sp < nsp; ++sp) {
       const float2 ml = part_ml[slot_l[sp] * QV + qv];
-      const float wsp = __builtin_amdgcn_exp2f(ml.x - mx);
+      const float wsp = __builtin_amdgcn_exp2f(ml.x - mx) * ml.y;
       if (sp < WS) wgt[sp][threadIdx.x] = wsp;
-      lsum += wsp * ml.y;
+      lsum += wsp;
     }
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
     for (int sp = 0; sp < nsp && sp < WS; ++sp) wgt[sp][threadIdx.x] *= inv;
@@ -834,17 +834,22 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[p][k] = 0.f;
   for (int sp = 0; sp < nsp; ++sp) {
-    const float* pp = part_o + (slot_l[sp] * QV + qv0) * D;
+    const uint16_t* pp = part_o + (slot_l[sp] * QV + qv0) * D;
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       const int e = p * kPass + 8 * threadIdx.x;
       const int ql = e / D;
-      const float wv = sp < WS ? wgt[sp][ql]
-                               : __builtin_amdgcn_exp2f(part_ml[slot_l[sp] * QV + qv0 + ql].x - mxq[ql]) * invq[ql];
-      const float4 x0 = *reinterpret_cast<const float4*>(pp + e);
-      const float4 x1 = *reinterpret_cast<const float4*>(pp + e + 4);
-      acc[p][0] += wv * x0.x; acc[p][1] += wv * x0.y; acc[p][2] += wv * x0.z; acc[p][3] += wv * x0.w;
-      acc[p][4] += wv * x1.x; acc[p][5] += wv * x1.y; acc[p][6] += wv * x1.z; acc[p][7] += wv * x1.w;
+      float wv;
+      if (sp < WS) {
+        wv = wgt[sp][ql];
+      } else {
+        const float2 ml = part_ml[slot_l[sp] * QV + qv0 + ql];
+        wv = __builtin_amdgcn_exp2f(ml.x - mxq[ql]) * ml.y * invq[ql];
+      }
+      float x[8];
+      Vec16<uint16_t>::unpack(ld16(pp + e), x);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[p][k] += wv * x[k];
     }
   }
 #pragma unroll
@@ -938,7 +943,7 @@ StreamLayout stream_layout(const AttnShape& s) {
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   L.plan_off = 0;
   L.o_off = a256((2 * kMaxStreamTiles + 1) * sizeof(int32_t));
-  L.ml_off = L.o_off + a256(slots * kW8Qv * s.d * sizeof(float));
+  L.ml_off = L.o_off + a256(slots * kW8Qv * s.d * sizeof(uint16_t));
   L.bytes = L.ml_off + a256(slots * kW8Qv * sizeof(float2));
   return L;
 }
@@ -969,7 +974,7 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
       const StreamLayout L = stream_layout(s);
       char* wb = static_cast<char*>(ws);
       int32_t* plan = reinterpret_cast<int32_t*>(wb + L.plan_off);
-      float* part_o = reinterpret_cast<float*>(wb + L.o_off);
+      uint16_t* part_o = reinterpret_cast<uint16_t*>(wb + L.o_off);
       float2* part_ml = reinterpret_cast<float2*>(wb + L.ml_off);
       dim3 grid((unsigned)(L.nbg * s.hkv));
 #define QCF_W8S(D)                                                                                \

@@ -10,9 +10,11 @@ Inputs are resident in HBM before the timed region; several buffer sets are
 rotated so the 256 MB last-level cache does not hold the previous step's data.
 
 Prints one JSON line:  metric = selected-token fused-prefill tokens/s per layer
-(|R| recomputed rows / step time), with the attention kernel's roofline
-fraction (algorithmic FLOPs per launch / its average HIP-event duration) and
-the CPU oracle's throughput on a bounded sample of the same workload.
+(|R| recomputed rows / step time), with the attention call's roofline
+fraction (algorithmic FLOPs per launch / its average HIP-event duration), its
+measured HBM traffic (the committed counter record, while the attention
+source is unchanged) and the CPU oracle's throughput on a bounded sample of
+the same workload.
 """
 from __future__ import annotations
 
@@ -30,6 +32,25 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def measured_traffic():
+    """HBM bytes per attention call from the committed counter record, or None when the
+    attention source has changed since the counters were taken."""
+    import hashlib
+    rec_path = os.path.join(ROOT, "profiles", "attention_c2_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2606_05875_amd", "csrc", "attention.hip")
+    try:
+        rec = None
+        for line in open(rec_path):
+            if line.startswith("{"):
+                rec = json.loads(line)
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("attention_source_sha256") != digest:
+        return None
+    return rec["bytes_per_call"]
 
 
 def attn_flops(step, R_pos):
@@ -160,9 +181,12 @@ def main():
         "data": "synthetic (seeded; shapes of the paper's 512-token-chunk RAG requests)",
         "config": {"workload": f"{args.config}: {w.meta['desc']}", "recomputed_rows": n_R,
                    "rho_bp": w.rho_bp, "tokens": w.n_rows, "buffer_sets": n_sets},
-        "roofline": {"kernel": "attn_bf16_kernel (qcf_sparse_prefill_attn, recomputed rows)",
+        "roofline": {"kernel": "qcf_sparse_prefill_attn, recomputed rows (attn_w8_kernel + "
+                               "attn_stream_merge_kernel)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic() if args.config == "c2" else None,
+                     "traffic_unit": "bytes per launch (HBM, calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE)",
                      "flops_per_launch": flops, "avg_launch_ms": attn_ms},
         "stage_ms": stage_ms,
         "assemble_GBs": asm_gbs,

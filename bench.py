@@ -34,9 +34,9 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
-def measured_traffic():
+def measured_traffic(kv_row_stride):
     """HBM bytes per attention call from the committed counter record, or None when the
-    attention source has changed since the counters were taken."""
+    attention source or the cache row stride has changed since the counters were taken."""
     import hashlib
     rec_path = os.path.join(ROOT, "profiles", "attention_c2_hbm_traffic.md")
     src = os.path.join(ROOT, "paper_2606_05875_amd", "csrc", "attention.hip")
@@ -48,7 +48,8 @@ def measured_traffic():
         digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("attention_source_sha256") != digest:
+    if (not rec or rec.get("attention_source_sha256") != digest
+            or rec.get("kv_row_stride") != kv_row_stride):
         return None
     return rec["bytes_per_call"]
 
@@ -195,7 +196,7 @@ def main():
                                "attn_stream_merge_kernel)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic() if args.config == "c2" else None,
+                     "traffic": measured_traffic(int(first.k.stride(0))) if args.config == "c2" else None,
                      "traffic_unit": "bytes per launch (HBM, calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE)",
                      "flops_per_launch": flops, "avg_launch_ms": attn_ms},
         "stage_ms": stage_ms,

@@ -14,7 +14,10 @@
  *    elements (head-major inside the row); consecutive rows are `row_stride`
  *    elements apart (row_stride >= n_kv_heads * head_dim).  Query and output
  *    tensors are dense ([rows, n_q_heads, head_dim]).  Base pointers are 16-byte
- *    aligned; row strides are multiples of 16 bytes.
+ *    aligned; row strides are multiples of 16 bytes.  The attention and score
+ *    kernels read one head's slice of every row; with a row of an even number
+ *    of head slices those slices fall on a fraction of the L2 channels, so
+ *    caches they read are best laid out with qcf_recommended_row_stride.
  *  - Index and position arrays are int32 device arrays; sizes fit int32.
  *  - dtype is QCF_F32 or QCF_BF16 (storage type of every floating tensor of the
  *    call, except score vectors, which are always float32); arithmetic is
@@ -44,7 +47,7 @@
 extern "C" {
 #endif
 
-#define QCF_VERSION 100
+#define QCF_VERSION 101
 
 typedef enum {
   QCF_OK = 0,
@@ -61,6 +64,17 @@ int qcf_version(void);
 const char* qcf_status_string(qcf_status status);
 
 /*
+ * qcf_recommended_row_stride -- row stride (in elements) for a K/V cache that
+ * the attention and score kernels will read: n_kv_heads * head_dim when
+ * n_kv_heads is odd, else (n_kv_heads + 1) * head_dim, i.e. one unused head
+ * slice of padding per row.  A row of an odd number of head slices puts the
+ * slice of one head in consecutive rows on different L2 channels (a row of
+ * 8 slices of 256 bytes reaches only a few of them).  Host function; returns
+ * 0 for n_kv_heads <= 0 or a head_dim other than 64 and 128.
+ */
+int64_t qcf_recommended_row_stride(int n_kv_heads, int head_dim);
+
+/*
  * qcf_rerope -- position remapping Pi_i and stitching of the reused chunk
  * caches into the request cache (Section 2.1.2, eq. pic_online).  A stored
  * chunk key is rotated at its chunk-local position; rotating it once more by
@@ -70,10 +84,10 @@ const char* qcf_status_string(qcf_status status);
  * dst = seg_start[s] + r:
  *     k_out[dst] = rope(k_in[src], seg_delta[s])
  *     v_out[dst] = v_in[src]                       (when v_out != NULL)
- *   k_out, v_out  [n_out_rows, row_stride]; k_in, v_in [n_in_rows, row_stride]
- *                 k_out may equal k_in (in place) when src == dst; v_in must be
- *                 non-NULL iff v_out is, and the V copy is skipped when
- *                 v_out == v_in.  Rows outside every segment are not touched.
+ *   k_out, v_out  [n_out_rows, out_row_stride]; k_in, v_in [n_in_rows, in_row_stride]
+ *                 k_out may equal k_in (in place, equal strides) when src == dst;
+ *                 v_in must be non-NULL iff v_out is, and the V copy is skipped
+ *                 when v_out == v_in.  Rows outside every segment are not touched.
  *   seg_start     [n_seg] first destination row of each segment (a chunk)
  *   seg_len       [n_seg] rows in each segment (<= max_seg_len)
  *   seg_delta     [n_seg] rotation offset of each segment in positions
@@ -83,7 +97,8 @@ const char* qcf_status_string(qcf_status status);
  */
 qcf_status qcf_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in,
                       qcf_dtype dtype, int64_t n_out_rows, int64_t n_in_rows, int n_kv_heads,
-                      int head_dim, int64_t row_stride, int n_seg, const int32_t* seg_start,
+                      int head_dim, int64_t out_row_stride, int64_t in_row_stride, int n_seg,
+                      const int32_t* seg_start,
                       const int32_t* seg_len, const int32_t* seg_delta, const int32_t* src_start,
                       int max_seg_len, double rope_theta, hipStream_t stream);
 
@@ -137,25 +152,26 @@ qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
  *  (3) probe slots j < n_probe with probe_src[j] >= 0:
  *        probe_k[j] = rope(k_pic[probe_src[j]], probe_delta[j]),  probe_v[j] = v_pic[probe_src[j]]
  *      slots with probe_src[j] < 0 are left to the query rows.
- *   k_cache, v_cache [n_rows, row_stride]; k_pic, v_pic [n_pic_rows, row_stride]
- *                    (read only; may not alias the outputs)
+ *   k_cache, v_cache [n_rows, row_stride]; k_pic, v_pic [n_pic_rows,
+ *                    pic_row_stride] (read only; may not alias the outputs)
+ *   probe_k, probe_v [n_probe, probe_row_stride]
  *   q_new [n_src_rows, n_q_heads * head_dim]; k_new, v_new [n_src_rows,
- *   n_kv_heads * head_dim]; q_u [n_query, n_q_heads * head_dim];
- *   probe_k, probe_v [n_probe, n_kv_heads * head_dim] (all dense)
+ *   n_kv_heads * head_dim]; q_u [n_query, n_q_heads * head_dim] (dense)
  *   max_seg_len >= every seg_len
  * The parts must write disjoint places: no query_row inside a segment's
  * destination rows, and each probe slot filled by (3) or by one query row.
  * Results of overlapping writes are unspecified.
  */
 qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t row_stride,
-                        const void* k_pic, const void* v_pic, int64_t n_pic_rows, int n_seg,
-                        const int32_t* seg_start, const int32_t* seg_len,
-                        const int32_t* seg_delta, const int32_t* src_start, int max_seg_len,
-                        const void* q_new, const void* k_new, const void* v_new,
-                        int64_t n_src_rows, int64_t n_query, const int32_t* query_row,
-                        const int32_t* query_pos, const int32_t* query_src,
-                        const int32_t* query_slot, void* q_u, void* probe_k, void* probe_v,
-                        int64_t n_probe, const int32_t* probe_src, const int32_t* probe_delta,
+                        const void* k_pic, const void* v_pic, int64_t n_pic_rows,
+                        int64_t pic_row_stride, int n_seg, const int32_t* seg_start,
+                        const int32_t* seg_len, const int32_t* seg_delta,
+                        const int32_t* src_start, int max_seg_len, const void* q_new,
+                        const void* k_new, const void* v_new, int64_t n_src_rows,
+                        int64_t n_query, const int32_t* query_row, const int32_t* query_pos,
+                        const int32_t* query_src, const int32_t* query_slot, void* q_u,
+                        void* probe_k, void* probe_v, int64_t n_probe, int64_t probe_row_stride,
+                        const int32_t* probe_src, const int32_t* probe_delta,
                         qcf_dtype dtype, int n_q_heads, int n_kv_heads, int head_dim,
                         double rope_theta, hipStream_t stream);
 

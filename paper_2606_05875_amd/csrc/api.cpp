@@ -30,11 +30,21 @@ qcf_status check_heads(int hq, int hkv, int d) {
 
 inline qcf_status hip_status(hipError_t e) { return e == hipSuccess ? QCF_OK : QCF_ERR_HIP; }
 
+// a K/V row stride: at least one row of heads, a whole number of 16-byte units
+inline bool kv_stride_ok(int64_t stride, int hkv, int d, qcf_dtype t) {
+  return stride >= (int64_t)hkv * d && (stride * esize(t)) % 16 == 0;
+}
+
 }  // namespace
 
 extern "C" {
 
 int qcf_version(void) { return QCF_VERSION; }
+
+int64_t qcf_recommended_row_stride(int n_kv_heads, int head_dim) {
+  if (n_kv_heads <= 0 || (head_dim != 64 && head_dim != 128)) return 0;
+  return (int64_t)(n_kv_heads + (n_kv_heads % 2 == 0 ? 1 : 0)) * head_dim;
+}
 
 const char* qcf_status_string(qcf_status s) {
   switch (s) {
@@ -49,9 +59,10 @@ const char* qcf_status_string(qcf_status s) {
 
 qcf_status qcf_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in,
                       qcf_dtype dtype, int64_t n_out_rows, int64_t n_in_rows, int n_kv_heads,
-                      int head_dim, int64_t row_stride, int n_seg, const int32_t* seg_start,
-                      const int32_t* seg_len, const int32_t* seg_delta, const int32_t* src_start,
-                      int max_seg_len, double rope_theta, hipStream_t stream) {
+                      int head_dim, int64_t out_row_stride, int64_t in_row_stride, int n_seg,
+                      const int32_t* seg_start, const int32_t* seg_len, const int32_t* seg_delta,
+                      const int32_t* src_start, int max_seg_len, double rope_theta,
+                      hipStream_t stream) {
   if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
   if (n_out_rows < 0 || n_out_rows > INT32_MAX || n_in_rows < 0 || n_in_rows > INT32_MAX ||
       n_seg < 0 || max_seg_len < 0)
@@ -59,10 +70,14 @@ qcf_status qcf_rerope(void* k_out, const void* k_in, void* v_out, const void* v_
   if (n_kv_heads <= 0) return QCF_ERR_INVALID_ARG;
   if (head_dim != 64 && head_dim != 128) return QCF_ERR_UNSUPPORTED;
   if (n_seg > 65535) return QCF_ERR_UNSUPPORTED;
-  if (row_stride < (int64_t)n_kv_heads * head_dim || (row_stride * esize(dtype)) % 16 != 0)
+  if (!kv_stride_ok(out_row_stride, n_kv_heads, head_dim, dtype) ||
+      !kv_stride_ok(in_row_stride, n_kv_heads, head_dim, dtype))
     return QCF_ERR_INVALID_ARG;
   if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
   if ((v_out == nullptr) != (v_in == nullptr)) return QCF_ERR_INVALID_ARG;
+  // in place needs the same row layout on both sides
+  if ((k_out == k_in || (v_out && v_out == v_in)) && out_row_stride != in_row_stride)
+    return QCF_ERR_INVALID_ARG;
   const bool empty = n_out_rows == 0 || n_in_rows == 0 || n_seg == 0 || max_seg_len == 0;
   if (!tensor_ok(k_out, empty) || !tensor_ok(k_in, empty) || !tensor_ok(v_out, true) ||
       !tensor_ok(v_in, true))
@@ -72,9 +87,9 @@ qcf_status qcf_rerope(void* k_out, const void* k_in, void* v_out, const void* v_
     return QCF_ERR_INVALID_ARG;
   if (empty) return QCF_OK;
   return hip_status(qcf::launch_rerope(k_out, k_in, v_out, v_in, dtype == QCF_BF16, n_out_rows,
-                                       n_in_rows, n_kv_heads, head_dim, row_stride, n_seg,
-                                       seg_start, seg_len, seg_delta, src_start, max_seg_len,
-                                       rope_theta, stream));
+                                       n_in_rows, n_kv_heads, head_dim, out_row_stride,
+                                       in_row_stride, n_seg, seg_start, seg_len, seg_delta,
+                                       src_start, max_seg_len, rope_theta, stream));
 }
 
 qcf_status qcf_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
@@ -122,14 +137,15 @@ qcf_status qcf_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
 }
 
 qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t row_stride,
-                        const void* k_pic, const void* v_pic, int64_t n_pic_rows, int n_seg,
-                        const int32_t* seg_start, const int32_t* seg_len,
-                        const int32_t* seg_delta, const int32_t* src_start, int max_seg_len,
-                        const void* q_new, const void* k_new, const void* v_new,
-                        int64_t n_src_rows, int64_t n_query, const int32_t* query_row,
-                        const int32_t* query_pos, const int32_t* query_src,
-                        const int32_t* query_slot, void* q_u, void* probe_k, void* probe_v,
-                        int64_t n_probe, const int32_t* probe_src, const int32_t* probe_delta,
+                        const void* k_pic, const void* v_pic, int64_t n_pic_rows,
+                        int64_t pic_row_stride, int n_seg, const int32_t* seg_start,
+                        const int32_t* seg_len, const int32_t* seg_delta,
+                        const int32_t* src_start, int max_seg_len, const void* q_new,
+                        const void* k_new, const void* v_new, int64_t n_src_rows,
+                        int64_t n_query, const int32_t* query_row, const int32_t* query_pos,
+                        const int32_t* query_src, const int32_t* query_slot, void* q_u,
+                        void* probe_k, void* probe_v, int64_t n_probe, int64_t probe_row_stride,
+                        const int32_t* probe_src, const int32_t* probe_delta,
                         qcf_dtype dtype, int n_q_heads, int n_kv_heads, int head_dim,
                         double rope_theta, hipStream_t stream) {
   if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
@@ -139,7 +155,9 @@ qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t ro
       n_src_rows < 0 || n_src_rows > INT32_MAX || n_query < 0 || n_query > INT32_MAX ||
       n_probe < 0 || n_probe > INT32_MAX || n_seg < 0 || max_seg_len < 0)
     return QCF_ERR_INVALID_ARG;
-  if (row_stride < (int64_t)n_kv_heads * head_dim || (row_stride * esize(dtype)) % 16 != 0)
+  if (!kv_stride_ok(row_stride, n_kv_heads, head_dim, dtype) ||
+      !kv_stride_ok(pic_row_stride, n_kv_heads, head_dim, dtype) ||
+      !kv_stride_ok(probe_row_stride, n_kv_heads, head_dim, dtype))
     return QCF_ERR_INVALID_ARG;
   if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
   const bool no_seg = n_seg == 0 || max_seg_len == 0;
@@ -167,6 +185,8 @@ qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t ro
   qcf::AssembleShape s{};
   s.n_rows = n_rows;
   s.row_stride = row_stride;
+  s.pic_row_stride = pic_row_stride;
+  s.probe_row_stride = probe_row_stride;
   s.n_pic_rows = n_pic_rows;
   s.n_src_rows = n_src_rows;
   s.n_query = n_query;

@@ -99,7 +99,7 @@ struct AssembleArgs {
   T *k_cache, *v_cache;
   int64_t n_rows, row_stride;
   const T *k_pic, *v_pic;
-  int64_t n_pic_rows;
+  int64_t n_pic_rows, pic_stride;
   const int32_t *seg_start, *seg_len, *seg_delta, *src_start;
   int n_seg, rows_per_block, tiles_per_seg;
   // query rows
@@ -110,7 +110,7 @@ struct AssembleArgs {
   const int32_t *query_row, *query_pos, *query_src, *query_slot;
   // probe buffer
   T *probe_k, *probe_v;
-  int64_t n_probe;
+  int64_t n_probe, probe_stride;
   const int32_t *probe_src, *probe_delta;
   int probe_rows_per_block;
   int hq, hkv;
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     const int64_t s0 = (A.src_start ? (int64_t)A.src_start[s] : (int64_t)A.seg_start[s]) + r0;
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.seg_delta[s], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D>(A.k_cache, A.v_cache, A.row_stride, A.k_pic, A.v_pic, A.row_stride, s0, d0,
+    remap_rows<T, D>(A.k_cache, A.v_cache, A.row_stride, A.k_pic, A.v_pic, A.pic_stride, s0, d0,
                      min(A.rows_per_block, len - r0), A.hkv, A.n_pic_rows, A.n_rows, cs);
     return;
   }
@@ -151,7 +151,7 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     remap_rows<T, D>(A.k_cache, A.v_cache, A.row_stride, A.k_new, A.v_new, kvw, src, row, 1, A.hkv,
                      A.n_src_rows, A.n_rows, cs);
     if (slot >= 0)
-      remap_rows<T, D>(A.probe_k, A.probe_v, kvw, A.k_new, A.v_new, kvw, src, slot, 1, A.hkv,
+      remap_rows<T, D>(A.probe_k, A.probe_v, A.probe_stride, A.k_new, A.v_new, kvw, src, slot, 1, A.hkv,
                        A.n_src_rows, A.n_probe, cs);
     // q: hq heads rotated into q_u[i]
     constexpr int VEC = Vec16<T>::N;
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     if (src < 0) continue;  // a query slot (written by that query row's block)
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.probe_delta[p], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D>(A.probe_k, A.probe_v, kvw, A.k_pic, A.v_pic, A.row_stride, src, p, 1, A.hkv,
+    remap_rows<T, D>(A.probe_k, A.probe_v, A.probe_stride, A.k_pic, A.v_pic, A.pic_stride, src, p, 1, A.hkv,
                      A.n_pic_rows, A.n_probe, cs);
   }
 }
@@ -199,6 +199,7 @@ hipError_t assemble_t(const AssembleShape& s, const AssemblePtrs& p, hipStream_t
   A.k_pic = static_cast<const T*>(p.k_pic);
   A.v_pic = static_cast<const T*>(p.v_pic);
   A.n_pic_rows = s.n_pic_rows;
+  A.pic_stride = s.pic_row_stride;
   A.seg_start = p.seg_start;
   A.seg_len = p.seg_len;
   A.seg_delta = p.seg_delta;
@@ -220,6 +221,7 @@ hipError_t assemble_t(const AssembleShape& s, const AssemblePtrs& p, hipStream_t
   A.probe_k = static_cast<T*>(p.probe_k);
   A.probe_v = static_cast<T*>(p.probe_v);
   A.n_probe = s.n_probe;
+  A.probe_stride = s.probe_row_stride;
   A.probe_src = p.probe_src;
   A.probe_delta = p.probe_delta;
   A.probe_rows_per_block = 4;

@@ -353,13 +353,18 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
   return i32x4{(int)(uint32_t)a, (int)(uint32_t)(a >> 32) & 0xffff, (int)bytes, 0x00020000};
 }
 
-// 16 bytes per lane from the buffer at byte offset voff into LDS at lds + 16 * lane
-// (zeros when voff is past the descriptor's range).  Issued as inline assembly
-// so that the compiler adds no waits of its own for it: the caller orders the
-// LDS traffic with explicit counter waits and barriers.
-__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, const void* lds) {
-  // the LDS base is wave-uniform; readfirstlane puts it in a scalar register
-  const uint32_t la = __builtin_amdgcn_readfirstlane((uint32_t)reinterpret_cast<uintptr_t>(lds));
+// LDS byte address of a __shared__ object (32 bits, as the LDS instructions take it)
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)p);
+}
+
+// 16 bytes per lane from the buffer at byte offset voff into LDS at byte
+// address lds + 16 * lane (zeros when voff is past the descriptor's range).
+// Issued as inline assembly so that the compiler adds no waits of its own for
+// it: the caller orders the LDS traffic with explicit counter waits and barriers.
+__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds) {
+  // the LDS address is wave-uniform; readfirstlane keeps it in a scalar register
+  const uint32_t la = __builtin_amdgcn_readfirstlane(lds);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
                : "s"(la), "v"(voff), "s"(rsrc)
@@ -374,14 +379,20 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
 
 // Work of an 8-wave block.  Plain mode: block -> (KV head g, request b, row
 // tile), the tile's whole key range.  Stream mode (few, unequal tiles): a
-// persistent grid of nbg blocks per KV head; the head's key steps -- the
-// 64-key tiles of every row tile of every request, in (request, row tile)
-// order -- are cut into nbg equal contiguous ranges, one per block, so every
-// block does the same amount of work whatever the row positions.  A row tile
-// cut by a range boundary leaves partial results (at most two per block:
-// its first and its last segment) that attn_stream_merge_kernel combines.
+// persistent grid of nbg blocks per KV head; the head's work -- every row
+// tile of every request in (request, row tile) order, each counted as
+// kSegCost start-up steps followed by its 64-key steps -- is cut into nbg
+// equal contiguous ranges, one per block, so every block does about the same
+// amount of work whatever the row positions.  A row tile cut by a range
+// boundary leaves partial results (at most two per block: its first and its
+// last segment) that attn_stream_merge_kernel combines.
 constexpr int kMaxStreamTiles = 256;  // row tiles (requests x tiles) of a stream-mode call
 constexpr int kStreamBlocks = 256;    // persistent blocks (one per CU of MI355X)
+// Start-up cost of a segment (row positions, Q and the first key tiles in
+// flight before the first product, plus its output stores), in key steps:
+// each row tile counts as this many extra steps when the ranges are cut, so
+// a block that starts several tiles gets fewer key steps.
+constexpr int kSegCost = 2;
 
 template <int D, bool kStream>
 __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
@@ -402,10 +413,16 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   __shared__ int red[kW8];
   __shared__ int plan_cum[kStream ? kMaxStreamTiles + 1 : 1];
   __shared__ int plan_end[kStream ? kMaxStreamTiles : 1];
+  __shared__ int req_rows[kStream ? kMaxStreamTiles + 1 : 1];  // cu_rows, cu_kv of the call
+  __shared__ int req_kv[kStream ? kMaxStreamTiles + 1 : 1];
 
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
+  // the wave index is uniform: readfirstlane lets everything derived from it live in
+  // scalar registers
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
   const int G = 1 << lg;
   const int rpb = kW8Qv >> lg;
+  const uint32_t k_base = lds_addr(k_lds), v_base = lds_addr(v_lds);
   const int qv = 32 * w + lq;
   const int g = blockIdx.x % hkv;
 
@@ -418,36 +435,15 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   typedef float f32x2_t __attribute__((ext_vector_type(2)));
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
-  // One segment: keys [kt_lo, kt_hi) of row tile `tile` of request b; the
+  // One segment: keys [kt_lo, kt_hi) of row tile `tile` of a request whose rows
+  // start at r0 (nr of them) and whose keys start at kv0 (nkv of them); the
   // result is final (slot < 0) or partial slot `slot` of the workspace.
-  auto segment = [&](int b, int tile, int kt_lo, int kt_hi, int64_t slot) {
-    const int64_t r0 = cu_rows[b];
-    const int nr = cu_rows[b + 1] - (int)r0;
-    const int rbase = tile * rpb;
-    const int64_t kv0 = cu_kv[b];
-    int nkv = cu_kv[b + 1] - (int)kv0;
-    if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
-    const int rl = rbase + (qv >> lg);
+  auto segment = [&](int64_t r0, int nr, int64_t kv0, int nkv, int tile, int kt_lo, int kt_hi,
+                     int64_t slot) {
+    const int rl = tile * rpb + (qv >> lg);
     const int head = g * G + (qv & (G - 1));
     const int64_t grow = r0 + rl;
     const bool valid = rl < nr && grow < n_rows;
-    const int qpos = valid ? row_pos[grow] : INT_MIN;
-    const int wmax = wave_max_i(valid ? qpos : -1);
-    const int wmin = wave_min_i(valid ? qpos : INT_MAX);
-    const int wave_end = min(nkv, wmax + 1);
-
-    bf16x8 qreg[D / 16];
-    {
-      const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
-#pragma unroll
-      for (int st = 0; st < D / 16; ++st)
-        qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
-    }
-    f32x16 o[D / 32];
-#pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
-    float m = valid ? -1e30f : INFINITY;
-    float ls = 0.f;
 
     // descriptors over this request's rows of KV head g: the last byte in range
     // is the end of the last key's head slice
@@ -481,11 +477,34 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
         const int j = w + kW8 * i;
         const uint32_t off = r < nt ? soff[i] + toff : kOob;
         if (j < KCH)
-          dma16(rk, off, k_lds + sg * KST + j * 512);
+          dma16(rk, off, k_base + (uint32_t)(sg * KST + j * 512) * 2u);
         else
-          dma16(rv, off, v_lds + sg * VST + (j - KCH) * 512);
+          dma16(rv, off, v_base + (uint32_t)(sg * VST + (j - KCH) * 512) * 2u);
       }
     };
+    // The first three key tiles go out before anything waits on memory (every
+    // LDS read of the previous segment ended at its last barrier), then the
+    // row positions and Q.
+    issue(0);
+    issue(1);
+    issue(2);
+    const int qpos = valid ? row_pos[grow] : INT_MIN;
+    bf16x8 qreg[D / 16];
+    {
+      const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
+#pragma unroll
+      for (int st = 0; st < D / 16; ++st)
+        qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
+    }
+    const int wmax = wave_max_i(valid ? qpos : -1);
+    const int wmin = wave_min_i(valid ? qpos : INT_MAX);
+    const int wave_end = min(nkv, wmax + 1);
+    f32x16 o[D / 32];
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
+    float m = valid ? -1e30f : INFINITY;
+    float ls = 0.f;
+
     // end of a step: this step's transfers may stay in flight, all older ones
     // (and every LDS read) are complete, then the block meets
     auto step_barrier = [&]() {
@@ -583,9 +602,6 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     // has landed.  Past the last tile the transfers still go out (zeros, no
     // memory traffic), so every step issues the same number of them.
     f32x16 sa[2], sb[2];
-    issue(0);
-    issue(1);
-    issue(2);
     asm volatile("" ::: "memory");
     wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
@@ -676,35 +692,56 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     int bmax = red[0];
 #pragma unroll
     for (int i = 1; i < kW8; ++i) bmax = max(bmax, red[i]);
-    segment(b, tile, 0, min(nkv, bmax + 1), -1);
+    segment(r0, nr, kv0, nkv, tile, 0, min(nkv, bmax + 1), -1);
     return;
   }
 
   // stream: the plan (key end and step count of every row tile), built by
-  // each block in LDS: wave w takes tiles w, w+8, ...; its lanes split the rows
+  // each block in LDS.  The requests' row and key offsets come first; then
+  // wave w takes tiles w, w+8, ... four at a time (their position loads are
+  // independent), its lanes splitting each tile's rows.
   const int n_tiles = batch * max_tiles;
-  for (int i = w; i < n_tiles; i += kW8) {
-    const int b = i / max_tiles, tile = i - b * max_tiles;
-    const int64_t r0 = cu_rows[b];
-    const int nr = cu_rows[b + 1] - (int)r0;
-    const int64_t kv0 = cu_kv[b];
-    int nkv = cu_kv[b + 1] - (int)kv0;
-    if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
-    int mx = -1;
-    for (int rr = tile * rpb + l; rr < min(nr, (tile + 1) * rpb); rr += 64)
-      if (r0 + rr < n_rows) mx = max(mx, row_pos[r0 + rr]);
-    mx = wave_max_i(mx);
-    if (l == 0) plan_end[i] = max(0, min(nkv, mx + 1));
+  for (int i = threadIdx.x; i <= batch; i += kW8 * 64) {
+    req_rows[i] = cu_rows[i];
+    req_kv[i] = cu_kv[i];
+  }
+  __syncthreads();
+  auto req_nkv = [&](int b) {
+    const int64_t kv0 = req_kv[b];
+    const int nkv = req_kv[b + 1] - (int)kv0;
+    return kv0 + nkv > n_kv_rows ? (int)(n_kv_rows - kv0) : nkv;
+  };
+  for (int i0 = w; i0 < n_tiles; i0 += 4 * kW8) {
+    int mx[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kW8;
+      mx[u] = -1;
+      if (i >= n_tiles) continue;
+      const int b = i / max_tiles, tile = i - b * max_tiles;
+      const int64_t r0 = req_rows[b];
+      const int nr = req_rows[b + 1] - (int)r0;
+      for (int rr = tile * rpb + l; rr < min(nr, (tile + 1) * rpb); rr += 64)
+        if (r0 + rr < n_rows) mx[u] = max(mx[u], row_pos[r0 + rr]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kW8;
+      const int m_all = wave_max_i(mx[u]);
+      if (l == 0 && i < n_tiles) plan_end[i] = max(0, min(req_nkv(i / max_tiles), m_all + 1));
+    }
   }
   __syncthreads();
   if (w == 0) {
-    // exclusive scan of the step counts (kMaxStreamTiles / 64 tiles per lane)
+    // exclusive scan of the tiles' costs, start-up plus key steps
+    // (kMaxStreamTiles / 64 tiles per lane)
     constexpr int PL = kMaxStreamTiles / 64;
     int loc[PL], sum = 0;
 #pragma unroll
     for (int k = 0; k < PL; ++k) {
       const int i = l * PL + k;
-      loc[k] = i < n_tiles ? (plan_end[i] + kKT - 1) / kKT : 0;
+      const int nst = i < n_tiles ? (plan_end[i] + kKT - 1) / kKT : 0;
+      loc[k] = nst > 0 ? nst + kSegCost : 0;
       sum += loc[k];
     }
     int incl = sum;
@@ -727,6 +764,8 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     for (int i = threadIdx.x; i <= n_tiles; i += kW8 * 64) plan_out[i] = plan_cum[i];
     for (int i = threadIdx.x; i < n_tiles; i += kW8 * 64) plan_out[kMaxStreamTiles + 1 + i] = plan_end[i];
   }
+  // this block's range [lo, hi_s) of the head's cost line; tile i occupies
+  // [plan_cum[i], plan_cum[i+1]): kSegCost start-up units, then its key steps
   const int r = blockIdx.x / hkv;
   const int64_t S = plan_cum[n_tiles];
   int lo = (int)(r * S / nbg);
@@ -735,14 +774,18 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   bool first = true;
   while (lo < hi_s) {
     while (plan_cum[i + 1] <= lo) ++i;  // skip tiles without steps
-    const int c0 = plan_cum[i], c1 = plan_cum[i + 1];
-    const int seg_end = min(hi_s, c1);
-    const int b = i / max_tiles, tile = i - b * max_tiles;
-    const bool whole = lo == c0 && seg_end == c1;
-    const int64_t slot = whole ? -1 : ((int64_t)(g * nbg + r) * 2 + (first ? 0 : 1));
-    segment(b, tile, (lo - c0) * kKT, min(plan_end[i], (seg_end - c0) * kKT), slot);
-    lo = seg_end;
-    first = false;
+    const int c1 = plan_cum[i + 1], a = plan_cum[i] + kSegCost;  // key step 0 at a
+    const int s_lo = max(lo, a), s_hi = min(hi_s, c1);
+    if (s_lo < s_hi) {
+      const int b = i / max_tiles, tile = i - b * max_tiles;
+      const bool whole = s_lo == a && s_hi == c1;
+      const int64_t slot = whole ? -1 : ((int64_t)(g * nbg + r) * 2 + (first ? 0 : 1));
+      const int64_t r0 = req_rows[b];
+      segment(r0, req_rows[b + 1] - (int)r0, req_kv[b], req_nkv(b), tile, (s_lo - a) * kKT,
+              min(plan_end[i], (s_hi - a) * kKT), slot);
+      first = false;
+    }
+    lo = c1;
   }
 }
 
@@ -771,6 +814,7 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
   const int64_t S = plan[n_tiles];
   const int c0 = plan[i], c1 = plan[i + 1];
   if (c1 <= c0 || S == 0) return;
+  const int a = c0 + kSegCost;  // the tile's first key step on the cost line
   // block holding step x: the largest r with floor(r S / nbg) <= x
   auto owner = [&](int x) {
     int a = 0, z = nbg - 1;
@@ -780,11 +824,12 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
     }
     return a;
   };
-  const int rf = owner(c0), rlst = owner(c1 - 1);
+  const int rf = owner(a), rlst = owner(c1 - 1);
   if (rf == rlst) return;  // one block did the whole tile
   // the blocks with a non-empty range between them, in order (with fewer steps
   // than blocks some ranges are empty); the first block's segment sits in its
-  // slot 1 when its range began before this tile, every other one's in slot 0
+  // slot 1 when its range began before this tile (it then did a segment of an
+  // earlier tile first), every other one's in slot 0
   if (threadIdx.x == 0) {
     int n = 0;
     for (int rr = rf; rr <= rlst; ++rr) {

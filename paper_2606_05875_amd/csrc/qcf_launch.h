@@ -10,7 +10,8 @@ namespace qcf {
 
 hipError_t launch_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in, bool bf16,
                          int64_t n_out_rows, int64_t n_in_rows, int hkv, int d,
-                         int64_t row_stride, int n_seg, const int32_t* seg_start,
+                         int64_t out_row_stride, int64_t in_row_stride, int n_seg,
+                         const int32_t* seg_start,
                          const int32_t* seg_len, const int32_t* seg_delta,
                          const int32_t* src_start, int max_seg_len, double theta,
                          hipStream_t stream);
@@ -33,7 +34,8 @@ hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
                               const int32_t* pos_base, int max_seg_len, hipStream_t stream);
 
 struct AssembleShape {
-  int64_t n_rows, row_stride, n_pic_rows, n_src_rows, n_query, n_probe;
+  int64_t n_rows, row_stride, pic_row_stride, probe_row_stride, n_pic_rows, n_src_rows, n_query,
+      n_probe;
   int n_seg, max_seg_len, hq, hkv, d;
   bool bf16;
   double theta;

@@ -21,7 +21,8 @@ constexpr int kUnitsPerThread = 4;  // (row, head, j-vector) units each thread o
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void rerope_kernel(
     T* k_out, const T* k_in, T* v_out, const T* v_in, int64_t n_out_rows, int64_t n_in_rows,
-    int hkv, int64_t row_stride, int rows_per_block, const int32_t* __restrict__ seg_start,
+    int hkv, int64_t out_stride, int64_t in_stride, int rows_per_block,
+    const int32_t* __restrict__ seg_start,
     const int32_t* __restrict__ seg_len, const int32_t* __restrict__ seg_delta,
     const int32_t* __restrict__ src_start, double theta) {
   constexpr int HALF = D / 2;
@@ -62,8 +63,8 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
         const int64_t src = src0 + rr, dst = dst0 + rr;
         if (src >= 0 && src < n_in_rows && dst >= 0 && dst < n_out_rows) {
           const int64_t in_head = (int64_t)h * D + jj[k];
-          off_in[k] = src * row_stride + in_head;
-          off_out[k] = dst * row_stride + in_head;
+          off_in[k] = src * in_stride + in_head;
+          off_out[k] = dst * out_stride + in_head;
           lo[k] = ld16(k_in + off_in[k]);
           hi[k] = ld16(k_in + off_in[k] + HALF);
         }
@@ -101,8 +102,8 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
         const int c = u - rr * vchunks;
         const int64_t src = src0 + rr, dst = dst0 + rr;
         if (src >= 0 && src < n_in_rows && dst >= 0 && dst < n_out_rows) {
-          oi[k] = src * row_stride + (int64_t)c * VEC;
-          oo[k] = dst * row_stride + (int64_t)c * VEC;
+          oi[k] = src * in_stride + (int64_t)c * VEC;
+          oo[k] = dst * out_stride + (int64_t)c * VEC;
           buf[k] = ld16(v_in + oi[k]);
         }
       }
@@ -115,7 +116,8 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
 
 template <typename T, int D>
 hipError_t launch_t(void* k_out, const void* k_in, void* v_out, const void* v_in,
-                    int64_t n_out_rows, int64_t n_in_rows, int hkv, int64_t row_stride, int n_seg,
+                    int64_t n_out_rows, int64_t n_in_rows, int hkv, int64_t out_stride,
+                    int64_t in_stride, int n_seg,
                     const int32_t* seg_start, const int32_t* seg_len, const int32_t* seg_delta,
                     const int32_t* src_start, int max_seg_len, double theta, hipStream_t stream) {
   const int units_per_row = hkv * (D / 2) / Vec16<T>::N;
@@ -123,7 +125,7 @@ hipError_t launch_t(void* k_out, const void* k_in, void* v_out, const void* v_in
   dim3 grid((max_seg_len + rpb - 1) / rpb, n_seg);
   rerope_kernel<T, D><<<grid, kThreads, 0, stream>>>(
       static_cast<T*>(k_out), static_cast<const T*>(k_in), static_cast<T*>(v_out),
-      static_cast<const T*>(v_in), n_out_rows, n_in_rows, hkv, row_stride, rpb, seg_start,
+      static_cast<const T*>(v_in), n_out_rows, n_in_rows, hkv, out_stride, in_stride, rpb, seg_start,
       seg_len, seg_delta, src_start, theta);
   return hipGetLastError();
 }
@@ -132,13 +134,15 @@ hipError_t launch_t(void* k_out, const void* k_in, void* v_out, const void* v_in
 
 hipError_t launch_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in, bool bf16,
                          int64_t n_out_rows, int64_t n_in_rows, int hkv, int d,
-                         int64_t row_stride, int n_seg, const int32_t* seg_start,
+                         int64_t out_row_stride, int64_t in_row_stride, int n_seg,
+                         const int32_t* seg_start,
                          const int32_t* seg_len, const int32_t* seg_delta,
                          const int32_t* src_start, int max_seg_len, double theta,
                          hipStream_t stream) {
   if (n_seg == 0 || max_seg_len == 0 || n_out_rows == 0 || n_in_rows == 0) return hipSuccess;
 #define QCF_REROPE(T, D)                                                                       \
-  return launch_t<T, D>(k_out, k_in, v_out, v_in, n_out_rows, n_in_rows, hkv, row_stride, n_seg, \
+  return launch_t<T, D>(k_out, k_in, v_out, v_in, n_out_rows, n_in_rows, hkv, out_row_stride,   \
+                        in_row_stride, n_seg,                                                  \
                         seg_start, seg_len, seg_delta, src_start, max_seg_len, theta, stream)
   if (bf16) {
     if (d == 64) QCF_REROPE(uint16_t, 64);

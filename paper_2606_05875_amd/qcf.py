@@ -14,7 +14,8 @@ import os
 import torch
 
 __all__ = [
-    "QcfError", "lib", "lib_path", "qcf_version", "qcf_status_string", "qcf_rerope",
+    "QcfError", "lib", "lib_path", "qcf_version", "qcf_status_string", "qcf_recommended_row_stride",
+    "qcf_rerope",
     "qcf_assemble", "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
     "qcf_select_topk", "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
     "EXPORTS",
@@ -32,10 +33,11 @@ _SZ = ctypes.c_size_t
 EXPORTS = {
     "qcf_version": (_I, []),
     "qcf_status_string": (ctypes.c_char_p, [_I]),
-    "qcf_rerope": (_I, [_P, _P, _P, _P, _I, _I64, _I64, _I, _I, _I64, _I, _P, _P, _P, _P, _I,
+    "qcf_recommended_row_stride": (_I64, [_I, _I]),
+    "qcf_rerope": (_I, [_P, _P, _P, _P, _I, _I64, _I64, _I, _I, _I64, _I64, _I, _P, _P, _P, _P, _I,
                         ctypes.c_double, _P]),
-    "qcf_assemble": (_I, [_P, _P, _I64, _I64, _P, _P, _I64, _I, _P, _P, _P, _P, _I, _P, _P, _P, _I64,
-                          _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P, _I, _I, _I, _I,
+    "qcf_assemble": (_I, [_P, _P, _I64, _I64, _P, _P, _I64, _I64, _I, _P, _P, _P, _P, _I, _P, _P, _P,
+                          _I64, _I64, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _P, _P, _I, _I, _I, _I,
                           ctypes.c_double, _P]),
     "qcf_gather_rows": (_I, [_P, _P, _P, _I64, _I64, _I64, _I64, _I64, _P]),
     "qcf_scatter_kv": (_I, [_P, _P, _I64, _I64, _P, _P, _P, _P, _I64, _P, _I, _I64, _P, _P, _I, _I,
@@ -124,6 +126,14 @@ def qcf_status_string(status: int) -> str:
     return lib().qcf_status_string(status).decode()
 
 
+def qcf_recommended_row_stride(n_kv_heads, head_dim):
+    """Row stride (elements) for a K/V cache read by the attention and score kernels; host call."""
+    r = int(lib().qcf_recommended_row_stride(int(n_kv_heads), int(head_dim)))
+    if r <= 0:
+        raise QcfError(f"no row stride for n_kv_heads={n_kv_heads}, head_dim={head_dim}")
+    return r
+
+
 def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_theta, v_out=None,
                v_in=None, src_start=None):
     """Remap each segment's keys by its offset (and stitch its values); shapes [T, H_kv, d]."""
@@ -134,16 +144,17 @@ def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_the
     for n, t in (("seg_start", seg_start), ("seg_len", seg_len), ("seg_delta", seg_delta),
                  ("src_start", src_start)):
         _i32(t, n)
-    if k_out.shape[1:] != k_in.shape[1:] or k_out.stride(0) != k_in.stride(0):
-        raise QcfError("k_out and k_in must have the same row shape and row stride")
+    if k_out.shape[1:] != k_in.shape[1:]:
+        raise QcfError("k_out and k_in must have the same row shape")
     if (v_out is None) != (v_in is None):
         raise QcfError("v_out and v_in go together")
     if v_out is not None and (v_out.shape != k_out.shape or v_in.shape != k_in.shape
                               or v_out.stride(0) != k_out.stride(0) or v_in.stride(0) != k_in.stride(0)):
-        raise QcfError("v_out/v_in must match k_out/k_in")
+        raise QcfError("v_out/v_in must match k_out/k_in in shape and row stride")
     T_in, H, d = k_in.shape
     st = lib().qcf_rerope(_ptr(k_out), _ptr(k_in), _ptr(v_out), _ptr(v_in), _dtype(k_in),
-                          k_out.shape[0], T_in, H, d, _rows(k_in, "k_in"), seg_start.numel(),
+                          k_out.shape[0], T_in, H, d, _rows(k_out, "k_out"), _rows(k_in, "k_in"),
+                          seg_start.numel(),
                           _ptr(seg_start), _ptr(seg_len), _ptr(seg_delta), _ptr(src_start),
                           int(max_seg_len), float(rope_theta), _stream())
     _check(st, "qcf_rerope")
@@ -166,11 +177,13 @@ def qcf_assemble(k_cache, v_cache, k_pic, v_pic, seg_start, seg_len, seg_delta, 
         _i32(t, n)
     T, hkv, d = k_cache.shape
     rs = _rows(k_cache, "k_cache")
+    prs = _rows(k_pic, "k_pic")
+    qrs = _rows(probe_k, "probe_k")
     if (v_cache.shape != k_cache.shape or v_cache.stride(0) != rs or k_pic.shape[1:] != (hkv, d)
-            or v_pic.shape != k_pic.shape or k_pic.stride(0) != rs or v_pic.stride(0) != rs):
-        raise QcfError("k_cache/v_cache/k_pic/v_pic must share the row shape and row stride")
-    for n, t in (("q_new", q_new), ("k_new", k_new), ("v_new", v_new), ("q_u", q_u),
-                 ("probe_k", probe_k), ("probe_v", probe_v)):
+            or v_pic.shape != k_pic.shape or v_pic.stride(0) != prs or probe_v.stride(0) != qrs):
+        raise QcfError("k_cache/v_cache, k_pic/v_pic and probe_k/probe_v pairs must match in row "
+                       "shape and row stride")
+    for n, t in (("q_new", q_new), ("k_new", k_new), ("v_new", v_new), ("q_u", q_u)):
         if not t.is_contiguous():
             raise QcfError(f"{n} must be dense")
     hq = q_new.shape[1]
@@ -185,11 +198,11 @@ def qcf_assemble(k_cache, v_cache, k_pic, v_pic, seg_start, seg_len, seg_delta, 
             or probe_delta.numel() != npb):
         raise QcfError("probe_k/probe_v must be [len(probe_src), H_kv, d]")
     st = lib().qcf_assemble(_ptr(k_cache), _ptr(v_cache), T, rs, _ptr(k_pic), _ptr(v_pic),
-                            k_pic.shape[0], seg_start.numel(), _ptr(seg_start), _ptr(seg_len),
+                            k_pic.shape[0], prs, seg_start.numel(), _ptr(seg_start), _ptr(seg_len),
                             _ptr(seg_delta), _ptr(src_start), int(max_seg_len), _ptr(q_new),
                             _ptr(k_new), _ptr(v_new), k_new.shape[0], nq, _ptr(query_row),
                             _ptr(query_pos), _ptr(query_src), _ptr(query_slot), _ptr(q_u),
-                            _ptr(probe_k), _ptr(probe_v), npb, _ptr(probe_src), _ptr(probe_delta),
+                            _ptr(probe_k), _ptr(probe_v), npb, qrs, _ptr(probe_src), _ptr(probe_delta),
                             _dtype(k_pic), hq, hkv, d, float(rope_theta), _stream())
     _check(st, "qcf_assemble")
 

@@ -112,6 +112,13 @@ class FusionPlan:
             max_seg=int(w.seg_len.max() if w.n_chunks else 0))
 
 
+def kv_buffer(rows, hkv, d, dtype, device, zero=False):
+    """[rows, hkv, d] K/V buffer whose rows are qcf_recommended_row_stride elements apart."""
+    stride = qcf.qcf_recommended_row_stride(hkv, d)
+    alloc = torch.zeros if zero else torch.empty
+    return alloc((rows, stride), dtype=dtype, device=device)[:, :hkv * d].view(rows, hkv, d)
+
+
 class FusionStep:
     """Device buffers and the call chain of one layer's fusion step for workload ``w``.
 
@@ -149,16 +156,17 @@ class FusionStep:
         self.probe_src, self.probe_delta = t(p.probe_src), t(p.probe_delta)
         self.query_slot = t(p.query_slot)
         self.R_idx_init, self.R_pos_init = t(p.R_idx_init), t(p.R_pos_init)
-        # working state and outputs
-        self.k = torch.zeros_like(self.k_pic)
-        self.v = torch.zeros_like(self.v_pic)
+        # working state and outputs; the caches the attention and score kernels read (the
+        # request cache and the probe buffer) get the library's padded row stride
+        self.k = kv_buffer(T, hkv, d, dt, dev, zero=True)
+        self.v = kv_buffer(T, hkv, d, dt, dev, zero=True)
         self.R_idx = self.R_idx_init.clone()
         self.R_pos = self.R_pos_init.clone()
         nU, nR, nP = p.u_idx.size, p.R_idx_init.size, p.probe_idx.size
         self.q_u = torch.empty((nU, hq, d), dtype=dt, device=dev)
         self.q_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
-        self.k_probe = torch.empty((nP, hkv, d), dtype=dt, device=dev)
-        self.v_probe = torch.empty((nP, hkv, d), dtype=dt, device=dev)
+        self.k_probe = kv_buffer(nP, hkv, d, dt, dev)
+        self.v_probe = kv_buffer(nP, hkv, d, dt, dev)
         self.o_probe = torch.empty((nU, hq, d), dtype=dt, device=dev)
         self.o = torch.empty((nR, hq, d), dtype=dt, device=dev)
         self.scores = torch.zeros(T, dtype=torch.float32, device=dev)

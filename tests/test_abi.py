@@ -20,7 +20,7 @@ def _declared():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     out = {}
-    for m in re.finditer(r"\b(?:qcf_status|size_t|int|const char\*)\s+(qcf_\w+)\s*\(([^;]*?)\)\s*;", text, re.S):
+    for m in re.finditer(r"\b(?:qcf_status|size_t|int64_t|int|const char\*)\s+(qcf_\w+)\s*\(([^;]*?)\)\s*;", text, re.S):
         args = m.group(2).strip()
         out[m.group(1)] = 0 if args in ("", "void") else args.count(",") + 1
     return out
@@ -36,7 +36,8 @@ def L():
 
 def test_every_declared_symbol_is_exported(L):
     decl = _declared()
-    assert set(decl) == {"qcf_version", "qcf_status_string", "qcf_rerope", "qcf_assemble",
+    assert set(decl) == {"qcf_version", "qcf_status_string", "qcf_recommended_row_stride",
+                         "qcf_rerope", "qcf_assemble",
                          "qcf_gather_rows",
                          "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
                          "qcf_select_topk", "qcf_sparse_prefill_attn_workspace_size",
@@ -48,7 +49,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.qcf_version() == 100
+    assert L.qcf_version() == 101
     for code in range(5):
         assert L.qcf_status_string(code)
     assert L.qcf_status_string(0) == b"ok"
@@ -56,13 +57,16 @@ def test_version_and_status_strings(L):
 
 def test_rerope_validation(L):
     s = None
-    r = lambda ko=A, ki=A, vo=None, vi=None, dt=BF16, n=10, d=128, stride=1024, theta=1e4, nseg=1: \
-        L.qcf_rerope(ko, ki, vo, vi, dt, n, n, 8, d, stride, nseg, A, A, A, None, 10, theta, s)
+    r = lambda ko=A, ki=A, vo=None, vi=None, dt=BF16, n=10, d=128, stride=1024, theta=1e4, nseg=1, \
+        istride=1024: L.qcf_rerope(ko, ki, vo, vi, dt, n, n, 8, d, stride, istride, nseg, A, A, A, None,
+                                   10, theta, s)
     assert r(ko=None, ki=None) == INVALID                 # null tensors with work to do
     assert r(d=96) == UNSUPPORTED
     assert r(dt=7) == UNSUPPORTED
     assert r(stride=512) == INVALID                       # row stride below H_kv * d
     assert r(stride=1028) == INVALID                      # not a 16-byte multiple
+    assert r(istride=1000) == INVALID                     # input stride below H_kv * d
+    assert r(stride=1152) == INVALID                      # in place with different strides
     assert r(ko=MIS) == INVALID                           # misaligned base
     assert r(theta=0.0) == INVALID
     assert r(n=-1) == INVALID
@@ -70,21 +74,23 @@ def test_rerope_validation(L):
     assert r(vo=A, vi=MIS) == INVALID
     assert r(nseg=70000) == UNSUPPORTED
     # nothing to do: OK without touching the device
-    assert L.qcf_rerope(None, None, None, None, BF16, 0, 0, 8, 128, 1024, 0, None, None, None, None,
-                        0, 1e4, s) == OK
+    assert L.qcf_rerope(None, None, None, None, BF16, 0, 0, 8, 128, 1024, 1024, 0, None, None, None,
+                        None, 0, 1e4, s) == OK
 
 
 def test_assemble_validation(L):
     def a(**kw):
         g = kw.get
-        return [g("kc", A), A, 100, g("stride", 1024), g("kp", A), A, 100, g("nseg", 2), A, A, A,
-                None, 50, g("qn", A), A, A, 100, g("nq", 4), A, A, None, g("slot", None), g("qu", A),
-                g("pk", A), A, g("np_", 8), A, A, g("dt", BF16), g("hq", 32), 8, g("d", 128),
-                g("theta", 1e4), None]
+        return [g("kc", A), A, 100, g("stride", 1024), g("kp", A), A, 100, g("pstride", 1024),
+                g("nseg", 2), A, A, A, None, 50, g("qn", A), A, A, 100, g("nq", 4), A, A, None,
+                g("slot", None), g("qu", A), g("pk", A), A, g("np_", 8), g("qstride", 1024), A, A,
+                g("dt", BF16), g("hq", 32), 8, g("d", 128), g("theta", 1e4), None]
     assert L.qcf_assemble(*a(dt=7)) == UNSUPPORTED
     assert L.qcf_assemble(*a(d=96)) == UNSUPPORTED
     assert L.qcf_assemble(*a(hq=36)) == INVALID
     assert L.qcf_assemble(*a(stride=1000)) == INVALID
+    assert L.qcf_assemble(*a(pstride=1000)) == INVALID
+    assert L.qcf_assemble(*a(qstride=1028)) == INVALID
     assert L.qcf_assemble(*a(theta=0.0)) == INVALID
     assert L.qcf_assemble(*a(kc=None)) == INVALID                 # cache written by segments
     assert L.qcf_assemble(*a(kp=MIS)) == INVALID
@@ -92,9 +98,19 @@ def test_assemble_validation(L):
     assert L.qcf_assemble(*a(pk=None)) == INVALID                 # probe slots to fill
     assert L.qcf_assemble(*a(nq=-1)) == INVALID
     # nothing to do: every pointer may be null
-    assert L.qcf_assemble(None, None, 0, 1024, None, None, 0, 0, None, None, None, None, 0, None,
-                          None, None, 0, 0, None, None, None, None, None, None, None, 0, None, None,
-                          BF16, 32, 8, 128, 1e4, None) == OK
+    assert L.qcf_assemble(None, None, 0, 1024, None, None, 0, 1024, 0, None, None, None, None, 0,
+                          None, None, None, 0, 0, None, None, None, None, None, None, None, 0, 1024,
+                          None, None, BF16, 32, 8, 128, 1e4, None) == OK
+
+
+def test_recommended_row_stride(L):
+    assert L.qcf_recommended_row_stride(8, 128) == 9 * 128      # even: one slice of padding
+    assert L.qcf_recommended_row_stride(2, 64) == 3 * 64
+    assert L.qcf_recommended_row_stride(1, 128) == 128          # odd: dense rows
+    assert L.qcf_recommended_row_stride(5, 64) == 5 * 64
+    assert L.qcf_recommended_row_stride(0, 128) == 0
+    assert L.qcf_recommended_row_stride(8, 96) == 0
+    assert qcf.qcf_recommended_row_stride(8, 128) == 1152
 
 
 def test_gather_validation(L):

@@ -34,6 +34,16 @@ def host(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
+def padded(a, pad, dtype):
+    """[rows, heads, d] device copy of a whose rows are `pad` elements longer than dense."""
+    rows = a.shape[0]
+    width = int(np.prod(a.shape[1:]))
+    base = torch.zeros((rows, width + pad), dtype=dtype, device="cuda")
+    view = base[:, :width].view(a.shape)
+    view.copy_(dev(a, dtype))
+    return view
+
+
 def draw(rng, shape, dtype, scale=1.0):
     x = (rng.standard_normal(shape) * scale).astype(np.float32)
     return round_to_bf16(x) if dtype == "bf16" else x
@@ -84,8 +94,9 @@ def test_rerope_from_chunk_store():
     seg_start = np.concatenate([[0], np.cumsum(lens)[:-1]])
     T = int(lens.sum()) + 16                                          # + query slots
     i32 = lambda a: dev(np.asarray(a, np.int32))
-    ko = torch.zeros((T, hkv, d), dtype=torch.bfloat16, device="cuda")
-    vo = torch.zeros_like(ko)
+    # request cache with padded rows (stride (H_kv + 1) * d), store dense
+    ko = padded(np.zeros((T, hkv, d), np.float32), d, torch.bfloat16)
+    vo = padded(np.zeros((T, hkv, d), np.float32), d, torch.bfloat16)
     qcf.qcf_rerope(ko, dev(pool_k, torch.bfloat16), i32(seg_start), i32(lens), i32(seg_start), 512, 5e5,
                    v_out=vo, v_in=dev(pool_v, torch.bfloat16), src_start=i32(store_start[order]))
     gk, gv = host(ko), host(vo)
@@ -95,12 +106,17 @@ def test_rerope_from_chunk_store():
         assert_ulp(gk[a:a + n], want, "bf16", f"chunk {c}")
         np.testing.assert_array_equal(gv[a:a + n], pool_v[src:src + n])
     assert np.all(gk[-16:] == 0)
+    assert not ko._base[:, hkv * d:].any() and not vo._base[:, hkv * d:].any()   # padding untouched
 
 
-@pytest.mark.parametrize("dtype,hq,hkv,d", [("bf16", 32, 8, 128), ("bf16", 16, 2, 64), ("f32", 8, 4, 128)])
-def test_assemble(dtype, hq, hkv, d):
-    """One launch: chunk remap + value stitch, query rows, probe buffer (anchors from the store)."""
-    say("assemble", dtype, hq, hkv, d)
+@pytest.mark.parametrize("dtype,hq,hkv,d,pads", [("bf16", 32, 8, 128, (0, 0, 0)), ("bf16", 16, 2, 64, (0, 0, 0)),
+                                                 ("f32", 8, 4, 128, (0, 0, 0)),
+                                                 ("bf16", 32, 8, 128, (128, 8, 136)),
+                                                 ("f32", 8, 2, 64, (4, 64, 0))])
+def test_assemble(dtype, hq, hkv, d, pads):
+    """One launch: chunk remap + value stitch, query rows, probe buffer (anchors from the store);
+    the cache, the chunk store and the probe buffer may each have their own padded row stride."""
+    say("assemble", dtype, hq, hkv, d, pads)
     rng = np.random.default_rng(21)
     theta = 5e5
     store_lens = np.array([513, 1, 300, 77, 1024])
@@ -134,12 +150,13 @@ def test_assemble(dtype, hq, hkv, d):
     slot = na + np.arange(nq)
     t = DT[dtype]
     i32 = lambda a: dev(np.asarray(a, np.int32))
-    kc = torch.full((T, hkv, d), 7.0, dtype=t, device="cuda")
-    vc = torch.full_like(kc, 7.0)
+    pc, pp, pq = pads
+    kc = padded(np.full((T, hkv, d), 7.0, np.float32), pc, t)
+    vc = padded(np.full((T, hkv, d), 7.0, np.float32), pc, t)
     qu = torch.empty((nq, hq, d), dtype=t, device="cuda")
-    pk = torch.empty((na + nq, hkv, d), dtype=t, device="cuda")
-    pv = torch.empty_like(pk)
-    qcf.qcf_assemble(kc, vc, dev(pool_k, t), dev(pool_v, t), i32(seg_start), i32(lens), i32(delta),
+    pk = padded(np.zeros((na + nq, hkv, d), np.float32), pq, t)
+    pv = padded(np.zeros((na + nq, hkv, d), np.float32), pq, t)
+    qcf.qcf_assemble(kc, vc, padded(pool_k, pp, t), padded(pool_v, pp, t), i32(seg_start), i32(lens), i32(delta),
                      int(lens.max()), dev(qn, t), dev(kn, t), dev(vn, t), i32(qrow), i32(qpos), qu, pk, pv,
                      i32(probe_src), i32(probe_delta), theta, src_start=i32(src_start),
                      query_src=i32(qrow), query_slot=i32(slot))

@@ -191,9 +191,10 @@ qcf_status qcf_assemble(void* k_cache, void* v_cache, int64_t n_rows, int64_t ro
  *   cu_q    [batch+1], cu_kv [batch+1], ctx_len [batch] device arrays;
  *   max_q_len >= max_b(cu_q[b+1]-cu_q[b]), max_ctx_len >= max_b ctx_len[b]
  *   workspace  >= qcf_probe_scores_workspace_size(...) bytes, 256-byte aligned; it
- *              holds the per-split softmax statistics between the two kernels and
- *              needs no initialisation.  Calls that overlap in time need separate
- *              workspaces.
+ *              holds the per-split softmax statistics and per-(KV head, query tile)
+ *              column sums between the kernels of the call and needs no
+ *              initialisation.  A workspace sized for one shape serves every
+ *              smaller one.  Calls that overlap in time need separate workspaces.
  */
 size_t qcf_probe_scores_workspace_size(int batch, int max_q_len, int max_ctx_len,
                                        int n_q_heads, int n_kv_heads, int head_dim);

@@ -22,7 +22,10 @@ constexpr int kUnits = 4;  // 16-byte units per thread per pass
 
 // rotate `nrows` rows (src rows s0.., dst rows d0..) of hkv heads by the angle
 // table cs; rows outside the bounds are skipped; V is copied alongside when
-// vdst is set.  All loads of a pass are issued before its stores.
+// vdst is set.  A round covers kUnits key units (rotate-half pairs) and
+// 2 kUnits value units per thread; all of its loads are issued, unmasked from
+// clamped rows, before its first store (a load under a lane condition gets a
+// wait of its own, which would serialise the round trips).
 template <typename T, int D>
 __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride, const T* ksrc,
                                            const T* vsrc, int64_t src_stride, int64_t s0,
@@ -32,64 +35,61 @@ __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride,
   constexpr int VEC = Vec16<T>::N;
   constexpr int UPH = HALF / VEC;
   const int upr = hkv * UPH;           // key units per row (rotate-half pairs)
-  const int vpr = hkv * D / VEC;       // value units per row
-  const int total = nrows * (upr + vpr);
-  for (int base = 0; base < total; base += kThreads * kUnits) {
-    uint4 a[kUnits], b[kUnits];
-    int64_t so[kUnits], dofs[kUnits];
-    int kind[kUnits], jj[kUnits];  // 0: skip, 1: key pair, 2: value
+  const int vpr = 2 * upr;             // value units per row
+  const int64_t s_hi = n_src - 1;
+  const int total_k = nrows * upr, total_v = vdst ? nrows * vpr : 0;
+  for (int kb = 0, vb = 0; kb < total_k || vb < total_v;
+       kb += kThreads * kUnits, vb += 2 * kThreads * kUnits) {
+    uint4 a[kUnits], b[kUnits], va[2 * kUnits];
+    int64_t kofs[kUnits], vofs[2 * kUnits];
+    int jj[kUnits];
+    bool kok[kUnits], vok[2 * kUnits];
 #pragma unroll
     for (int k = 0; k < kUnits; ++k) {
-      const int u = base + threadIdx.x + k * kThreads;
-      kind[k] = 0;
-      jj[k] = 0;
-      if (u >= total) continue;
-      int r, c;
-      bool is_key;
-      if (u < nrows * upr) {
-        r = u / upr;
-        c = u - r * upr;
-        is_key = true;
-      } else {
-        const int uv = u - nrows * upr;
-        r = uv / vpr;
-        c = uv - r * vpr;
-        is_key = false;
-      }
+      const int u = kb + threadIdx.x + k * kThreads;
+      const int uc = min(u, max(total_k - 1, 0));
+      const int r = uc / upr, c = uc - r * upr;
+      const int h = c / UPH;
       const int64_t s = s0 + r, d = d0 + r;
-      if (s < 0 || s >= n_src || d < 0 || d >= n_dst) continue;
-      if (is_key) {
-        const int h = c / UPH;
-        jj[k] = (c - h * UPH) * VEC;
-        so[k] = s * src_stride + (int64_t)h * D + jj[k];
-        dofs[k] = d * dst_stride + (int64_t)h * D + jj[k];
-        a[k] = ld16(ksrc + so[k]);
-        b[k] = ld16(ksrc + so[k] + HALF);
-        kind[k] = 1;
-      } else if (vdst) {
-        so[k] = s * src_stride + (int64_t)c * VEC;
-        dofs[k] = d * dst_stride + (int64_t)c * VEC;
-        a[k] = ld16(vsrc + so[k]);
-        kind[k] = 2;
+      kok[k] = u < total_k && s >= 0 && s < n_src && d >= 0 && d < n_dst;
+      jj[k] = (c - h * UPH) * VEC;
+      const int64_t so = min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)h * D + jj[k];
+      kofs[k] = d * dst_stride + (int64_t)h * D + jj[k];
+      a[k] = ld16(ksrc + so);
+      b[k] = ld16(ksrc + so + HALF);
+    }
+    if (vdst) {
+#pragma unroll
+      for (int k = 0; k < 2 * kUnits; ++k) {
+        const int u = vb + threadIdx.x + k * kThreads;
+        const int uc = min(u, max(total_v - 1, 0));
+        const int r = uc / vpr, c = uc - r * vpr;
+        const int64_t s = s0 + r, d = d0 + r;
+        vok[k] = u < total_v && s >= 0 && s < n_src && d >= 0 && d < n_dst;
+        vofs[k] = d * dst_stride + (int64_t)c * VEC;
+        va[k] = ld16(vsrc + min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)c * VEC);
       }
     }
 #pragma unroll
     for (int k = 0; k < kUnits; ++k) {
-      if (kind[k] == 1) {
-        float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
-        Vec16<T>::unpack(a[k], x1);
-        Vec16<T>::unpack(b[k], x2);
+      float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
+      Vec16<T>::unpack(a[k], x1);
+      Vec16<T>::unpack(b[k], x2);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const float2 rr = cs[jj[k] + e];
-          y1[e] = x1[e] * rr.x - x2[e] * rr.y;
-          y2[e] = x1[e] * rr.y + x2[e] * rr.x;
-        }
-        st16(kdst + dofs[k], Vec16<T>::pack(y1));
-        st16(kdst + dofs[k] + HALF, Vec16<T>::pack(y2));
-      } else if (kind[k] == 2) {
-        st16(vdst + dofs[k], a[k]);
+      for (int e = 0; e < VEC; ++e) {
+        const float2 rr = cs[jj[k] + e];
+        y1[e] = x1[e] * rr.x - x2[e] * rr.y;
+        y2[e] = x1[e] * rr.y + x2[e] * rr.x;
       }
+      if (kok[k]) {
+        st16(kdst + kofs[k], Vec16<T>::pack(y1));
+        st16(kdst + kofs[k] + HALF, Vec16<T>::pack(y2));
+      }
+    }
+    if (vdst) {
+#pragma unroll
+      for (int k = 0; k < 2 * kUnits; ++k)
+        if (vok[k]) st16(vdst + vofs[k], va[k]);
     }
   }
 }
@@ -205,8 +205,9 @@ hipError_t assemble_t(const AssembleShape& s, const AssemblePtrs& p, hipStream_t
   A.seg_delta = p.seg_delta;
   A.src_start = p.src_start;
   A.n_seg = s.n_seg;
-  const int units_per_row = s.hkv * (D / 2) / Vec16<T>::N * 3;  // key pairs + values
-  A.rows_per_block = max(1, kThreads * kUnits / units_per_row);
+  // rows per chunk tile: one round of kUnits key units per thread
+  const int key_units_per_row = s.hkv * (D / 2) / Vec16<T>::N;
+  A.rows_per_block = max(1, kThreads * kUnits / key_units_per_row);
   A.tiles_per_seg = (s.max_seg_len + A.rows_per_block - 1) / A.rows_per_block;
   A.k_new = static_cast<const T*>(p.k_new);
   A.v_new = static_cast<const T*>(p.v_new);
@@ -224,7 +225,7 @@ hipError_t assemble_t(const AssembleShape& s, const AssemblePtrs& p, hipStream_t
   A.probe_stride = s.probe_row_stride;
   A.probe_src = p.probe_src;
   A.probe_delta = p.probe_delta;
-  A.probe_rows_per_block = 4;
+  A.probe_rows_per_block = 1;  // one slot per block: its loads are the only round trip
   A.hq = s.hq;
   A.hkv = s.hkv;
   A.theta = s.theta;

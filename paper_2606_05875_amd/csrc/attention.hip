@@ -392,7 +392,7 @@ constexpr int kStreamBlocks = 256;    // persistent blocks (one per CU of MI355X
 // flight before the first product, plus its output stores), in key steps:
 // each row tile counts as this many extra steps when the ranges are cut, so
 // a block that starts several tiles gets fewer key steps.
-constexpr int kSegCost = 2;
+constexpr int kSegCost = 4;
 
 template <int D, bool kStream>
 __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
@@ -488,14 +488,18 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     issue(0);
     issue(1);
     issue(2);
-    const int qpos = valid ? row_pos[grow] : INT_MIN;
+    // unconditional loads from a real row (a load under a lane condition gets a
+    // wait of its own, which would also wait for the tiles above); a padding
+    // lane's Q only has to be finite: its keys are all masked
+    const int64_t crow = min(grow, n_rows - 1);
+    const int pos_raw = row_pos[crow];
     bf16x8 qreg[D / 16];
     {
-      const uint16_t* qp = q + grow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
+      const uint16_t* qp = q + crow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
 #pragma unroll
-      for (int st = 0; st < D / 16; ++st)
-        qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
+      for (int st = 0; st < D / 16; ++st) qreg[st] = as_bf16x8(ld16(qp + 16 * st));
     }
+    const int qpos = valid ? pos_raw : INT_MIN;
     const int wmax = wave_max_i(valid ? qpos : -1);
     const int wmin = wave_min_i(valid ? qpos : INT_MAX);
     const int wave_end = min(nkv, wmax + 1);
@@ -686,7 +690,8 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     int nkv = cu_kv[b + 1] - (int)kv0;
     if (kv0 + nkv > n_kv_rows) nkv = (int)(n_kv_rows - kv0);
     const int rl = tile * rpb + (qv >> lg);
-    const int mx = wave_max_i(rl < nr && r0 + rl < n_rows ? row_pos[r0 + rl] : -1);
+    const int pos_raw = row_pos[min(r0 + rl, n_rows - 1)];
+    const int mx = wave_max_i(rl < nr && r0 + rl < n_rows ? pos_raw : -1);
     if (l == 0) red[w] = mx;
     __syncthreads();
     int bmax = red[0];
@@ -712,17 +717,30 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     return kv0 + nkv > n_kv_rows ? (int)(n_kv_rows - kv0) : nkv;
   };
   for (int i0 = w; i0 < n_tiles; i0 += 4 * kW8) {
-    int mx[4];
+    // all position loads of the four tiles go out before any is used (clamped
+    // to a real row, masked afterwards)
+    constexpr int RR = kW8Qv / 64;  // lanes' passes over a tile's rows (rows per tile <= kW8Qv)
+    int pv[4][RR];
+    bool ok[4][RR];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * kW8;
-      mx[u] = -1;
-      if (i >= n_tiles) continue;
+      const int i = min(i0 + u * kW8, n_tiles - 1);
       const int b = i / max_tiles, tile = i - b * max_tiles;
       const int64_t r0 = req_rows[b];
       const int nr = req_rows[b + 1] - (int)r0;
-      for (int rr = tile * rpb + l; rr < min(nr, (tile + 1) * rpb); rr += 64)
-        if (r0 + rr < n_rows) mx[u] = max(mx[u], row_pos[r0 + rr]);
+#pragma unroll
+      for (int k = 0; k < RR; ++k) {
+        const int rr = tile * rpb + l + 64 * k;
+        ok[u][k] = i0 + u * kW8 < n_tiles && l + 64 * k < rpb && rr < nr && r0 + rr < n_rows;
+        pv[u][k] = row_pos[min(r0 + rr, n_rows - 1)];
+      }
+    }
+    int mx[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      mx[u] = -1;
+#pragma unroll
+      for (int k = 0; k < RR; ++k) mx[u] = max(mx[u], ok[u][k] ? pv[u][k] : -1);
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {

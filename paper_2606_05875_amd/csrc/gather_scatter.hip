@@ -29,30 +29,48 @@ __global__ __launch_bounds__(kThreads) void gather_rows_kernel(
   }
 }
 
-// Rotate `units` 16-byte rotate-half vectors of a row: unit u covers head
-// u / UPH, pair offset j = (u % UPH) * VEC.
+// One recomputed row per block.  Every load of the row -- the value heads,
+// the key heads' and the query heads' rotate-half pairs, kRound units of each
+// per thread -- is issued, unmasked from clamped units, before the first
+// store (a load under a lane condition gets a wait of its own); the angle
+// table is formed meanwhile.  Rows wider than a round finish in later rounds.
+constexpr int kRound = 2;
+
 template <typename T, int D>
-__device__ __forceinline__ void rope_row(T* dst, const T* src, int units, const float2* cs) {
-  constexpr int HALF = D / 2;
-  constexpr int VEC = Vec16<T>::N;
-  constexpr int UPH = HALF / VEC;
-  for (int u = threadIdx.x; u < units; u += kThreads) {
-    const int h = u / UPH;
-    const int j = (u - h * UPH) * VEC;
-    const int off = h * D + j;
-    float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
-    Vec16<T>::unpack(ld16(src + off), x1);
-    Vec16<T>::unpack(ld16(src + off + HALF), x2);
+struct RopeUnits {
+  static constexpr int HALF = D / 2, VEC = Vec16<T>::N, UPH = HALF / VEC;
+  uint4 a[kRound], b[kRound];
+  int off[kRound], jj[kRound];
+  __device__ __forceinline__ void load(const T* src, int base, int units) {
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      const float2 r = cs[j + e];
-      y1[e] = x1[e] * r.x - x2[e] * r.y;
-      y2[e] = x1[e] * r.y + x2[e] * r.x;
+    for (int k = 0; k < kRound; ++k) {
+      const int u = min(base + (int)threadIdx.x + k * kThreads, units - 1);
+      const int h = u / UPH;
+      jj[k] = (u - h * UPH) * VEC;
+      off[k] = h * D + jj[k];
+      a[k] = ld16(src + off[k]);
+      b[k] = ld16(src + off[k] + HALF);
     }
-    st16(dst + off, Vec16<T>::pack(y1));
-    st16(dst + off + HALF, Vec16<T>::pack(y2));
   }
-}
+  __device__ __forceinline__ void store(T* dst, int base, int units, const float2* cs) const {
+#pragma unroll
+    for (int k = 0; k < kRound; ++k) {
+      float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
+      Vec16<T>::unpack(a[k], x1);
+      Vec16<T>::unpack(b[k], x2);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float2 r = cs[jj[k] + e];
+        y1[e] = x1[e] * r.x - x2[e] * r.y;
+        y2[e] = x1[e] * r.y + x2[e] * r.x;
+      }
+      if (base + (int)threadIdx.x + k * kThreads < units) {
+        st16(dst + off[k], Vec16<T>::pack(y1));
+        st16(dst + off[k] + HALF, Vec16<T>::pack(y2));
+      }
+    }
+  }
+};
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void scatter_kv_kernel(
@@ -62,24 +80,40 @@ __global__ __launch_bounds__(kThreads) void scatter_kv_kernel(
     double theta) {
   constexpr int HALF = D / 2;
   constexpr int VEC = Vec16<T>::N;
+  constexpr int UPH = HALF / VEC;
   __shared__ float2 cs[HALF];
   const int64_t r = blockIdx.x;
   const int64_t s = src_idx ? (int64_t)src_idx[r] : r;
   if (s < 0 || s >= n_src_rows) return;
   const int64_t dst = row_idx[r];
   const bool dst_ok = dst >= 0 && dst < n_cache_rows;
-  if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)row_pos[r], threadIdx.x, D, theta);
-  __syncthreads();
-  const int kv_row = hkv * D;
-  if (dst_ok) {
-    rope_row<T, D>(k_cache + dst * cache_stride, k_new + s * kv_row, hkv * (HALF / VEC), cs);
-    const T* vs = v_new + s * kv_row;
-    T* vd = v_cache + dst * cache_stride;
-    for (int c = threadIdx.x; c < kv_row / VEC; c += kThreads) st16(vd + c * VEC, ld16(vs + c * VEC));
-  }
-  if (q_out) {
-    const int q_row = hq * D;
-    rope_row<T, D>(q_out + r * q_row, q_new + s * q_row, hq * (HALF / VEC), cs);
+  const int kv_row = hkv * D, q_row = hq * D;
+  const int nv = kv_row / VEC, nk = hkv * UPH, nq = q_out ? hq * UPH : 0;
+  const T* vs = v_new + s * kv_row;
+  const T* ks = k_new + s * kv_row;
+  const T* qs = q_new ? q_new + s * q_row : nullptr;
+  T* vd = v_cache + (dst_ok ? dst : 0) * cache_stride;
+  T* kd = k_cache + (dst_ok ? dst : 0) * cache_stride;
+  for (int base = 0; base < max(max(nv, nk), nq); base += kThreads * kRound) {
+    uint4 vbuf[kRound];
+#pragma unroll
+    for (int k = 0; k < kRound; ++k) vbuf[k] = ld16(vs + min(base + (int)threadIdx.x + k * kThreads, nv - 1) * VEC);
+    RopeUnits<T, D> ku, qu;
+    ku.load(ks, min(base, nk - 1), nk);
+    if (nq > 0) qu.load(qs, min(base, nq - 1), nq);
+    if (base == 0) {
+      if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)row_pos[r], threadIdx.x, D, theta);
+      __syncthreads();
+    }
+    if (dst_ok) {
+      if (base < nk) ku.store(kd, base, nk, cs);
+#pragma unroll
+      for (int k = 0; k < kRound; ++k) {
+        const int c = base + threadIdx.x + k * kThreads;
+        if (c < nv) st16(vd + c * VEC, vbuf[k]);
+      }
+    }
+    if (base < nq) qu.store(q_out + r * q_row, base, nq, cs);
   }
 }
 

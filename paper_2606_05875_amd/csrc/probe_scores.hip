@@ -3,29 +3,33 @@
 //
 // I(t) = sum_{i,h} softmax_t(q_{i,h} . k_{t,g(h)} * scale) needs every query
 // row's softmax denominator over all N context keys before any column can be
-// summed, so the bf16 path runs in two launches:
-//   stats   : grid (128-query-vector tile, KV head x key split, request), at
-//             most 16 key splits.  Each wave holds 32 query vectors of one
-//             KV-head group in registers; the split's keys pass through LDS in
-//             128-key sub-tiles (the next one prefetched into registers while
-//             the current one is in use) and every row keeps an online
-//             (max, sum); the split's base-2 log-sum-exp is written.  The
-//             first split's blocks also store their Q registers in MFMA
-//             operand order, so the column pass reads them contiguously.
-//   columns : grid (32-key chunk, request).  The block's eight waves share out
-//             the (KV head, 32-query-vector) items of the request, one head at
-//             a time per wave; for each item a wave merges the query vectors'
-//             split log-sum-exps in a fixed order, recomputes the logits
-//             against its keys (held in registers per head) and adds the
-//             probabilities 2^(logit - lse) per key.  The waves' per-key sums are added in wave order in LDS and
-//             written (or added) to the scores.
-// No block waits for another: the two launches are the only global
-// synchronisation.  QK^T runs on the matrix cores as S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16: A = 32 keys x 16 d (a 16-byte row slice of K per
-// lane), B = 16 d x 32 query vectors (a 16-byte row slice of Q per lane).  The
-// fp32 path uses the vector ALUs.  Every reduction has a fixed order, so
-// results are deterministic.
+// summed, so the bf16 path runs in three launches over the same grid of
+// (KV head, 256-query-vector tile, key split, request) blocks, the head
+// fastest, with the splits chosen for about 512 blocks:
+//   stats   : each of the 8 waves holds 32 query vectors of one KV-head group
+//             in registers; the split's keys pass through LDS (128 at a time,
+//             the next ones prefetched into registers) in 32-key products,
+//             and every vector keeps an online (max, sum); the split's base-2
+//             log-sum-exp is written.
+//   columns : the same tiles again.  Each vector's log-sum-exp over all splits
+//             is merged once per block (its partials loaded together, folded
+//             in split order); the logits are recomputed and each key's
+//             probabilities 2^(logit - lse) summed over the tile's vectors
+//             into a per-(head, tile) column buffer.
+//   final   : scores[t] (+)= those column sums in (head, tile) order.
+// Every block issues its loads together and waits once per K chunk: on this
+// part a dependent round trip to memory costs microseconds under load.
+// No block waits for another: the launches are the only global
+// synchronisation.  QK^T runs on the matrix cores (v_mfma_f32_32x32x16_bf16)
+// with the same operand registers either way round: the statistics take S^T =
+// K Q^T (a lane owns one query vector, so its max and sum stay in the lane),
+// the columns take S = Q K^T (a lane owns one key, so its sum over the query
+// vectors is 16 in-lane additions and one lane swap).  The fp32 path uses the
+// vector ALUs.  Every reduction has a fixed order, so results are
+// deterministic.
 #include <math.h>
+
+#include <algorithm>
 
 #include "qcf_device.h"
 #include "qcf_launch.h"
@@ -33,15 +37,16 @@
 namespace qcf {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kQvPerBlock = 128;  // stats pass: 4 waves x 32 query vectors
-constexpr int kSubKeys = 128;     // stats pass: keys per LDS sub-tile
-constexpr int kMaxSplits = 16;    // stats pass: key splits per query tile
-constexpr int kColKeys = 32;      // column pass: keys per block
+constexpr int kThreads = 256;      // fp32 path, final pass
+constexpr int kW = 8;              // bf16 path: waves per block
+constexpr int kQvTile = 32 * kW;   // query vectors per block
+constexpr int kChunkKeys = 128;    // keys staged in LDS at a time
+constexpr int kMaxSplits = 64;     // key splits per query tile
+constexpr int kPassBlocks = 512;   // blocks aimed for when choosing the splits
 
 struct WsLayout {
-  size_t part_off, frag_off, total;
-  int n_splits, n_sub, max_qv, n_qt;
+  size_t part_off, col_off, total;
+  int n_qt, n_splits, split_keys, max_qv;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -50,18 +55,20 @@ WsLayout ws_layout(const ProbeShape& s) {
   WsLayout w{};
   const int grp = s.hq / s.hkv;
   w.max_qv = s.max_q_len * grp;
-  w.n_qt = (w.max_qv + kQvPerBlock - 1) / kQvPerBlock;
-  const int sub_tiles = (s.max_ctx_len + kSubKeys - 1) / kSubKeys;
-  w.n_sub = (sub_tiles + kMaxSplits - 1) / kMaxSplits;
-  if (w.n_sub < 1) w.n_sub = 1;
-  w.n_splits = (sub_tiles + w.n_sub - 1) / w.n_sub;
-  if (w.n_splits < 1) w.n_splits = 1;
+  w.n_qt = (w.max_qv + kQvTile - 1) / kQvTile;
+  // key splits of whole 32-key groups, about kPassBlocks blocks per pass
+  const int64_t per_split = (int64_t)std::max(1, w.n_qt) * s.hkv * std::max(1, s.batch);
+  const int want = (int)std::min<int64_t>(
+      kMaxSplits, std::max<int64_t>(1, (kPassBlocks + per_split - 1) / per_split));
+  const int ctx = std::max(1, s.max_ctx_len);
+  w.split_keys = ((ctx + want - 1) / want + 31) / 32 * 32;
+  w.n_splits = (ctx + w.split_keys - 1) / w.split_keys;
   const size_t nb = (size_t)s.batch * s.hkv;
+  // both regions grow with the shape (the split region is sized for the most
+  // splits), so a workspace sized for one call serves any smaller one
   w.part_off = 0;
-  w.frag_off = align256(nb * w.n_splits * w.max_qv * sizeof(float));
-  // Q in MFMA B-fragment order: per (request, head, 32-vector item, 16-wide k
-  // step), the 64 lanes' 16-byte slices back to back
-  w.total = w.frag_off + nb * (size_t)w.n_qt * 4 * (s.d / 16) * 64 * 16;
+  w.col_off = align256(nb * kMaxSplits * w.max_qv * sizeof(float));
+  w.total = w.col_off + align256(nb * (size_t)w.n_qt * s.max_ctx_len * sizeof(float));
   return w;
 }
 
@@ -73,253 +80,191 @@ __device__ __forceinline__ float2 combine_ml(float2 a, float2 b) {
   return make_float2(m, a.y * exp2f(a.x - m) + b.y * exp2f(b.x - m));
 }
 
-// ---------------------------------------------------------------- bf16 stats
-template <int D>
-__global__ __launch_bounds__(kThreads) void probe_stats_bf16(
-    float* __restrict__ part, uint16_t* __restrict__ qfrag, const uint16_t* __restrict__ q,
-    int64_t n_q_rows,
-    const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
+// ---------------------------------------------------------------- bf16 passes
+template <int D, bool kCols>
+__global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
+    float* __restrict__ part, float* __restrict__ colp, const uint16_t* __restrict__ q,
+    int64_t n_q_rows, const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
-    const int32_t* __restrict__ ctx_len, int hq, int hkv, int lg, int n_splits, int n_sub,
-    int max_qv, float scale2) {
-  constexpr int KSTR = D + 8;
-  constexpr int CPR = D / 8;                        // 16-byte chunks per K row
-  constexpr int PER = kSubKeys * CPR / kThreads;    // chunks per thread per sub-tile
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kSubKeys * KSTR];
+    const int32_t* __restrict__ ctx_len, int hq, int hkv, int lg, int n_qt, int n_splits,
+    int split_keys, int max_qv, int max_ctx, float scale2) {
+  constexpr int KSTR = D + 8;                          // padded LDS row (conflict-free reads)
+  constexpr int CPR = D / 8;                           // 16-byte pieces per K row
+  constexpr int PER = kChunkKeys * CPR / (kW * 64);    // pieces per thread per chunk
+  constexpr int SPL = kMaxSplits / 2;                  // splits per lane in the merge
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kChunkKeys * KSTR];
+  __shared__ float lse_l[kCols ? kQvTile : 1];
+  __shared__ float red[kCols ? kW : 1][kCols ? kChunkKeys : 1];
 
-  const int tile = blockIdx.x;
-  const int g = blockIdx.y % hkv, split = blockIdx.y / hkv, b = blockIdx.z;
+  // block -> (KV head, query tile, split, request) with the head fastest:
+  // blocks are dealt to the XCDs in turn, so with 8 KV heads every block of a
+  // head runs on one XCD and its Q and split statistics are shared in that L2
+  const int g = blockIdx.x % hkv;
+  const int rest = blockIdx.x / hkv;
+  const int qt = rest % n_qt, split = (rest / n_qt) % n_splits, b = rest / (n_qt * n_splits);
   const int64_t q0 = cu_q[b];
   const int nqv = min((cu_q[b + 1] - (int)q0) << lg, max_qv);
-  if (tile * kQvPerBlock >= nqv) return;
+  if (qt * kQvTile >= nqv) return;
   const int64_t k0 = cu_kv[b];
   const int N = ctx_len[b];
-  const int key_lo = split * n_sub * kSubKeys;
-  const int key_hi = min(N, key_lo + n_sub * kSubKeys);
-  const int n_here = key_hi > key_lo ? (key_hi - key_lo + kSubKeys - 1) / kSubKeys : 0;
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
-  const int qv = tile * kQvPerBlock + 32 * w + lq;
+  const int key_lo = split * split_keys;
+  const int key_hi = min(N, key_lo + split_keys);
+  if (kCols && key_lo >= key_hi) return;  // no keys: no columns (an empty split's statistics are still written)
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
+  const int qv = qt * kQvTile + 32 * w + lq;
   const int64_t qrow = q0 + (qv >> lg);
   const bool valid = qv < nqv && qrow < n_q_rows;
   const int head = g * (1 << lg) + (qv & ((1 << lg) - 1));
 
+  // Every load below is unconditional, its indices clamped to real rows: a
+  // load under a lane condition gets a wait of its own, which serialises the
+  // round trips.  Keys past the split and query vectors past the tile are
+  // masked where their products are used, so the rows read for them only
+  // have to be finite.
   uint4 buf[PER];
-  auto fetch = [&](int sub) {
+  auto fetch = [&](int c0) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * kThreads;
-      const int key = key_lo + sub * kSubKeys + c / CPR, ch = c % CPR;
-      const int64_t row = k0 + key;
-      buf[i] = (key < key_hi && row < n_kv_rows) ? ld16(k + row * k_stride + (int64_t)g * D + ch * 8)
-                                                 : make_uint4(0, 0, 0, 0);
+      const int c = threadIdx.x + i * kW * 64;
+      const int key = min(c0 + c / CPR, key_hi - 1), ch = c % CPR;
+      const int64_t row = min(k0 + key, n_kv_rows - 1);
+      buf[i] = ld16(k + row * k_stride + (int64_t)g * D + ch * 8);
     }
   };
-  if (n_here > 0) fetch(0);
+  if (key_lo < key_hi) fetch(key_lo);
   bf16x8 qreg[D / 16];
   {
-    const uint16_t* qp = q + qrow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
+    const uint16_t* qp = q + min(qrow, n_q_rows - 1) * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st)
-      qreg[st] = as_bf16x8(valid ? ld16(qp + 16 * st) : make_uint4(0, 0, 0, 0));
+    for (int st = 0; st < D / 16; ++st) qreg[st] = as_bf16x8(ld16(qp + 16 * st));
   }
-  if (split == 0) {  // one block per (tile, head, request) stores the fragments
-    const int item = tile * 4 + w;
-    uint16_t* fp = qfrag + ((((int64_t)(b * hkv + g) * gridDim.x * 4 + item) * (D / 16)) * 64 + l) * 8;
+  float lse_v[kCols ? 16 : 1];
+  if (kCols) {
+    // the vector's base-2 log-sum-exp over every split: lanes l (even splits)
+    // and l^32 (odd splits) fold theirs in split order, then even + odd; its
+    // padding rows get a reference that sends every exponential to 0
+    // (branch-free, so every load is issued before the first one is used;
+    // an empty split's -inf and a masked slot count as a floor with weight 0)
+    const float* pg = part + (int64_t)(b * hkv + g) * n_splits * max_qv + min(qv, max_qv - 1);
+    float x[SPL];
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st) st16(fp + st * 64 * 8, __builtin_bit_cast(uint4, qreg[st]));
+    for (int j = 0; j < SPL; ++j) x[j] = pg[min(2 * j + hi, n_splits - 1) * max_qv];
+    asm volatile("" ::: "memory");  // all of them in flight before the first is used
+    constexpr float kFloor = -1e30f;
+    float mx = kFloor, ls = 0.f;
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) {
+      const bool ok = valid && 2 * j + hi < n_splits && x[j] > kFloor;
+      const float xj = ok ? x[j] : kFloor;
+      const float mn = fmaxf(mx, xj);
+      ls = ls * __builtin_amdgcn_exp2f(mx - mn) + (ok ? __builtin_amdgcn_exp2f(xj - mn) : 0.f);
+      mx = mn;
+    }
+    if (ls == 0.f) mx = -INFINITY;
+    const float2 mine = make_float2(mx, ls);
+    const float2 other = make_float2(__shfl_xor(mx, 32, 64), __shfl_xor(ls, 32, 64));
+    const float2 ml = hi == 0 ? combine_ml(mine, other) : combine_ml(other, mine);
+    if (hi == 0) lse_l[32 * w + lq] = (valid && ml.y > 0.f) ? ml.x + __builtin_amdgcn_logf(ml.y) : 1e30f;
+    __syncthreads();
+    // S layout: value v of a lane belongs to query vector 8(v>>2)+4hi+(v&3) of the wave
+#pragma unroll
+    for (int v = 0; v < 16; ++v) lse_v[v] = lse_l[32 * w + 8 * (v >> 2) + 4 * hi + (v & 3)];
   }
   float m = -INFINITY, ls = 0.f;
-  for (int sub = 0; sub < n_here; ++sub) {
-    if (sub > 0) __syncthreads();  // the previous sub-tile is no longer read
+  for (int c0 = key_lo; c0 < key_hi; c0 += kChunkKeys) {
+    if (c0 > key_lo) __syncthreads();  // the previous chunk (and its sums) are no longer read
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * kThreads;
+      const int c = threadIdx.x + i * kW * 64;
       st16(&k_lds[(c / CPR) * KSTR + (c % CPR) * 8], buf[i]);
     }
     __syncthreads();
-    if (sub + 1 < n_here) fetch(sub + 1);  // in flight during this sub-tile's work
-    // two halves of 64 keys, each folded into the running (max, sum); logits are
-    // scaled into the log2 domain, masked only in the split's last sub-tile
-    const bool tail = key_lo + (sub + 1) * kSubKeys > key_hi;
+    if (c0 + kChunkKeys < key_hi) fetch(c0 + kChunkKeys);  // in flight during this chunk's work
+    const int n_keys = min(key_hi - c0, kChunkKeys);
+    const int n_grp = (n_keys + 31) / 32;
+    for (int kg = 0; kg < n_grp; ++kg) {
+      bf16x8 a[D / 16];
 #pragma unroll
-    for (int half = 0; half < kSubKeys / 64; ++half) {
-      const int kt0 = key_lo + sub * kSubKeys + half * 64;
-      f32x16 sacc[2];
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        sacc[blk] = f32x16{};
-#pragma unroll
-        for (int st = 0; st < D / 16; ++st) {
-          const bf16x8 a =
-              as_bf16x8(ld16(&k_lds[(half * 64 + blk * 32 + lq) * KSTR + 8 * hi + 16 * st]));
-          sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[st], sacc[blk], 0, 0, 0);
-        }
-      }
-      if (tail) {
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            if (kt0 + blk * 32 + 8 * (v >> 2) + 4 * hi + (v & 3) >= key_hi) sacc[blk][v] = -INFINITY;
-      }
-      float mt = -INFINITY;
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[blk][v]);
-      const float mn = fmaxf(m, mt * scale2);
-      if (mn != -INFINITY) {
-        float acc = 0.f;
-#pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc += __builtin_amdgcn_exp2f(fmaf(sacc[blk][v], scale2, -mn));
-        ls = ls * __builtin_amdgcn_exp2f(m - mn) + acc;
-        m = mn;
-      }
-    }
-  }
-  // lanes l and l^32 hold disjoint keys of the same query vector; the split's
-  // base-2 log-sum-exp log2(sum_t 2^(logit_t)) = max + log2(sum) (-inf: no keys)
-  const float2 ml = combine_ml(make_float2(m, ls), make_float2(__shfl_xor(m, 32, 64), __shfl_xor(ls, 32, 64)));
-  if (valid && hi == 0)
-    part[((int64_t)(b * hkv + g) * n_splits + split) * max_qv + qv] =
-        ml.y > 0.f ? ml.x + __builtin_amdgcn_logf(ml.y) : -INFINITY;
-}
-
-// ---------------------------------------------------------------- bf16 columns
-constexpr int kColWaves = 8;
-
-// Operands of one (KV head, 32-query-vector) item of the column pass: the Q
-// slice (B operand) of the lane's query vector and its per-split log-sum-exps
-// (even splits in lanes 0-31, odd splits in lanes 32-63).
-template <int D>
-struct ColItem {
-  bf16x8 q[D / 16];
-  float p[kMaxSplits / 2];
-  bool live;
-};
-
-template <int D>
-__global__ __launch_bounds__(kColWaves * 64) void probe_cols_bf16(
-    float* __restrict__ scores, int accumulate, const float* __restrict__ part,
-    const uint16_t* __restrict__ qfrag, int n_items_max, int64_t n_q_rows,
-    const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
-    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
-    const int32_t* __restrict__ ctx_len, int hkv, int lg, int n_splits, int max_qv,
-    float scale2) {
-  __shared__ float red[kColWaves][kColKeys];
-  const int chunk = blockIdx.x, b = blockIdx.y;
-  const int N = ctx_len[b];
-  const int kc0 = chunk * kColKeys;
-  const int64_t k0 = cu_kv[b];
-  if (kc0 >= N || k0 + kc0 >= n_kv_rows) return;
-  const int64_t q0 = cu_q[b];
-  // query vectors whose rows exist (the rest of a 32-wide item is padding)
-  const int nqv = min(min((cu_q[b + 1] - (int)q0) << lg, max_qv), (int)max<int64_t>(0, n_q_rows - q0) << lg);
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lq = l & 31, hi = l >> 5;
-  const int nsub = (nqv + 31) >> 5;
-  // waves per KV head (heads beyond the waves are taken in turns), and this
-  // wave's share of the head's 32-query-vector items
-  const int wpg = hkv >= kColWaves ? 1 : kColWaves / hkv;
-  const int spw = (nsub + wpg - 1) / wpg;
-  const int part_w = w % wpg;
-  const int s0 = part_w * spw, s1 = min(nsub, s0 + spw);
-  // keys past the context (or the tensor) read the last real row; their sums are dropped
-  const int64_t krow = min(k0 + min(kc0 + lq, N - 1), n_kv_rows - 1);
-
-  float col[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) col[v] = 0.f;
-
-  if (w < hkv * wpg && s0 < s1) {
-    for (int g = w / wpg; g < hkv; g += kColWaves / wpg) {
-      bf16x8 kreg[D / 16];
-      {
-        const uint16_t* kp = k + krow * k_stride + (int64_t)g * D + 8 * hi;
-#pragma unroll
-        for (int st = 0; st < D / 16; ++st) kreg[st] = as_bf16x8(ld16(kp + 16 * st));
-      }
-      const float* pg = part + ((int64_t)(b * hkv + g) * n_splits) * max_qv;
-      const uint16_t* fg = qfrag + (int64_t)(b * hkv + g) * n_items_max * (D / 16) * 64 * 8 + l * 8;
-      // every load below is unconditional (indices clamped), so the hardware's
-      // in-order load counter lets two items stay in flight while one is used
-      auto load_item = [&](int sub, ColItem<D>& c) {
-        const int qv_raw = sub * 32 + lq;
-        c.live = sub < s1 && qv_raw < nqv;
-        const int qv = min(qv_raw, nqv - 1);
-        const uint16_t* fp = fg + (int64_t)min(sub, nsub - 1) * (D / 16) * 64 * 8;
-#pragma unroll
-        for (int st = 0; st < D / 16; ++st) c.q[st] = as_bf16x8(ld16(fp + st * 64 * 8));
-#pragma unroll
-        for (int j = 0; j < kMaxSplits / 2; ++j)
-          c.p[j] = pg[(int64_t)min(2 * j + hi, n_splits - 1) * max_qv + qv];
-      };
-      auto use_item = [&](const ColItem<D>& c) {
-        // the query vector's log-sum-exp over all keys from the splits', in a
-        // fixed order: global max, then the even and odd splits' sums (lanes
-        // 0-31 / 32-63), even + odd; copies past the last split are masked
-        float pv[kMaxSplits / 2];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < kMaxSplits / 2; ++j) {
-          pv[j] = 2 * j + hi < n_splits ? c.p[j] : -INFINITY;
-          mx = fmaxf(mx, pv[j]);
-        }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        float ls = 0.f;
-        if (mx != -INFINITY) {
-#pragma unroll
-          for (int j = 0; j < kMaxSplits / 2; ++j) ls += __builtin_amdgcn_exp2f(pv[j] - mx);
-        }
-        const float lo = __shfl_xor(ls, 32, 64);
-        const float lsum = hi == 0 ? ls + lo : lo + ls;
-        // padding (and a request without keys) get a reference that sends every
-        // exponential to 0
-        const float lse = (c.live && lsum > 0.f) ? mx + __builtin_amdgcn_logf(lsum) : 1e30f;
-        f32x16 sacc = f32x16{};
+      for (int st = 0; st < D / 16; ++st) a[st] = as_bf16x8(ld16(&k_lds[(kg * 32 + lq) * KSTR + 8 * hi + 16 * st]));
+      const int kt0 = c0 + kg * 32;
+      f32x16 sacc = f32x16{};
+      if (!kCols) {
+        // S^T: value v of this lane is key 8(v>>2)+4hi+(v&3) of the group for the
+        // lane's query vector; logits go to the log2 domain, keys past the split
+        // are masked
 #pragma unroll
         for (int st = 0; st < D / 16; ++st)
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kreg[st], c.q[st], sacc, 0, 0, 0);
-        // S^T layout: value v of this lane is key 8(v>>2)+4hi+(v&3) of query vector
-        // lq, whose log-sum-exp this lane holds: probability = 2^(logit - lse)
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[st], qreg[st], sacc, 0, 0, 0);
+        if (kt0 + 32 > key_hi) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) col[v] += __builtin_amdgcn_exp2f(fmaf(sacc[v], scale2, -lse));
-      };
-      ColItem<D> ca, cb, cc;
-      load_item(s0, ca);
-      load_item(s0 + 1, cb);
-      for (int sub = s0; sub < s1; sub += 3) {
-        load_item(sub + 2, cc);
-        use_item(ca);
-        load_item(sub + 3, ca);
-        if (sub + 1 < s1) use_item(cb);
-        load_item(sub + 4, cb);
-        if (sub + 2 < s1) use_item(cc);
+          for (int v = 0; v < 16; ++v)
+            if (kt0 + 8 * (v >> 2) + 4 * hi + (v & 3) >= key_hi) sacc[v] = -INFINITY;
+        }
+        float mt = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[v]);
+        const float mn = fmaxf(m, mt * scale2);
+        if (mn != -INFINITY) {
+          float acc = 0.f;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc += __builtin_amdgcn_exp2f(fmaf(sacc[v], scale2, -mn));
+          ls = ls * __builtin_amdgcn_exp2f(m - mn) + acc;
+          m = mn;
+        }
+      } else {
+        // S: this lane's key kt0 + lq, value v for query vector 8(v>>2)+4hi+(v&3)
+#pragma unroll
+        for (int st = 0; st < D / 16; ++st)
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qreg[st], a[st], sacc, 0, 0, 0);
+        float cs = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) cs += __builtin_amdgcn_exp2f(fmaf(sacc[v], scale2, -lse_v[v]));
+        const float cs_other = __shfl_xor(cs, 32, 64);
+        if (hi == 0) red[w][kg * 32 + lq] = kt0 + lq < key_hi ? cs + cs_other : 0.f;
+      }
+    }
+    if (kCols) {
+      __syncthreads();
+      if (threadIdx.x < n_keys) {
+        float acc = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < kW; ++ww) acc += red[ww][threadIdx.x];
+        colp[((int64_t)(b * hkv + g) * n_qt + qt) * max_ctx + c0 + threadIdx.x] = acc;
       }
     }
   }
-  // per-key sums over the wave's 32 query-vector columns (lanes with the same hi)
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) col[v] += __shfl_xor(col[v], o, 64);
+  if (!kCols) {
+    // lanes l and l^32 hold disjoint keys of the same query vector; the split's
+    // base-2 log-sum-exp log2(sum_t 2^(logit_t)) = max + log2(sum) (-inf: no keys)
+    const float2 ml = combine_ml(make_float2(m, ls), make_float2(__shfl_xor(m, 32, 64), __shfl_xor(ls, 32, 64)));
+    if (valid && hi == 0)
+      part[((int64_t)(b * hkv + g) * n_splits + split) * max_qv + qv] =
+          ml.y > 0.f ? ml.x + __builtin_amdgcn_logf(ml.y) : -INFINITY;
   }
-  if (lq == 0) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) red[w][8 * (v >> 2) + 4 * hi + (v & 3)] = col[v];
-  }
-  __syncthreads();
-  if (threadIdx.x < kColKeys) {
-    const int t = kc0 + threadIdx.x;
-    const int64_t row = k0 + t;
-    if (t < N && row < n_kv_rows) {
-      float acc = 0.f;
-#pragma unroll
-      for (int ww = 0; ww < kColWaves; ++ww) acc += red[ww][threadIdx.x];
-      scores[row] = accumulate ? scores[row] + acc : acc;
-    }
-  }
+}
+
+// ---------------------------------------------------------------- bf16 final
+// scores[t] (+)= the column sums of every (KV head, query tile) of the request
+// that has query vectors, head-major
+__global__ __launch_bounds__(kThreads) void scores_final(float* __restrict__ scores, int accumulate,
+                                                         const float* __restrict__ colp,
+                                                         const int32_t* __restrict__ cu_q,
+                                                         const int32_t* __restrict__ cu_kv,
+                                                         const int32_t* __restrict__ ctx_len,
+                                                         int64_t n_kv_rows, int hkv, int lg,
+                                                         int n_qt, int max_qv, int max_ctx) {
+  const int t = blockIdx.x * kThreads + threadIdx.x, b = blockIdx.y;
+  if (t >= ctx_len[b]) return;
+  const int64_t row = cu_kv[b] + t;
+  if (row >= n_kv_rows) return;
+  const int nqv = min((cu_q[b + 1] - cu_q[b]) << lg, max_qv);
+  const int nt = (nqv + kQvTile - 1) / kQvTile;
+  const float* cp = colp + (int64_t)b * hkv * n_qt * max_ctx + t;
+  float acc = 0.f;
+  for (int g = 0; g < hkv; ++g)
+    for (int j = 0; j < nt; ++j) acc += cp[((int64_t)g * n_qt + j) * max_ctx];
+  scores[row] = accumulate ? scores[row] + acc : acc;
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -440,28 +385,34 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
     return hipGetLastError();
   }
   const WsLayout w = ws_layout(s);
-  if ((int64_t)s.hkv * w.n_splits > 65535) return hipErrorInvalidConfiguration;
-  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + w.part_off);
-  uint16_t* qfrag = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + w.frag_off);
+  if (s.batch > 65535) return hipErrorInvalidConfiguration;
+  char* wb = static_cast<char*>(ws);
+  float* part = reinterpret_cast<float*>(wb + w.part_off);
+  float* colp = reinterpret_cast<float*>(wb + w.col_off);
   const uint16_t* qb = static_cast<const uint16_t*>(q);
   const uint16_t* kb = static_cast<const uint16_t*>(k);
-  if (w.max_qv > 0) {
-    dim3 ga(w.n_qt, s.hkv * w.n_splits, s.batch);
-#define QCF_STATS(D)                                                                             \
-  probe_stats_bf16<D><<<ga, kThreads, 0, stream>>>(part, qfrag, qb, n_q_rows, kb, n_kv_rows,     \
-                                                   k_row_stride, cu_q, cu_kv, ctx_len, s.hq,     \
-                                                   s.hkv, lg, w.n_splits, w.n_sub, w.max_qv, scale2)
-    if (s.d == 64) QCF_STATS(64); else QCF_STATS(128);
-#undef QCF_STATS
+  if (w.max_qv > 0 && n_q_rows > 0 && n_kv_rows > 0) {
+    const int64_t nblk = (int64_t)s.hkv * w.n_qt * w.n_splits * s.batch;
+    if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)nblk);
+#define QCF_PASS(D, C)                                                                             \
+  scores_pass_bf16<D, C><<<grid, kW * 64, 0, stream>>>(part, colp, qb, n_q_rows, kb, n_kv_rows,   \
+                                                       k_row_stride, cu_q, cu_kv, ctx_len, s.hq, \
+                                                       s.hkv, lg, w.n_qt, w.n_splits,            \
+                                                       w.split_keys, w.max_qv, s.max_ctx_len,    \
+                                                       scale2)
+    if (s.d == 64) {
+      QCF_PASS(64, false);
+      QCF_PASS(64, true);
+    } else {
+      QCF_PASS(128, false);
+      QCF_PASS(128, true);
+    }
+#undef QCF_PASS
   }
-  dim3 gc((s.max_ctx_len + kColKeys - 1) / kColKeys, s.batch);
-#define QCF_COLS(D)                                                                             \
-  probe_cols_bf16<D><<<gc, kColWaves * 64, 0, stream>>>(scores, accumulate, part, qfrag,       \
-                                                  w.n_qt * 4, n_q_rows, kb, n_kv_rows,           \
-                                                  k_row_stride, cu_q, cu_kv, ctx_len, s.hkv, lg,  \
-                                                  w.n_splits, w.max_qv, scale2)
-  if (s.d == 64) QCF_COLS(64); else QCF_COLS(128);
-#undef QCF_COLS
+  scores_final<<<dim3((s.max_ctx_len + kThreads - 1) / kThreads, s.batch), kThreads, 0, stream>>>(
+      scores, accumulate, colp, cu_q, cu_kv, ctx_len, n_kv_rows, s.hkv, lg, std::max(1, w.n_qt),
+      w.max_qv, s.max_ctx_len);
   return hipGetLastError();
 }
 

@@ -866,13 +866,40 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
   const int nr = cu_rows[b + 1] - (int)r0;
   const int rbase = tile * rpb;
   const int qv0 = quarter * QQ;
+  // Every load of the first kMR partials (their O pieces and, for the first
+  // QQ threads, their (max, sum)) is issued before any is used, from clamped
+  // slots; later partials (rare) follow one at a time.
+  constexpr int kPass = kThreads * 8;
+  constexpr int NP = QQ * D / kPass;
+  constexpr int kMR = 4;
+  uint4 ob[kMR][NP];
+#pragma unroll
+  for (int sp = 0; sp < kMR; ++sp) {
+    const uint16_t* pp = part_o + (slot_l[min(sp, nsp - 1)] * QV + qv0) * D;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) ob[sp][p] = ld16(pp + p * kPass + 8 * threadIdx.x);
+  }
   if (threadIdx.x < QQ) {
     const int qv = qv0 + threadIdx.x;
+    float2 mlr[kMR];
+#pragma unroll
+    for (int sp = 0; sp < kMR; ++sp) mlr[sp] = part_ml[slot_l[min(sp, nsp - 1)] * QV + qv];
     float mx = -1e30f;
-    for (int sp = 0; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[slot_l[sp] * QV + qv].x);
-    // split sp's weight on its normalised partial: sum_sp 2^(m_sp - max) / total
+#pragma unroll
+    for (int sp = 0; sp < kMR; ++sp)
+      if (sp < nsp) mx = fmaxf(mx, mlr[sp].x);
+    for (int sp = kMR; sp < nsp; ++sp) mx = fmaxf(mx, part_ml[slot_l[sp] * QV + qv].x);
+    // split sp's weight on its normalised partial: 2^(m_sp - max) * l_sp / total
     float lsum = 0.f;
-    for (int sp = 0; sp < nsp; ++sp) {
+#pragma unroll
+    for (int sp = 0; sp < kMR; ++sp) {
+      if (sp < nsp) {
+        const float wsp = __builtin_amdgcn_exp2f(mlr[sp].x - mx) * mlr[sp].y;
+        wgt[sp][threadIdx.x] = wsp;
+        lsum += wsp;
+      }
+    }
+    for (int sp = kMR; sp < nsp; ++sp) {
       const float2 ml = part_ml[slot_l[sp] * QV + qv];
       const float wsp = __builtin_amdgcn_exp2f(ml.x - mx) * ml.y;
       if (sp < WS) wgt[sp][threadIdx.x] = wsp;
@@ -888,16 +915,13 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
       lse[grow * hq + g * G + (qv & (G - 1))] = lsum > 0.f ? (mx + log2f(lsum)) * kLn2 : -INFINITY;
   }
   __syncthreads();
-  // QQ x D outputs, 8 consecutive ones per thread and pass, all passes in flight
-  constexpr int kPass = kThreads * 8;
-  constexpr int NP = QQ * D / kPass;
+  // QQ x D outputs, 8 consecutive ones per thread and pass; partials combined in order
   float acc[NP][8];
 #pragma unroll
   for (int p = 0; p < NP; ++p)
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[p][k] = 0.f;
-  for (int sp = 0; sp < nsp; ++sp) {
-    const uint16_t* pp = part_o + (slot_l[sp] * QV + qv0) * D;
+  auto add_partial = [&](int sp, const uint4* o) {
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       const int e = p * kPass + 8 * threadIdx.x;
@@ -910,10 +934,20 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
         wv = __builtin_amdgcn_exp2f(ml.x - mxq[ql]) * ml.y * invq[ql];
       }
       float x[8];
-      Vec16<uint16_t>::unpack(ld16(pp + e), x);
+      Vec16<uint16_t>::unpack(o[p], x);
 #pragma unroll
       for (int k = 0; k < 8; ++k) acc[p][k] += wv * x[k];
     }
+  };
+#pragma unroll
+  for (int sp = 0; sp < kMR; ++sp)
+    if (sp < nsp) add_partial(sp, ob[sp]);
+  for (int sp = kMR; sp < nsp; ++sp) {
+    uint4 o[NP];
+    const uint16_t* pp = part_o + (slot_l[sp] * QV + qv0) * D;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) o[p] = ld16(pp + p * kPass + 8 * threadIdx.x);
+    add_partial(sp, o);
   }
 #pragma unroll
   for (int p = 0; p < NP; ++p) {

@@ -1,0 +1,186 @@
+"""QCFuse over a multi-layer attention stack on the GPU (the c3 configuration).
+
+The hot-path steps of every layer run in libqcf (re-positioning, the probe
+buffer and query-row rotation, probe attention, critical-layer scores, the
+per-chunk top-k, the fresh-row scatter and the recomputed-row attention).  The
+stack's own glue -- RMSNorm, the Wq/Wk/Wv/Wo projections and the residual --
+is plain torch (library GEMMs); it only produces each layer's inputs.
+
+Flow (Section 3.5 with the critical-layer selector of Section 3.4.2):
+  offline  each chunk runs through the stack alone at positions 0..n_i-1 and
+           its per-layer K/V becomes the chunk's PIC cache (all chunks of a
+           layer as one batch of independent sequences);
+  probe    layers 0..max(L*): qcf_assemble re-positions the layer's chunks
+           into the request cache, rotates the query rows' fresh q/k at
+           N + i and fills the probe buffer [anchors ; query]; the query rows
+           attend over it; at a critical layer qcf_probe_scores adds the
+           layer's importance to the scores;
+  select   one qcf_select_topk -> P; R = [P ; query rows] per request;
+  recompute every layer: re-position (layers past the probe), scatter R's
+           fresh K/V (q rotated alongside), attend R over the fused cache.
+No device-to-host synchronisation happens inside ``run()``.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from . import qcf
+from .step import FusionPlan, kv_buffer
+
+__all__ = ["FusionStack"]
+
+
+class FusionStack:
+    def __init__(self, sw, rho_bp: int | None = None, device="cuda"):
+        self.sw = sw
+        self.rho_bp = sw.rho_bp if rho_bp is None else int(rho_bp)
+        self.plan = p = FusionPlan.build(sw, self.rho_bp)
+        dt = torch.bfloat16 if sw.dtype == "bf16" else torch.float32
+        self.dtype = dt
+        dev = torch.device(device)
+        self.device = dev
+        T, hq, hkv, d, L = sw.n_rows, sw.n_q_heads, sw.n_kv_heads, sw.head_dim, sw.n_layers
+        self.scale = 1.0 / math.sqrt(d)
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        f = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+        self.embed = f(sw.embed)
+        self.wq, self.wk, self.wv, self.wo = f(sw.wq), f(sw.wk), f(sw.wv), f(sw.wo)
+        # layout
+        self.seg_start, self.seg_len, self.seg_delta = t(sw.seg_start), t(sw.seg_len), t(sw.seg_delta)
+        self.seg_k, self.out_start, self.pos_base = t(p.seg_k), t(p.out_start), t(p.pos_base)
+        self.cu_kv, self.ctx_len, self.cu_q = t(sw.cu_kv), t(sw.ctx_len), t(sw.cu_q)
+        self.cu_R, self.cu_probe = t(p.cu_R), t(p.cu_probe)
+        self.u_idx, self.u_pos = t(p.u_idx), t(p.u_pos)
+        self.probe_pos, self.probe_src = t(p.probe_pos), t(p.probe_src)
+        self.probe_delta, self.query_slot = t(p.probe_delta), t(p.query_slot)
+        self.R_idx_init, self.R_pos_init = t(p.R_idx_init), t(p.R_pos_init)
+        self.u_src = t(np.arange(p.u_idx.size, dtype=np.int32))
+        # offline PIC layout: every chunk a sequence of its own, keys at rows seg_start..
+        self.ctx_rows = t(np.concatenate([np.arange(a, a + n) for a, n in zip(sw.seg_start, sw.seg_len)])
+                          .astype(np.int32) if sw.n_chunks else np.zeros(0, np.int32))
+        self.ctx_local = t(np.concatenate([np.arange(n) for n in sw.seg_len]).astype(np.int32)
+                           if sw.n_chunks else np.zeros(0, np.int32))
+        self.cu_chunk_rows = t(np.concatenate([[0], np.cumsum(sw.seg_len)]).astype(np.int32))
+        self.cu_chunk_kv = t(np.concatenate([sw.seg_start, [T]]).astype(np.int32))
+        self.max_chunk_kv = int(np.diff(np.concatenate([sw.seg_start, [T]])).max()) if sw.n_chunks else 1
+        # caches: PIC and the per-layer request caches (padded rows, see kv_buffer)
+        self.k_pic = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+        self.v_pic = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+        self.k_req = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+        self.v_req = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+        nU, nR, nP = p.u_idx.size, p.R_idx_init.size, p.probe_idx.size
+        self.k_probe = kv_buffer(nP, hkv, d, dt, dev)
+        self.v_probe = kv_buffer(nP, hkv, d, dt, dev)
+        self.q_u = torch.empty((nU, hq, d), dtype=dt, device=dev)
+        self.o_probe = torch.empty((nU, hq, d), dtype=dt, device=dev)
+        self.scores = torch.zeros(T, dtype=torch.float32, device=dev)
+        self.R_idx = self.R_idx_init.clone()
+        self.R_pos = self.R_pos_init.clone()
+        self.q_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
+        self.o_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
+        self.max_kv = int(np.diff(sw.cu_kv).max()) if sw.batch else 1
+        nws = qcf.qcf_probe_scores_workspace_size(sw.batch, p.max_q, p.max_ctx, hq, hkv, d)
+        self.ws_scores = torch.empty(max(nws, 256), dtype=torch.uint8, device=dev)
+        wa = lambda b, r, kv: qcf.qcf_sparse_prefill_attn_workspace_size(b, r, max(kv, 1), hq, hkv, d, dt)
+        self.ws_attn = torch.empty(max(wa(sw.batch, p.max_R, self.max_kv),
+                                       wa(sw.n_chunks, int(sw.seg_len.max()) if sw.n_chunks else 1,
+                                          self.max_chunk_kv),
+                                       wa(sw.batch, p.max_q, p.max_probe), 256),
+                                   dtype=torch.uint8, device=dev)
+        self.pic_built = False
+
+    # -- glue: RMSNorm, projections, residual (torch) ---------------------------
+    def _qkv(self, l, h):
+        sw = self.sw
+        n = h.shape[0]
+        hf = h.float()
+        x = (hf * torch.rsqrt((hf * hf).mean(-1, keepdim=True) + sw.rms_eps)).to(self.dtype)
+        q = (x @ self.wq[l]).view(n, sw.n_q_heads, sw.head_dim)
+        k = (x @ self.wk[l]).view(n, sw.n_kv_heads, sw.head_dim)
+        v = (x @ self.wv[l]).view(n, sw.n_kv_heads, sw.head_dim)
+        return q.contiguous(), k.contiguous(), v.contiguous()
+
+    def _residual(self, l, h, o):
+        return h + (o.reshape(o.shape[0], -1) @ self.wo[l])
+
+    # -- offline: PIC caches --------------------------------------------------
+    def build_pic(self):
+        """Each chunk alone through the stack at positions 0..n_i-1 (all chunks as one batch)."""
+        sw = self.sw
+        n = int(self.ctx_rows.numel())
+        h = self.embed.index_select(0, self.ctx_rows.long())
+        q_rot = torch.empty((n, sw.n_q_heads, sw.head_dim), dtype=self.dtype, device=self.device)
+        o = torch.empty_like(q_rot)
+        for l in range(sw.n_layers):
+            q, k, v = self._qkv(l, h)
+            qcf.qcf_scatter_kv(self.k_pic[l], self.v_pic[l], k, v, self.ctx_rows, self.ctx_local,
+                               sw.rope_theta, q_new=q, q_out=q_rot)
+            qcf.qcf_sparse_prefill_attn(o, q_rot, self.ctx_local, self.cu_chunk_rows, self.k_pic[l],
+                                        self.v_pic[l], self.cu_chunk_kv,
+                                        int(sw.seg_len.max()), self.max_chunk_kv, self.scale,
+                                        workspace=self.ws_attn)
+            h = self._residual(l, h, o)
+        self.pic_built = True
+
+    # -- online ---------------------------------------------------------------
+    def run(self):
+        sw, p = self.sw, self.plan
+        if not self.pic_built:
+            self.build_pic()
+        L = sw.n_layers
+        lmax = max(sw.critical_layers)
+        # query probe over [anchor cache ; query] up to the last critical layer
+        hU = self.embed.index_select(0, self.u_idx.long())
+        first = True
+        for l in range(lmax + 1):
+            q, k, v = self._qkv(l, hU)
+            qcf.qcf_assemble(self.k_req[l], self.v_req[l], self.k_pic[l], self.v_pic[l], self.seg_start,
+                             self.seg_len, self.seg_delta, p.max_seg, q, k, v, self.u_idx, self.u_pos,
+                             self.q_u, self.k_probe, self.v_probe, self.probe_src, self.probe_delta,
+                             sw.rope_theta, query_src=self.u_src, query_slot=self.query_slot)
+            qcf.qcf_sparse_prefill_attn(self.o_probe, self.q_u, self.u_pos, self.cu_q, self.k_probe,
+                                        self.v_probe, self.cu_probe, p.max_q, p.max_probe, self.scale,
+                                        kv_pos=self.probe_pos, workspace=self.ws_attn)
+            if l in sw.critical_layers:
+                qcf.qcf_probe_scores(self.scores, self.q_u, self.k_req[l], self.cu_q, self.cu_kv,
+                                     self.ctx_len, p.max_q, p.max_ctx, self.scale,
+                                     accumulate=not first, workspace=self.ws_scores)
+                first = False
+            hU = self._residual(l, hU, self.o_probe)
+        self.h_probe = hU
+        # one selection for every layer
+        self.R_idx.copy_(self.R_idx_init)
+        self.R_pos.copy_(self.R_pos_init)
+        qcf.qcf_select_topk(self.R_idx, self.scores, self.seg_start, self.seg_len, self.seg_k,
+                            self.out_start, p.max_seg, out_pos=self.R_pos, pos_base=self.pos_base)
+        # recompute R through every layer over the fused caches
+        hR = self.embed.index_select(0, self.R_idx.long())
+        for l in range(L):
+            if l > lmax:
+                qcf.qcf_rerope(self.k_req[l], self.k_pic[l], self.seg_start, self.seg_len, self.seg_delta,
+                               p.max_seg, sw.rope_theta, v_out=self.v_req[l], v_in=self.v_pic[l])
+            q, k, v = self._qkv(l, hR)
+            qcf.qcf_scatter_kv(self.k_req[l], self.v_req[l], k, v, self.R_idx, self.R_pos, sw.rope_theta,
+                               q_new=q, q_out=self.q_R)
+            qcf.qcf_sparse_prefill_attn(self.o_R, self.q_R, self.R_pos, self.cu_R, self.k_req[l],
+                                        self.v_req[l], self.cu_kv, p.max_R, self.max_kv, self.scale,
+                                        workspace=self.ws_attn)
+            hR = self._residual(l, hR, self.o_R)
+        self.h_R = hR
+
+    def results(self):
+        torch.cuda.synchronize()
+        c = lambda x: x.float().cpu().numpy().astype(np.float64)
+        p = self.plan
+        R = self.R_idx.cpu().numpy()
+        hR = c(self.h_R)
+        hP = c(self.h_probe)
+        cq = self.sw.cu_q
+        return dict(scores=self.scores.double().cpu().numpy(), R=R, cu_R=p.cu_R,
+                    P=[R[p.cu_R[b]:p.cu_R[b] + p.n_P[b]] for b in range(self.sw.batch)],
+                    h_R=[hR[p.cu_R[b]:p.cu_R[b + 1]] for b in range(self.sw.batch)],
+                    h_probe=[hP[cq[b]:cq[b + 1]] for b in range(self.sw.batch)],
+                    k_fuse=[c(k) for k in self.k_req], v_fuse=[c(v) for v in self.v_req])

@@ -38,7 +38,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["CONFIGS", "Workload", "make_workload", "round_to_bf16", "config_names"]
+__all__ = ["CONFIGS", "Workload", "make_workload", "round_to_bf16", "config_names", "STACK_CONFIGS",
+           "StackWorkload", "make_stack_workload"]
 
 
 # ---------------------------------------------------------------------------
@@ -294,3 +295,132 @@ def make_workload(name: str, seed: int = 0, rho_bp: int | None = None,
         k_pic=k_pic, v_pic=v_pic, q_new=q_new, k_new=k_new, v_new=v_new,
         meta=dict(seed=seed, desc=cfg.get("desc", "")),
     )
+
+
+# ---------------------------------------------------------------------------
+# multi-layer stack (the c3 configuration)
+# ---------------------------------------------------------------------------
+# A stack of attention blocks (RMSNorm, Wq/Wk/Wv, rotary, causal GQA attention,
+# Wo, residual) with random weights.  The selector scores at the critical
+# layers and one selection drives the recomputation of every layer.  Weights
+# are N(0, sigma^2) with sigma = 0.02 * sqrt(4096 / d_model), so a reduced
+# shape keeps the logit statistics of the 4096-wide stack; embeddings are
+# N(0, 1).  Anchors are drawn uniformly inside each chunk.
+STACK_CONFIGS = {
+    "c3": dict(index=3, dtype="bf16", chunks=[512] * 20, n_q=64, n_layers=36, d_model=4096,
+               n_q_heads=32, n_kv_heads=8, head_dim=128, rope_theta=1.0e6, anchors=52,
+               critical_layers=(2, 12, 24), rho_bp=3000,
+               desc="Qwen3-8B-shaped 36-layer stack: 20x512 chunks + 64-token query, 32/8/128, "
+                    "critical layers 2, 12, 24"),
+    # the same structure at a size the float64 oracle runs in seconds
+    "c3_small": dict(index=31, dtype="f32", chunks=[96, 64, 80, 33], n_q=12, n_layers=6,
+                     d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64, rope_theta=1.0e6,
+                     anchors=6, critical_layers=(1, 3), rho_bp=3000,
+                     desc="reduced c3-shaped stack: 6 layers, 4 chunks, 12-token query, 4/2/64"),
+}
+
+
+@dataclass
+class StackWorkload:
+    """Inputs of a multi-layer request batch (host arrays, float32 values exact in dtype)."""
+
+    name: str
+    dtype: str
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    rope_theta: float
+    rho_bp: int
+    critical_layers: tuple
+    rms_eps: float
+    chunk_lens: list
+    q_lens: list
+    cu_kv: np.ndarray
+    ctx_len: np.ndarray
+    cu_q: np.ndarray
+    seg_start: np.ndarray
+    seg_len: np.ndarray
+    seg_req: np.ndarray
+    seg_delta: np.ndarray
+    anchor_local: list
+    embed: np.ndarray        # [T, d_model] input hidden state of every token
+    wq: np.ndarray           # [L, d_model, H_q*d]
+    wk: np.ndarray           # [L, d_model, H_kv*d]
+    wv: np.ndarray           # [L, d_model, H_kv*d]
+    wo: np.ndarray           # [L, H_q*d, d_model]
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def batch(self) -> int:
+        return len(self.q_lens)
+
+    @property
+    def n_rows(self) -> int:
+        return int(self.cu_kv[-1])
+
+    @property
+    def n_chunks(self) -> int:
+        return int(self.seg_start.shape[0])
+
+
+def make_stack_workload(name: str = "c3", seed: int = 0, rho_bp: int | None = None,
+                        chunk_lens=None, q_lens=None, anchors_per_chunk: int | None = None,
+                        dtype: str | None = None, overrides: dict | None = None) -> StackWorkload:
+    """Draw a stack config's inputs.  Draw order (fixed): anchors, embeddings, then per
+    layer Wq, Wk, Wv, Wo."""
+    cfg = dict(STACK_CONFIGS[name])
+    if overrides:
+        cfg.update(overrides)
+    rng = np.random.default_rng([seed, cfg["index"]])
+    chunk_lens = [list(map(int, c)) for c in (chunk_lens or [cfg["chunks"]])]
+    q_lens_l = list(q_lens) if q_lens is not None else [int(cfg["n_q"])] * len(chunk_lens)
+    hq, hkv, d = int(cfg["n_q_heads"]), int(cfg["n_kv_heads"]), int(cfg["head_dim"])
+    dm, L = int(cfg["d_model"]), int(cfg["n_layers"])
+    dt = dtype or cfg["dtype"]
+    n_anchor = int(cfg["anchors"] if anchors_per_chunk is None else anchors_per_chunk)
+    B = len(q_lens_l)
+    ctx = np.array([sum(c) for c in chunk_lens], np.int64)
+    rows = ctx + np.array(q_lens_l, np.int64)
+    cu_kv = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    cu_q = np.concatenate([[0], np.cumsum(q_lens_l)]).astype(np.int32)
+    seg_start, seg_len, seg_req, seg_delta = [], [], [], []
+    for b in range(B):
+        off = 0
+        for n in chunk_lens[b]:
+            seg_start.append(int(cu_kv[b]) + off)
+            seg_len.append(n)
+            seg_req.append(b)
+            seg_delta.append(off)
+            off += n
+    seg_start, seg_len = np.array(seg_start, np.int32), np.array(seg_len, np.int32)
+    seg_req, seg_delta = np.array(seg_req, np.int32), np.array(seg_delta, np.int32)
+    anchor_local = []
+    for s in range(seg_start.size):
+        a = min(n_anchor, int(seg_len[s]))
+        anchor_local.append(np.sort(rng.choice(int(seg_len[s]), size=a, replace=False)).astype(np.int32))
+    T = int(cu_kv[-1])
+    sigma = np.float32(0.02 * np.sqrt(4096.0 / dm))
+    embed = rng.standard_normal((T, dm), dtype=np.float32)
+    wq = np.empty((L, dm, hq * d), np.float32)
+    wk = np.empty((L, dm, hkv * d), np.float32)
+    wv = np.empty((L, dm, hkv * d), np.float32)
+    wo = np.empty((L, hq * d, dm), np.float32)
+    if dt not in ("bf16", "f32"):
+        raise ValueError(dt)
+    rnd = round_to_bf16 if dt == "bf16" else (lambda x: x)
+    for l in range(L):   # rounded layer by layer (the full stack is several GB)
+        wq[l] = rnd(rng.standard_normal((dm, hq * d), dtype=np.float32) * sigma)
+        wk[l] = rnd(rng.standard_normal((dm, hkv * d), dtype=np.float32) * sigma)
+        wv[l] = rnd(rng.standard_normal((dm, hkv * d), dtype=np.float32) * sigma)
+        wo[l] = rnd(rng.standard_normal((hq * d, dm), dtype=np.float32) * sigma)
+    embed = rnd(embed)
+    return StackWorkload(
+        name=name, dtype=dt, n_layers=L, d_model=dm, n_q_heads=hq, n_kv_heads=hkv, head_dim=d,
+        rope_theta=float(cfg["rope_theta"]), rho_bp=int(cfg["rho_bp"] if rho_bp is None else rho_bp),
+        critical_layers=tuple(int(x) for x in cfg["critical_layers"]), rms_eps=1e-6,
+        chunk_lens=chunk_lens, q_lens=q_lens_l, cu_kv=cu_kv, ctx_len=ctx.astype(np.int32),
+        cu_q=cu_q, seg_start=seg_start, seg_len=seg_len, seg_req=seg_req, seg_delta=seg_delta,
+        anchor_local=anchor_local, embed=embed, wq=wq, wk=wk, wv=wv, wo=wo,
+        meta=dict(seed=seed, desc=cfg.get("desc", "")))

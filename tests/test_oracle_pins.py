@@ -336,3 +336,117 @@ def test_generator_is_deterministic_and_exact():
     assert c5.batch == 16 and 8 * 16 <= c5.n_chunks <= 16 * 16
     assert np.all((c5.seg_len >= 256) & (c5.seg_len <= 1024))
     assert all(16 <= n <= 128 for n in c5.q_lens)
+
+
+# ---------------------------------------------------------------- the multi-layer stack (c3)
+from oracle import stack as S  # noqa: E402
+from paper_2606_05875_amd.workloads import make_stack_workload  # noqa: E402
+
+
+def torch_forward(sw, rows, n_layers=None):
+    """Independent causal forward of rows (positions 0..n-1): torch float64, SDPA with
+    repeated KV heads, complex rotary.  Returns per-layer rotated q and k, v, final h."""
+    d, hq, hkv = sw.head_dim, sw.n_q_heads, sw.n_kv_heads
+    n = len(rows)
+    pos = np.arange(n)
+    h = torch.tensor(np.asarray(sw.embed[rows], np.float64))
+    qs, ks, vs = [], [], []
+    for l in range(sw.n_layers if n_layers is None else n_layers):
+        x = h / torch.sqrt((h * h).mean(-1, keepdim=True) + sw.rms_eps)
+        t = lambda w: x @ torch.tensor(np.asarray(w[l], np.float64))
+        q = torch.tensor(rope_complex(t(sw.wq).view(n, hq, d).numpy(), pos, sw.rope_theta))
+        k = torch.tensor(rope_complex(t(sw.wk).view(n, hkv, d).numpy(), pos, sw.rope_theta))
+        v = t(sw.wv).view(n, hkv, d)
+        qs.append(q.numpy())
+        ks.append(k.numpy())
+        vs.append(v.numpy())
+        kk = k.repeat_interleave(hq // hkv, dim=1).transpose(0, 1)
+        vv = v.repeat_interleave(hq // hkv, dim=1).transpose(0, 1)
+        o = F.scaled_dot_product_attention(q.transpose(0, 1), kk, vv, is_causal=True)
+        h = h + o.transpose(0, 1).reshape(n, hq * d) @ torch.tensor(np.asarray(sw.wo[l], np.float64))
+    return qs, ks, vs, h.numpy()
+
+
+def small_stack(**kw):
+    base = dict(overrides=dict(n_layers=4, critical_layers=(1, 2)))
+    base.update(kw)
+    return make_stack_workload("c3_small", **base)
+
+
+def test_stack_ratio_one_is_full_forward():
+    # every context row recomputed: each request's rows must come out of the
+    # stack exactly as a plain causal forward of the request (paper: ratio 1 = full prefill)
+    sw = small_stack(chunk_lens=[[40, 24], [33]], q_lens=[6, 5])
+    res = S.stack_fusion(sw, rho_bp=10000)
+    for b in range(sw.batch):
+        rows = np.arange(sw.cu_kv[b], sw.cu_kv[b + 1])
+        assert np.array_equal(res["R"][b], rows)
+        _, ks, vs, h = torch_forward(sw, rows)
+        np.testing.assert_allclose(res["h_R"][b], h, rtol=2e-5, atol=2e-5)
+        for l in range(sw.n_layers):
+            np.testing.assert_allclose(res["k_fuse"][l][rows], ks[l], rtol=2e-5, atol=2e-5)
+            np.testing.assert_allclose(res["v_fuse"][l][rows], vs[l], rtol=2e-5, atol=2e-5)
+
+
+def test_stack_ratio_zero_single_chunk_is_exact_reuse():
+    # one chunk stored alone at positions 0..n-1 is exactly the prefix of the
+    # request, so reusing it (ratio 0) gives the query rows the full forward's states
+    sw = small_stack(chunk_lens=[[57]], q_lens=[7])
+    res = S.stack_fusion(sw, rho_bp=0)
+    rows = np.arange(sw.cu_kv[0], sw.cu_kv[1])
+    assert res["P"][0].size == 0
+    _, _, _, h = torch_forward(sw, rows)
+    np.testing.assert_allclose(res["h_R"][0], h[57:], rtol=2e-5, atol=2e-5)
+
+
+def test_stack_probe_with_every_token_as_anchor():
+    # with every context token an anchor of a single chunk, the query probe is
+    # the full forward of the request's query rows up to the last critical
+    # layer, and the scores are the full-view softmax masses at the critical layers
+    sw = small_stack(chunk_lens=[[45]], q_lens=[6], anchors_per_chunk=45)
+    assert sw.anchor_local[0].size == 45
+    res = S.stack_fusion(sw)
+    rows = np.arange(sw.cu_kv[0], sw.cu_kv[1])
+    lmax = max(sw.critical_layers)
+    qs, ks, _, h = torch_forward(sw, rows, n_layers=lmax + 1)
+    np.testing.assert_allclose(res["h_probe"][0], h[45:], rtol=2e-5, atol=2e-5)
+    want = np.zeros(45)
+    for l in sw.critical_layers:
+        g = sw.n_q_heads // sw.n_kv_heads
+        for hh in range(sw.n_q_heads):
+            lg = torch.tensor(qs[l][45:, hh] @ ks[l][:45, hh // g].T) / math.sqrt(sw.head_dim)
+            want += torch.softmax(lg, dim=1).sum(0).numpy()
+    np.testing.assert_allclose(res["scores"][:45], want, rtol=1e-4, atol=1e-6)
+
+
+def test_stack_scores_sum_to_softmax_count():
+    # each (layer, head, query row) softmax over the context sums to 1
+    sw = small_stack(chunk_lens=[[40, 24], [33]], q_lens=[6, 5])
+    res = S.stack_fusion(sw)
+    for b in range(sw.batch):
+        a, N = int(sw.cu_kv[b]), int(sw.ctx_len[b])
+        tot = res["scores"][a:a + N].sum()
+        assert abs(tot - len(sw.critical_layers) * sw.n_q_heads * sw.q_lens[b]) < 1e-9 * tot
+        counts = [(3000 * n) // 10000 for n in sw.chunk_lens[b]]
+        assert res["P"][b].size == sum(counts)
+
+
+def test_stack_pin_catches_probe_position_error():
+    # a planted mistake (query rows rotated at 0..n_q-1 instead of N..N+n_q-1 in
+    # the probe) must fail the all-anchors pin
+    sw = small_stack(chunk_lens=[[45]], q_lens=[6], anchors_per_chunk=45)
+    orig = S.block_qkv
+
+    def bad(sw_, l, h, pos):
+        if len(pos) == 6 and pos[0] == 45:
+            pos = pos - 45
+        return orig(sw_, l, h, pos)
+
+    S.block_qkv = bad
+    try:
+        res = S.stack_fusion(sw)
+    finally:
+        S.block_qkv = orig
+    rows = np.arange(sw.cu_kv[0], sw.cu_kv[1])
+    _, _, _, h = torch_forward(sw, rows, n_layers=max(sw.critical_layers) + 1)
+    assert not np.allclose(res["h_probe"][0], h[45:], rtol=2e-5, atol=2e-5)

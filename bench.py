@@ -84,6 +84,56 @@ def probe_attn_flops(step):
     return 4.0 * w.n_q_heads * w.head_dim * tot
 
 
+def stack_study(args):
+    """c3: the 36-layer stack.  Times the selector with the compact view (anchors, critical
+    layers) and with the full view (every context token, every layer), the recompute of
+    every layer, and the overlap of the two selections (the paper's requirement
+    T_select(C_A, L*) < T_select(C, L) and the coverage it trades for it)."""
+    import torch
+    from paper_2606_05875_amd.stack import FusionStack
+    from paper_2606_05875_amd.workloads import full_view, make_stack_workload
+
+    torch.cuda.set_device(0)
+    sw = make_stack_workload("c3")
+    res = {}
+    for view, w in (("anchors", sw), ("full", full_view(sw))):
+        st = FusionStack(w)
+        st.build_pic()
+        for _ in range(max(1, args.warmup)):
+            st.run()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        t_sel, t_rec = [], []
+        for _ in range(args.steps):
+            ev[0].record()
+            st.select()
+            ev[1].record()
+            st.recompute()
+            ev[2].record()
+            torch.cuda.synchronize()
+            t_sel.append(ev[0].elapsed_time(ev[1]))
+            t_rec.append(ev[1].elapsed_time(ev[2]))
+        out = st.results()
+        res[view] = dict(select_ms=float(np.median(t_sel)), recompute_ms=float(np.median(t_rec)),
+                         P=np.concatenate(out["P"]), n_R=int(out["R"].size))
+        del st
+        torch.cuda.empty_cache()
+    a, f = res["anchors"], res["full"]
+    overlap = np.intersect1d(a["P"], f["P"]).size / max(f["P"].size, 1)
+    L = sw.n_layers
+    print(json.dumps({
+        "metric": "c3 stack: selected-token fused-prefill tokens/s per layer", "unit": "tokens/s",
+        "value": a["n_R"] * L / ((a["select_ms"] + a["recompute_ms"]) * 1e-3),
+        "recompute_only_value": a["n_R"] * L / (a["recompute_ms"] * 1e-3),
+        "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic (seeded, random weights)",
+        "config": {"workload": "c3: " + sw.meta["desc"], "recomputed_rows": a["n_R"], "layers": L,
+                   "rho_bp": sw.rho_bp},
+        "select_ms": {"anchors_critical_layers": a["select_ms"], "full_view_all_layers": f["select_ms"]},
+        "recompute_ms": a["recompute_ms"],
+        "select_speedup": f["select_ms"] / a["select_ms"],
+        "P_overlap_with_full_view": overlap}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -95,6 +145,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 256 MiB device-to-device copy 20 times (HBM counter calibration)")
+    ap.add_argument("--stack", action="store_true",
+                    help="the c3 multi-layer stack instead: selection (anchor view vs full view) and "
+                         "recompute times, one JSON line (not the headline metric)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -112,6 +165,8 @@ def main():
         print(json.dumps({"calibration": "copy", "bytes_read": x.numel() * 4, "bytes_written": y.numel() * 4,
                           "launches": 20}), flush=True)
         return
+    if args.stack:
+        return stack_study(args)
     from paper_2606_05875_amd.step import FusionStep
     from paper_2606_05875_amd.workloads import make_workload
 

@@ -10,14 +10,15 @@ Flow (Section 3.5 with the critical-layer selector of Section 3.4.2):
   offline  each chunk runs through the stack alone at positions 0..n_i-1 and
            its per-layer K/V becomes the chunk's PIC cache (all chunks of a
            layer as one batch of independent sequences);
-  probe    layers 0..max(L*): qcf_assemble re-positions the layer's chunks
-           into the request cache, rotates the query rows' fresh q/k at
-           N + i and fills the probe buffer [anchors ; query]; the query rows
-           attend over it; at a critical layer qcf_probe_scores adds the
-           layer's importance to the scores;
+  probe    layers 0..max(L*): qcf_assemble rotates the query rows' fresh q/k
+           at N + i and fills the probe buffer [anchors ; query] (anchors
+           re-positioned straight from the stored chunks); the query rows
+           attend over it; at a critical layer the same launch also
+           re-positions the layer's chunks into the request cache and
+           qcf_probe_scores adds the layer's importance to the scores;
   select   one qcf_select_topk -> P; R = [P ; query rows] per request;
-  recompute every layer: re-position (layers past the probe), scatter R's
-           fresh K/V (q rotated alongside), attend R over the fused cache.
+  recompute every layer: re-position (layers that were not scored), scatter
+           R's fresh K/V (q rotated alongside), attend R over the fused cache.
 No device-to-host synchronisation happens inside ``run()``.
 """
 from __future__ import annotations
@@ -91,6 +92,7 @@ class FusionStack:
                                        wa(sw.batch, p.max_q, p.max_probe), 256),
                                    dtype=torch.uint8, device=dev)
         self.pic_built = False
+        self.no_seg = torch.zeros(0, dtype=torch.int32, device=dev)
 
     # -- glue: RMSNorm, projections, residual (torch) ---------------------------
     def _qkv(self, l, h):
@@ -127,18 +129,26 @@ class FusionStack:
 
     # -- online ---------------------------------------------------------------
     def run(self):
+        self.select()
+        self.recompute()
+
+    def select(self):
+        """Query probe up to the last critical layer, scores, one per-chunk top-k."""
         sw, p = self.sw, self.plan
         if not self.pic_built:
             self.build_pic()
-        L = sw.n_layers
         lmax = max(sw.critical_layers)
         # query probe over [anchor cache ; query] up to the last critical layer
         hU = self.embed.index_select(0, self.u_idx.long())
         first = True
         for l in range(lmax + 1):
             q, k, v = self._qkv(l, hU)
-            qcf.qcf_assemble(self.k_req[l], self.v_req[l], self.k_pic[l], self.v_pic[l], self.seg_start,
-                             self.seg_len, self.seg_delta, p.max_seg, q, k, v, self.u_idx, self.u_pos,
+            # the whole context is re-positioned here only where it is scored; other
+            # layers get the probe buffer and query rows now and their chunks in recompute()
+            crit = l in sw.critical_layers
+            segs = (self.seg_start, self.seg_len, self.seg_delta) if crit else (self.no_seg,) * 3
+            qcf.qcf_assemble(self.k_req[l], self.v_req[l], self.k_pic[l], self.v_pic[l], *segs,
+                             p.max_seg if crit else 0, q, k, v, self.u_idx, self.u_pos,
                              self.q_u, self.k_probe, self.v_probe, self.probe_src, self.probe_delta,
                              sw.rope_theta, query_src=self.u_src, query_slot=self.query_slot)
             qcf.qcf_sparse_prefill_attn(self.o_probe, self.q_u, self.u_pos, self.cu_q, self.k_probe,
@@ -156,10 +166,15 @@ class FusionStack:
         self.R_pos.copy_(self.R_pos_init)
         qcf.qcf_select_topk(self.R_idx, self.scores, self.seg_start, self.seg_len, self.seg_k,
                             self.out_start, p.max_seg, out_pos=self.R_pos, pos_base=self.pos_base)
-        # recompute R through every layer over the fused caches
+
+    def recompute(self):
+        """R through every layer over the fused caches (after select())."""
+        sw, p = self.sw, self.plan
+        L = sw.n_layers
+        lmax = max(sw.critical_layers)
         hR = self.embed.index_select(0, self.R_idx.long())
         for l in range(L):
-            if l > lmax:
+            if l not in sw.critical_layers:
                 qcf.qcf_rerope(self.k_req[l], self.k_pic[l], self.seg_start, self.seg_len, self.seg_delta,
                                p.max_seg, sw.rope_theta, v_out=self.v_req[l], v_in=self.v_pic[l])
             q, k, v = self._qkv(l, hR)

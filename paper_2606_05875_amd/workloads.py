@@ -39,7 +39,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 __all__ = ["CONFIGS", "Workload", "make_workload", "round_to_bf16", "config_names", "STACK_CONFIGS",
-           "StackWorkload", "make_stack_workload"]
+           "StackWorkload", "make_stack_workload", "full_view"]
 
 
 # ---------------------------------------------------------------------------
@@ -424,3 +424,14 @@ def make_stack_workload(name: str = "c3", seed: int = 0, rho_bp: int | None = No
         cu_q=cu_q, seg_start=seg_start, seg_len=seg_len, seg_req=seg_req, seg_delta=seg_delta,
         anchor_local=anchor_local, embed=embed, wq=wq, wk=wk, wv=wv, wo=wo,
         meta=dict(seed=seed, desc=cfg.get("desc", "")))
+
+
+def full_view(sw: StackWorkload) -> StackWorkload:
+    """The same request batch seen by the full-view reference selector (Section 3.2.2):
+    every context token is an anchor (the probe reads the complete stitched cache) and every
+    layer scores (the full layer set).  Layout only; nothing is recomputed here."""
+    import dataclasses
+    return dataclasses.replace(
+        sw, anchor_local=[np.arange(int(n), dtype=np.int32) for n in sw.seg_len],
+        critical_layers=tuple(range(sw.n_layers)),
+        meta=dict(sw.meta, view="full"))

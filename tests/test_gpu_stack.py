@@ -120,3 +120,20 @@ def test_stack_c3_full_size_properties():
     st.run()
     got = st.results()
     bf16_properties(sw, st, got)
+
+
+def test_stack_full_view_selector_matches_oracle():
+    # the full-view reference selector: every context token an anchor, every layer scores
+    from paper_2606_05875_amd.workloads import full_view
+    sw = full_view(make_stack_workload("c3_small", chunk_lens=[[40, 24, 17], [33]], q_lens=[6, 5]))
+    say("stack full view f32", sw.chunk_lens, sw.critical_layers)
+    want = S.stack_fusion(sw)
+    assert cut_margin(want["scores"], sw, sw.rho_bp) > 1e-4
+    st = FusionStack(sw)
+    st.run()
+    got = st.results()
+    np.testing.assert_allclose(got["scores"], want["scores"], rtol=1e-4, atol=1e-6)
+    for b in range(sw.batch):
+        np.testing.assert_array_equal(got["P"][b], want["P"][b])
+        np.testing.assert_allclose(got["h_probe"][b], want["h_probe"][b], rtol=2e-4, atol=2e-4)
+        np.testing.assert_allclose(got["h_R"][b], want["h_R"][b], rtol=2e-4, atol=2e-4)

@@ -31,7 +31,7 @@ import torch
 from . import qcf
 from .step import FusionPlan, kv_buffer
 
-__all__ = ["FusionStack"]
+__all__ = ["FusionStack", "HostPicPipeline"]
 
 
 class FusionStack:
@@ -127,16 +127,30 @@ class FusionStack:
             h = self._residual(l, h, o)
         self.pic_built = True
 
-    # -- online ---------------------------------------------------------------
-    def run(self):
-        self.select()
-        self.recompute()
+    # -- where the stored chunk caches come from ---------------------------------
+    class _Resident:
+        """Every layer's PIC cache stays in device memory."""
 
-    def select(self):
+        def __init__(self, st):
+            self.st = st
+
+        def get(self, l, full):
+            return self.st.k_pic[l], self.st.v_pic[l], self.st.probe_src
+
+        def release(self, l):
+            pass
+
+    # -- online ---------------------------------------------------------------
+    def run(self, src=None):
+        self.select(src)
+        self.recompute(src)
+
+    def select(self, src=None):
         """Query probe up to the last critical layer, scores, one per-chunk top-k."""
         sw, p = self.sw, self.plan
         if not self.pic_built:
             self.build_pic()
+        src = src or self._Resident(self)
         lmax = max(sw.critical_layers)
         # query probe over [anchor cache ; query] up to the last critical layer
         hU = self.embed.index_select(0, self.u_idx.long())
@@ -147,10 +161,12 @@ class FusionStack:
             # layers get the probe buffer and query rows now and their chunks in recompute()
             crit = l in sw.critical_layers
             segs = (self.seg_start, self.seg_len, self.seg_delta) if crit else (self.no_seg,) * 3
-            qcf.qcf_assemble(self.k_req[l], self.v_req[l], self.k_pic[l], self.v_pic[l], *segs,
+            kp, vp, psrc = src.get(l, full=crit)
+            qcf.qcf_assemble(self.k_req[l], self.v_req[l], kp, vp, *segs,
                              p.max_seg if crit else 0, q, k, v, self.u_idx, self.u_pos,
-                             self.q_u, self.k_probe, self.v_probe, self.probe_src, self.probe_delta,
+                             self.q_u, self.k_probe, self.v_probe, psrc, self.probe_delta,
                              sw.rope_theta, query_src=self.u_src, query_slot=self.query_slot)
+            src.release(l)
             qcf.qcf_sparse_prefill_attn(self.o_probe, self.q_u, self.u_pos, self.cu_q, self.k_probe,
                                         self.v_probe, self.cu_probe, p.max_q, p.max_probe, self.scale,
                                         kv_pos=self.probe_pos, workspace=self.ws_attn)
@@ -167,16 +183,18 @@ class FusionStack:
         qcf.qcf_select_topk(self.R_idx, self.scores, self.seg_start, self.seg_len, self.seg_k,
                             self.out_start, p.max_seg, out_pos=self.R_pos, pos_base=self.pos_base)
 
-    def recompute(self):
+    def recompute(self, src=None):
         """R through every layer over the fused caches (after select())."""
         sw, p = self.sw, self.plan
+        src = src or self._Resident(self)
         L = sw.n_layers
-        lmax = max(sw.critical_layers)
         hR = self.embed.index_select(0, self.R_idx.long())
         for l in range(L):
             if l not in sw.critical_layers:
-                qcf.qcf_rerope(self.k_req[l], self.k_pic[l], self.seg_start, self.seg_len, self.seg_delta,
-                               p.max_seg, sw.rope_theta, v_out=self.v_req[l], v_in=self.v_pic[l])
+                kp, vp, _ = src.get(l, full=True)
+                qcf.qcf_rerope(self.k_req[l], kp, self.seg_start, self.seg_len, self.seg_delta,
+                               p.max_seg, sw.rope_theta, v_out=self.v_req[l], v_in=vp)
+                src.release(l)
             q, k, v = self._qkv(l, hR)
             qcf.qcf_scatter_kv(self.k_req[l], self.v_req[l], k, v, self.R_idx, self.R_pos, sw.rope_theta,
                                q_new=q, q_out=self.q_R)
@@ -199,3 +217,118 @@ class FusionStack:
                     h_R=[hR[p.cu_R[b]:p.cu_R[b + 1]] for b in range(self.sw.batch)],
                     h_probe=[hP[cq[b]:cq[b + 1]] for b in range(self.sw.batch)],
                     k_fuse=[c(k) for k in self.k_req], v_fuse=[c(v) for v in self.v_req])
+
+
+class HostPicPipeline:
+    """Layer-wise pipelining of the stored chunk caches from pinned host memory
+    (Section 3.5: the caches of later layers load while earlier layers compute).
+
+    The PIC caches are moved to pinned host memory, every layer's full cache
+    and, separately, the compact block of its anchor rows in probe-buffer
+    order.  A copy stream (default priority) fills device staging slots (three
+    by default) in
+    the order the compute asks for them: during selection each probe layer
+    needs only its anchor block (a critical layer its full cache, which is
+    re-positioned there), during the recompute every layer not re-positioned
+    during selection needs its full cache.  The compute stream waits for a
+    slot's copy before its first use and frees the slot right after the launch
+    that reads it (assemble or re-position), so the next copy into it overlaps
+    the rest of that layer and the following one.  Results are bit-identical to
+    the device-resident run (same kernels, same values).
+    """
+
+    def __init__(self, st: FusionStack, slots: int = 3):
+        sw, p = st.sw, st.plan
+        self.st = st
+        self.n_slots = max(2, int(slots))
+        dev, dt = st.device, st.dtype
+        T, hkv, d = sw.n_rows, sw.n_kv_heads, sw.head_dim
+        if not st.pic_built:
+            st.build_pic()
+        anchor_slots = np.nonzero(p.probe_src >= 0)[0]
+        a_rows = torch.from_numpy(p.probe_src[anchor_slots].astype(np.int64)).to(dev)
+        self.k_host, self.v_host, self.ka_host, self.va_host = [], [], [], []
+        for l in range(sw.n_layers):
+            for lst, x in ((self.k_host, st.k_pic[l]), (self.v_host, st.v_pic[l])):
+                h = torch.empty((T, hkv, d), dtype=dt, pin_memory=True)
+                h.copy_(x)
+                lst.append(h)
+            for lst, x in ((self.ka_host, st.k_pic[l]), (self.va_host, st.v_pic[l])):
+                h = torch.empty((anchor_slots.size, hkv, d), dtype=dt, pin_memory=True)
+                h.copy_(x.index_select(0, a_rows))
+                lst.append(h)
+        torch.cuda.synchronize()
+        # probe slots index the compact anchor block (query slots stay -1)
+        compact = np.full(p.probe_src.size, -1, np.int32)
+        compact[anchor_slots] = np.arange(anchor_slots.size, dtype=np.int32)
+        self.probe_src_compact = torch.from_numpy(compact).to(dev)
+        self.stage_k = [torch.empty((T, hkv, d), dtype=dt, device=dev) for _ in range(self.n_slots)]
+        self.stage_v = [torch.empty((T, hkv, d), dtype=dt, device=dev) for _ in range(self.n_slots)]
+        self.copy_stream = torch.cuda.Stream(device=dev)
+        # the order in which the compute asks for caches: (layer, full?)
+        lmax = max(sw.critical_layers)
+        self.order = [(l, l in sw.critical_layers) for l in range(lmax + 1)]
+        self.order += [(l, True) for l in range(sw.n_layers) if l not in sw.critical_layers]
+        self.bytes = sum((T if full else anchor_slots.size) * hkv * d * 2 * st.k_pic[0].element_size()
+                         for _, full in self.order)
+
+    def free_device_pic(self):
+        """Drop the device-resident caches (the pipeline then holds the only device copies)."""
+        st = self.st
+        st.k_pic = [None] * len(st.k_pic)
+        st.v_pic = [None] * len(st.v_pic)
+        torch.cuda.empty_cache()
+
+    def _issue(self, i):
+        if i >= len(self.order):
+            return
+        l, full = self.order[i]
+        slot = i % self.n_slots
+        with torch.cuda.stream(self.copy_stream):
+            if self.slot_free[slot] is not None:
+                self.copy_stream.wait_event(self.slot_free[slot])
+            src_k = self.k_host[l] if full else self.ka_host[l]
+            src_v = self.v_host[l] if full else self.va_host[l]
+            n = src_k.shape[0]
+            self.stage_k[slot][:n].copy_(src_k, non_blocking=True)
+            self.stage_v[slot][:n].copy_(src_v, non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(self.copy_stream)
+            self.copied[i] = ev
+
+    def begin(self):
+        """Enqueue the first copies, one per slot (call before select())."""
+        self.next = 0
+        self.copied = {}
+        self.slot_free = [None] * self.n_slots
+        for i in range(self.n_slots):
+            self._issue(i)
+        return self
+
+    def get(self, l, full):
+        i = self.next
+        assert self.order[i] == (l, full), (self.order[i], l, full)
+        torch.cuda.current_stream().wait_event(self.copied[i])
+        slot = i % self.n_slots
+        return self.stage_k[slot], self.stage_v[slot], (self.st.probe_src if full else self.probe_src_compact)
+
+    def release(self, l):
+        i = self.next
+        slot = i % self.n_slots
+        ev = torch.cuda.Event()
+        ev.record(torch.cuda.current_stream())
+        self.slot_free[slot] = ev
+        self.next = i + 1
+        self._issue(i + self.n_slots)
+
+    def copy_only(self):
+        """The copy sequence alone, back to back on the copy stream (no compute), for
+        timing the loads; the current stream waits for the last one."""
+        with torch.cuda.stream(self.copy_stream):
+            for i, (l, full) in enumerate(self.order):
+                src_k = self.k_host[l] if full else self.ka_host[l]
+                src_v = self.v_host[l] if full else self.va_host[l]
+                n = src_k.shape[0]
+                self.stage_k[i % self.n_slots][:n].copy_(src_k, non_blocking=True)
+                self.stage_v[i % self.n_slots][:n].copy_(src_v, non_blocking=True)
+        torch.cuda.current_stream().wait_stream(self.copy_stream)

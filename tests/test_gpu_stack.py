@@ -137,3 +137,33 @@ def test_stack_full_view_selector_matches_oracle():
         np.testing.assert_array_equal(got["P"][b], want["P"][b])
         np.testing.assert_allclose(got["h_probe"][b], want["h_probe"][b], rtol=2e-4, atol=2e-4)
         np.testing.assert_allclose(got["h_R"][b], want["h_R"][b], rtol=2e-4, atol=2e-4)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stack_host_pipeline_is_bit_identical(dtype):
+    # PIC caches streamed layer by layer from pinned host memory through two
+    # staging slots give exactly the device-resident run's results
+    from paper_2606_05875_amd.stack import HostPicPipeline
+    sw = make_stack_workload("c3_small", dtype=dtype, chunk_lens=[[40, 24, 17], [33]], q_lens=[6, 5])
+    say("stack host pipeline", dtype)
+    st = FusionStack(sw)
+    st.run()
+    want = st.results()
+    pipe = HostPicPipeline(st)
+    pipe.free_device_pic()
+    st.scores.zero_()
+    st.run(pipe.begin())
+    got = st.results()
+    np.testing.assert_array_equal(got["scores"], want["scores"])
+    np.testing.assert_array_equal(got["R"], want["R"])
+    for x, y in zip(got["h_R"], want["h_R"]):
+        np.testing.assert_array_equal(x, y)
+    for x, y in zip(got["h_probe"], want["h_probe"]):
+        np.testing.assert_array_equal(x, y)
+    for l in range(sw.n_layers):
+        np.testing.assert_array_equal(got["k_fuse"][l], want["k_fuse"][l])
+    # and again, reusing the pipeline
+    st.run(pipe.begin())
+    again = st.results()
+    for x, y in zip(again["h_R"], want["h_R"]):
+        np.testing.assert_array_equal(x, y)

@@ -179,6 +179,62 @@ def pipeline_study(args):
         "overlapped_ms": t_over, "overlap_efficiency": eff, "staging_slots": pipe.n_slots}), flush=True)
 
 
+def anchor_profile(args):
+    """Recall@10% (eq. profile_recall_at10) of planted evidence on the c3 stack: the query
+    probe with no anchors, Sink and Knorm anchors at several retained ratios, the full
+    view, and scoring at one layer at a time.  The evidence is a mechanism demonstration:
+    context duplicates of query tokens plus key heads that match their group's first query
+    head (the workload generator's ``evidence``); it is not the paper's span-labelled data."""
+    import dataclasses
+    import torch
+    from paper_2606_05875_amd.anchors import anchors_knorm, anchors_sink
+    from paper_2606_05875_amd.stack import FusionStack
+    from paper_2606_05875_amd.workloads import make_stack_workload
+
+    torch.cuda.set_device(0)
+    sw = make_stack_workload("c3", evidence=(2, 64))
+    E = sw.meta["evidence_rows"]
+    base = FusionStack(sw, rho_bp=1000)
+    base.build_pic()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def recall(anchor_local, layers):
+        sv = dataclasses.replace(sw, anchor_local=[np.asarray(a, np.int32) for a in anchor_local],
+                                 critical_layers=tuple(layers))
+        st = FusionStack(sv, rho_bp=1000, share=base)
+        st.select()
+        torch.cuda.synchronize()
+        ev[0].record()
+        st.select()
+        ev[1].record()
+        torch.cuda.synchronize()
+        P = st.R_idx.cpu().numpy()[:int(st.plan.n_P.sum())]
+        return float(np.isin(E, P).mean()), ev[0].elapsed_time(ev[1])
+
+    Lstar = sw.critical_layers
+    rows = []
+    r, t = recall([np.zeros(0, np.int32)] * sw.n_chunks, Lstar)
+    rows.append(dict(view="query only (r_a = 0)", recall=r, select_ms=t))
+    for ra in (500, 1000, 2000, 5000):
+        for name, fn in (("sink", lambda ra=ra: anchors_sink(sw.seg_len, ra)),
+                         ("knorm", lambda ra=ra: anchors_knorm(base.k_pic, sw.seg_start, sw.seg_len, ra))):
+            r, t = recall(fn(), Lstar)
+            rows.append(dict(view=f"{name} r_a = {ra / 10000:g}", recall=r, select_ms=t))
+    r, t = recall([np.arange(n) for n in sw.seg_len], Lstar)
+    rows.append(dict(view="full context (r_a = 1)", recall=r, select_ms=t))
+    kn = anchors_knorm(base.k_pic, sw.seg_start, sw.seg_len, 1000)
+    per_layer = [recall(kn, (l,))[0] for l in range(sw.n_layers)]
+    best = sorted(range(sw.n_layers), key=lambda l: -per_layer[l])[:3]
+    r_best, t_best = recall(kn, tuple(sorted(best)))
+    r_all, t_all = recall(kn, tuple(range(sw.n_layers)))
+    print(json.dumps({
+        "metric": "c3 stack: Recall@10% of planted evidence", "workload": "c3: " + sw.meta["desc"],
+        "evidence_rows": int(E.size), "scoring_layers_for_anchor_rows": list(Lstar),
+        "anchor_views": rows, "per_layer_recall_knorm10": per_layer,
+        "top3_layers": sorted(best), "top3_layers_recall": r_best, "top3_select_ms": t_best,
+        "all_layers_recall": r_all, "all_layers_select_ms": t_all}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -197,6 +253,9 @@ def main():
                     help="with --stack: the stored chunk caches stream layer by layer from pinned host "
                          "memory (copy-only, compute-only and overlapped times)")
     ap.add_argument("--slots", type=int, default=3, help="with --pipeline: device staging slots")
+    ap.add_argument("--anchor-profile", action="store_true",
+                    help="with --stack: Recall@10%% of planted evidence over anchor rules/ratios and "
+                         "single scoring layers (a mechanism demonstration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -215,6 +274,8 @@ def main():
                           "launches": 20}), flush=True)
         return
     if args.stack:
+        if args.anchor_profile:
+            return anchor_profile(args)
         return pipeline_study(args) if args.pipeline else stack_study(args)
     from paper_2606_05875_amd.step import FusionStep
     from paper_2606_05875_amd.workloads import make_workload

@@ -35,9 +35,10 @@ from __future__ import annotations
 
 import numpy as np
 
-from .qcfuse import (attention, critical_scores, round_storage, rope, select_per_chunk)
+from .qcfuse import (attention, critical_scores, round_storage, rope, select_per_chunk, select_topk)
 
-__all__ = ["rms_norm", "block_qkv", "full_forward", "build_pic", "stack_fusion"]
+__all__ = ["rms_norm", "block_qkv", "full_forward", "build_pic", "stack_fusion", "anchor_count",
+           "anchors_sink", "anchors_knorm"]
 
 
 def rms_norm(h, eps):
@@ -181,3 +182,28 @@ def stack_fusion(sw, rho_bp=None, pic=None):
         res["o_probe"].append(o_probe)
         res["h_probe"].append(hU)
     return res
+
+
+# ---------------------------------------------------------------------------
+# offline anchor sets  (Section 3.3.1, eq. anchor_set)
+# ---------------------------------------------------------------------------
+def anchor_count(n, ra_bp):
+    """ceil(r_a * n) with r_a in basis points (integer arithmetic)."""
+    return (int(ra_bp) * int(n) + 9999) // 10000
+
+
+def anchors_sink(seg_len, ra_bp):
+    """Sink rule: the first ceil(r_a n_i) positions of every chunk."""
+    return [np.arange(anchor_count(n, ra_bp), dtype=np.int64) for n in seg_len]
+
+
+def anchors_knorm(K_pic, seg_start, seg_len, ra_bp):
+    """Knorm rule: per chunk, the ceil(r_a n_i) positions whose stored keys have the
+    smallest L2 norm (mean over layers and KV heads of the per-head norm); equal
+    scores to the lower position, output ascending."""
+    norms = np.mean([np.linalg.norm(np.asarray(k, np.float64), axis=-1).mean(axis=-1) for k in K_pic], axis=0)
+    out = []
+    for a, n in zip(seg_start, seg_len):
+        a, n = int(a), int(n)
+        out.append(select_topk(-norms[a:a + n], anchor_count(n, ra_bp)))
+    return out

@@ -35,7 +35,9 @@ __all__ = ["FusionStack", "HostPicPipeline"]
 
 
 class FusionStack:
-    def __init__(self, sw, rho_bp: int | None = None, device="cuda"):
+    def __init__(self, sw, rho_bp: int | None = None, device="cuda", share: "FusionStack | None" = None):
+        """``share``: another FusionStack of the same weights and chunks whose uploaded
+        inputs and PIC caches are reused (another anchor view, critical-layer set or ratio)."""
         self.sw = sw
         self.rho_bp = sw.rho_bp if rho_bp is None else int(rho_bp)
         self.plan = p = FusionPlan.build(sw, self.rho_bp)
@@ -47,8 +49,12 @@ class FusionStack:
         self.scale = 1.0 / math.sqrt(d)
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         f = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
-        self.embed = f(sw.embed)
-        self.wq, self.wk, self.wv, self.wo = f(sw.wq), f(sw.wk), f(sw.wv), f(sw.wo)
+        if share is not None:
+            self.embed, self.wq, self.wk, self.wv, self.wo = (share.embed, share.wq, share.wk, share.wv,
+                                                              share.wo)
+        else:
+            self.embed = f(sw.embed)
+            self.wq, self.wk, self.wv, self.wo = f(sw.wq), f(sw.wk), f(sw.wv), f(sw.wo)
         # layout
         self.seg_start, self.seg_len, self.seg_delta = t(sw.seg_start), t(sw.seg_len), t(sw.seg_delta)
         self.seg_k, self.out_start, self.pos_base = t(p.seg_k), t(p.out_start), t(p.pos_base)
@@ -68,10 +74,14 @@ class FusionStack:
         self.cu_chunk_kv = t(np.concatenate([sw.seg_start, [T]]).astype(np.int32))
         self.max_chunk_kv = int(np.diff(np.concatenate([sw.seg_start, [T]])).max()) if sw.n_chunks else 1
         # caches: PIC and the per-layer request caches (padded rows, see kv_buffer)
-        self.k_pic = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
-        self.v_pic = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
-        self.k_req = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
-        self.v_req = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+        if share is not None:
+            self.k_pic, self.v_pic = share.k_pic, share.v_pic
+            self.k_req, self.v_req = share.k_req, share.v_req
+        else:
+            self.k_pic = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+            self.v_pic = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+            self.k_req = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
+            self.v_req = [kv_buffer(T, hkv, d, dt, dev, zero=True) for _ in range(L)]
         nU, nR, nP = p.u_idx.size, p.R_idx_init.size, p.probe_idx.size
         self.k_probe = kv_buffer(nP, hkv, d, dt, dev)
         self.v_probe = kv_buffer(nP, hkv, d, dt, dev)
@@ -91,7 +101,7 @@ class FusionStack:
                                           self.max_chunk_kv),
                                        wa(sw.batch, p.max_q, p.max_probe), 256),
                                    dtype=torch.uint8, device=dev)
-        self.pic_built = False
+        self.pic_built = share.pic_built if share is not None else False
         self.no_seg = torch.zeros(0, dtype=torch.int32, device=dev)
 
     # -- glue: RMSNorm, projections, residual (torch) ---------------------------

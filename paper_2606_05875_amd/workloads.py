@@ -367,9 +367,18 @@ class StackWorkload:
 
 def make_stack_workload(name: str = "c3", seed: int = 0, rho_bp: int | None = None,
                         chunk_lens=None, q_lens=None, anchors_per_chunk: int | None = None,
-                        dtype: str | None = None, overrides: dict | None = None) -> StackWorkload:
+                        dtype: str | None = None, overrides: dict | None = None,
+                        evidence: tuple | None = None) -> StackWorkload:
     """Draw a stack config's inputs.  Draw order (fixed): anchors, embeddings, then per
-    layer Wq, Wk, Wv, Wo."""
+    layer Wq, Wk, Wv, Wo; then, with ``evidence``, the planted evidence.
+
+    ``evidence = (n_chunks, count)`` plants answer-bearing tokens for a recall profile
+    (a mechanism demonstration, the paper's span-labelled datasets being absent): ``count``
+    context positions spread over ``n_chunks`` drawn chunks get the embedding of a drawn
+    user-query token plus 10% noise, and in every layer the key projection of each KV head
+    is the query projection of the group's first query head, so a query token's first
+    head matches its own duplicates ("matching heads").  The positions are returned in
+    ``meta["evidence_rows"]``."""
     cfg = dict(STACK_CONFIGS[name])
     if overrides:
         cfg.update(overrides)
@@ -415,6 +424,26 @@ def make_stack_workload(name: str = "c3", seed: int = 0, rho_bp: int | None = No
         wk[l] = rnd(rng.standard_normal((dm, hkv * d), dtype=np.float32) * sigma)
         wv[l] = rnd(rng.standard_normal((dm, hkv * d), dtype=np.float32) * sigma)
         wo[l] = rnd(rng.standard_normal((hq * d, dm), dtype=np.float32) * sigma)
+    ev_rows = np.zeros(0, np.int32)
+    if evidence is not None:
+        n_ev_chunks, count = int(evidence[0]), int(evidence[1])
+        grp = hq // hkv
+        for l in range(L):
+            for g in range(hkv):
+                wk[l][:, g * d:(g + 1) * d] = wq[l][:, g * grp * d:(g * grp + 1) * d]
+        ev = []
+        for b in range(B):
+            segs = np.nonzero(seg_req == b)[0]
+            pick = np.sort(rng.choice(segs, size=min(n_ev_chunks, segs.size), replace=False))
+            per = [count // pick.size + (1 if i < count % pick.size else 0) for i in range(pick.size)]
+            qrows = np.arange(cu_kv[b] + ctx[b], cu_kv[b + 1])
+            for s_, cnt in zip(pick, per):
+                loc = rng.choice(int(seg_len[s_]), size=min(cnt, int(seg_len[s_])), replace=False)
+                rows_e = int(seg_start[s_]) + loc
+                src = rng.choice(qrows, size=rows_e.size)
+                embed[rows_e] = embed[src] + 0.1 * rng.standard_normal((rows_e.size, dm), dtype=np.float32)
+                ev.append(rows_e)
+        ev_rows = np.sort(np.concatenate(ev)).astype(np.int32)
     embed = rnd(embed)
     return StackWorkload(
         name=name, dtype=dt, n_layers=L, d_model=dm, n_q_heads=hq, n_kv_heads=hkv, head_dim=d,
@@ -423,7 +452,7 @@ def make_stack_workload(name: str = "c3", seed: int = 0, rho_bp: int | None = No
         chunk_lens=chunk_lens, q_lens=q_lens_l, cu_kv=cu_kv, ctx_len=ctx.astype(np.int32),
         cu_q=cu_q, seg_start=seg_start, seg_len=seg_len, seg_req=seg_req, seg_delta=seg_delta,
         anchor_local=anchor_local, embed=embed, wq=wq, wk=wk, wv=wv, wo=wo,
-        meta=dict(seed=seed, desc=cfg.get("desc", "")))
+        meta=dict(seed=seed, desc=cfg.get("desc", ""), evidence_rows=ev_rows))
 
 
 def full_view(sw: StackWorkload) -> StackWorkload:

@@ -167,3 +167,25 @@ def test_stack_host_pipeline_is_bit_identical(dtype):
     again = st.results()
     for x, y in zip(again["h_R"], want["h_R"]):
         np.testing.assert_array_equal(x, y)
+
+
+def test_knorm_anchors_match_oracle():
+    from paper_2606_05875_amd.anchors import anchors_knorm
+    sw = make_stack_workload("c3_small", chunk_lens=[[40, 24, 17], [33]], q_lens=[6, 5])
+    say("knorm anchors", sw.chunk_lens)
+    K, V = S.build_pic(sw)
+    want = S.anchors_knorm(K, sw.seg_start, sw.seg_len, 1500)
+    st = FusionStack(sw)
+    st.build_pic()
+    got = anchors_knorm(st.k_pic, sw.seg_start, sw.seg_len, 1500)
+    for g, w_ in zip(got, want):
+        np.testing.assert_array_equal(g, w_)
+    # the shared-input view with those anchors runs and matches the oracle's selection
+    import dataclasses
+    sv = dataclasses.replace(sw, anchor_local=[np.asarray(a, np.int32) for a in want])
+    st2 = FusionStack(sv, share=st)
+    st2.run()
+    ref = S.stack_fusion(sv, pic=(K, V))
+    got2 = st2.results()
+    for b in range(sw.batch):
+        np.testing.assert_array_equal(got2["P"][b], ref["P"][b])

@@ -450,3 +450,22 @@ def test_stack_pin_catches_probe_position_error():
     rows = np.arange(sw.cu_kv[0], sw.cu_kv[1])
     _, _, _, h = torch_forward(sw, rows, n_layers=max(sw.critical_layers) + 1)
     assert not np.allclose(res["h_probe"][0], h[45:], rtol=2e-5, atol=2e-5)
+
+
+def test_anchor_rules():
+    # eq. anchor_set: ceil(r_a n) positions per chunk; Sink = the first ones; Knorm = the
+    # smallest mean key norms, checked against a plain sort of hand-made norms
+    assert [S.anchor_count(n, 1000) for n in (1, 9, 10, 11, 512)] == [1, 1, 1, 2, 52]
+    assert all(S.anchor_count(n, ra) == math.ceil(ra * n / 10000) for n in range(1, 70) for ra in (1, 333, 5000))
+    sk = S.anchors_sink([10, 3], 2500)
+    assert [list(x) for x in sk] == [[0, 1, 2], [0]]
+    rng = np.random.default_rng(5)
+    L, T, H, d = 3, 14, 2, 4
+    K = [rng.standard_normal((T, H, d)) for _ in range(L)]
+    K[1][3] *= 0.01          # a near-zero key -> chosen first
+    got = S.anchors_knorm(K, [0, 9], [9, 5], 3000)
+    mean_norm = [np.mean([np.sqrt((K[l][t] ** 2).sum(-1)).mean() for l in range(L)]) for t in range(T)]
+    want0 = sorted(sorted(range(9), key=lambda t: (mean_norm[t], t))[:3])
+    want1 = sorted(sorted(range(5), key=lambda t: (mean_norm[9 + t], t))[:2])
+    assert list(got[0]) == want0 and 3 in want0
+    assert list(got[1]) == want1

@@ -306,6 +306,22 @@ def main():
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
 
+    # the same steps in the fused-scores flow (scores straight from the stored chunk keys,
+    # re-positioning on a second stream), for comparison
+    for st in steps:
+        st.fused = True
+    for i in range(args.warmup):
+        steps[i % n_sets].run()
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(args.steps):
+        steps[i % n_sets].run()
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step_fused = t_start.elapsed_time(t_end) / args.steps
+    for st in steps:
+        st.fused = False
+
     # roofline: the same steps again, with events on the launch stream around every
     # recomputed-row attention call
     n_ev = min(args.steps, 100)
@@ -329,7 +345,8 @@ def main():
 
     # per-stage breakdown (separate, untimed for the headline): events around each stage
     stage_ms = {}
-    for name in FusionStep.STAGES:
+    for name in ("assemble", "scores", "rope_table", "rerope", "query_assemble", "scores_pic",
+                 "probe_attn", "select", "scatter", "attn"):
         fn = getattr(first, "stage_" + name)
         reps = 20
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -364,6 +381,7 @@ def main():
                      "traffic": measured_traffic(int(first.k.stride(0))) if args.config == "c2" else None,
                      "traffic_unit": "bytes per launch (HBM, calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE)",
                      "flops_per_launch": flops, "avg_launch_ms": attn_ms},
+        "ms_per_step_fused_scores_flow": ms_step_fused,
         "stage_ms": stage_ms,
         "assemble_GBs": asm_gbs,
         "assemble_hbm_frac": asm_gbs / PEAK_HBM_GBS,

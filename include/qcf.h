@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define QCF_VERSION 101
+#define QCF_VERSION 102
 
 typedef enum {
   QCF_OK = 0,
@@ -205,6 +205,47 @@ qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_
                             int max_ctx_len, int n_q_heads, int n_kv_heads, int head_dim,
                             float softmax_scale, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
+
+/*
+ * qcf_rope_table -- the rotations that move stored chunk keys to their request
+ * offsets (Section 2.1.2, eq. pic_online) as a table:
+ *   table[2 * (i * head_dim/2 + j) + {0, 1}] = cos, sin of pos[i] * theta^(-2j/head_dim)
+ * formed in float64 and rounded to float32 -- the values every rotation of
+ * this library uses for offset pos[i].  The table depends only on the
+ * offsets, so one table serves every layer of a request.
+ *   table  float32 [n, head_dim/2, 2] device output (16-byte aligned)
+ *   pos    int32 [n] device offsets
+ */
+qcf_status qcf_rope_table(float* table, const int32_t* pos, int64_t n, int head_dim,
+                          double rope_theta, hipStream_t stream);
+
+/*
+ * qcf_probe_scores_pic -- qcf_probe_scores over keys re-positioned on the fly
+ * (eq. pic_online fused into eq. single_layer_importance): the keys are read
+ * from the stored chunk caches and each is turned, in registers, by its row
+ * of a qcf_rope_table table before it meets the queries:
+ *   key of row t = rotate(k_pic[t], rope_table[key_rot[t]]), rounded to dtype,
+ * which is bit for bit the key qcf_rerope / qcf_assemble store for a chunk
+ * row whose offset is the table row's, so the scores equal those of
+ * qcf_rerope followed by qcf_probe_scores on the re-positioned cache.  The
+ * re-positioned keys are not written; the call depends only on the stored
+ * caches and the rotated queries.
+ *   k_pic    [n_kv_rows, k_row_stride] stored keys, rows laid out as the request
+ *            cache (row cu_kv[b] + t holds context token t of request b)
+ *   key_rot  int32 [n_kv_rows] table row of each key row (only context rows
+ *            are read; values are clamped into [0, n_rot))
+ *   rope_table, n_rot  a qcf_rope_table table of n_rot rows
+ * Every other argument, the workspace and the result are as for
+ * qcf_probe_scores (same workspace size).
+ */
+qcf_status qcf_probe_scores_pic(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                                const void* k_pic, int64_t n_kv_rows, int64_t k_row_stride,
+                                const int32_t* key_rot, const float* rope_table, int64_t n_rot,
+                                qcf_dtype dtype, int batch, const int32_t* cu_q,
+                                const int32_t* cu_kv, const int32_t* ctx_len, int max_q_len,
+                                int max_ctx_len, int n_q_heads, int n_kv_heads, int head_dim,
+                                float softmax_scale, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /*
  * qcf_select_topk -- recomputation set of eq. critical_mask, taken per

@@ -230,12 +230,17 @@ size_t qcf_probe_scores_workspace_size(int batch, int max_q_len, int max_ctx_len
   return qcf::probe_scores_workspace(s);
 }
 
-qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
-                            const void* k, int64_t n_kv_rows, int64_t k_row_stride,
-                            qcf_dtype dtype, int batch, const int32_t* cu_q, const int32_t* cu_kv,
-                            const int32_t* ctx_len, int max_q_len, int max_ctx_len, int n_q_heads,
-                            int n_kv_heads, int head_dim, float softmax_scale, void* workspace,
-                            size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+qcf_status probe_scores_impl(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                             const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                             const qcf::KeyRot& rot, qcf_dtype dtype, int batch,
+                             const int32_t* cu_q, const int32_t* cu_kv, const int32_t* ctx_len,
+                             int max_q_len, int max_ctx_len, int n_q_heads, int n_kv_heads,
+                             int head_dim, float softmax_scale, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
   if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
   qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
   if (st != QCF_OK) return st;
@@ -258,8 +263,53 @@ qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_
     return QCF_ERR_WORKSPACE;
   qcf::ProbeShape s{batch, max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim};
   return hip_status(qcf::launch_probe_scores(scores, accumulate, q, n_q_rows, k, n_kv_rows,
-                                             k_row_stride, dtype == QCF_BF16, cu_q, cu_kv, ctx_len,
-                                             s, softmax_scale, workspace, stream));
+                                             k_row_stride, rot, dtype == QCF_BF16, cu_q, cu_kv,
+                                             ctx_len, s, softmax_scale, workspace, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                            const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                            qcf_dtype dtype, int batch, const int32_t* cu_q, const int32_t* cu_kv,
+                            const int32_t* ctx_len, int max_q_len, int max_ctx_len, int n_q_heads,
+                            int n_kv_heads, int head_dim, float softmax_scale, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  return probe_scores_impl(scores, accumulate, q, n_q_rows, k, n_kv_rows, k_row_stride,
+                           qcf::KeyRot{nullptr, nullptr, 0}, dtype, batch, cu_q, cu_kv, ctx_len,
+                           max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim, softmax_scale,
+                           workspace, workspace_bytes, stream);
+}
+
+qcf_status qcf_rope_table(float* table, const int32_t* pos, int64_t n, int head_dim,
+                          double rope_theta, hipStream_t stream) {
+  if (n < 0 || n > INT32_MAX) return QCF_ERR_INVALID_ARG;
+  if (head_dim != 64 && head_dim != 128) return QCF_ERR_UNSUPPORTED;
+  if (!(rope_theta > 0.0)) return QCF_ERR_INVALID_ARG;
+  if (!tensor_ok(table, n == 0) || !index_ok(pos, n == 0)) return QCF_ERR_INVALID_ARG;
+  if (n == 0) return QCF_OK;
+  return hip_status(qcf::launch_rope_table(table, pos, n, head_dim, rope_theta, stream));
+}
+
+qcf_status qcf_probe_scores_pic(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                                const void* k_pic, int64_t n_kv_rows, int64_t k_row_stride,
+                                const int32_t* key_rot, const float* rope_table, int64_t n_rot,
+                                qcf_dtype dtype, int batch, const int32_t* cu_q,
+                                const int32_t* cu_kv, const int32_t* ctx_len, int max_q_len,
+                                int max_ctx_len, int n_q_heads, int n_kv_heads, int head_dim,
+                                float softmax_scale, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  const bool empty = batch == 0 || max_ctx_len == 0 || n_kv_rows == 0;
+  if (n_rot < 0 || n_rot > INT32_MAX) return QCF_ERR_INVALID_ARG;
+  if (!empty && (n_rot == 0 || !index_ok(key_rot, false) || !tensor_ok(rope_table, false)))
+    return QCF_ERR_INVALID_ARG;
+  // with no key to read the table is not touched (the other checks still apply)
+  const qcf::KeyRot rot{empty ? nullptr : key_rot, rope_table, n_rot};
+  return probe_scores_impl(scores, accumulate, q, n_q_rows, k_pic, n_kv_rows, k_row_stride, rot,
+                           dtype, batch, cu_q, cu_kv, ctx_len, max_q_len, max_ctx_len, n_q_heads,
+                           n_kv_heads, head_dim, softmax_scale, workspace, workspace_bytes, stream);
 }
 
 qcf_status qcf_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out, const float* scores,

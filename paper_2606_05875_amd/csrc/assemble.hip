@@ -77,9 +77,7 @@ __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride,
       Vec16<T>::unpack(b[k], x2);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float2 rr = cs[jj[k] + e];
-        y1[e] = x1[e] * rr.x - x2[e] * rr.y;
-        y2[e] = x1[e] * rr.y + x2[e] * rr.x;
+        rope_pair(x1[e], x2[e], cs[jj[k] + e], y1[e], y2[e]);
       }
       if (kok[k]) {
         st16(kdst + kofs[k], Vec16<T>::pack(y1));
@@ -165,9 +163,7 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
       Vec16<T>::unpack(ld16(qs + off + HALF), x2);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float2 rr = cs[j + e];
-        y1[e] = x1[e] * rr.x - x2[e] * rr.y;
-        y2[e] = x1[e] * rr.y + x2[e] * rr.x;
+        rope_pair(x1[e], x2[e], cs[j + e], y1[e], y2[e]);
       }
       st16(qd + off, Vec16<T>::pack(y1));
       st16(qd + off + HALF, Vec16<T>::pack(y2));

@@ -60,9 +60,7 @@ struct RopeUnits {
       Vec16<T>::unpack(b[k], x2);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float2 r = cs[jj[k] + e];
-        y1[e] = x1[e] * r.x - x2[e] * r.y;
-        y2[e] = x1[e] * r.y + x2[e] * r.x;
+        rope_pair(x1[e], x2[e], cs[jj[k] + e], y1[e], y2[e]);
       }
       if (base + (int)threadIdx.x + k * kThreads < units) {
         st16(dst + off[k], Vec16<T>::pack(y1));

@@ -27,6 +27,12 @@
 // vectors is 16 in-lane additions and one lane swap).  The fp32 path uses the
 // vector ALUs.  Every reduction has a fixed order, so results are
 // deterministic.
+//
+// With a rotation table (kRot) the keys come from the stored chunk caches and
+// each is moved to its request offset on the fly (eq. pic_online): a thread
+// loads rotate-half piece pairs of a key, turns them by the key's table row in
+// float32 and rounds to bf16 before the LDS store -- the very bits a stored
+// re-positioned key has -- so no re-positioned copy is read or waited for.
 #include <math.h>
 
 #include <algorithm>
@@ -81,10 +87,11 @@ __device__ __forceinline__ float2 combine_ml(float2 a, float2 b) {
 }
 
 // ---------------------------------------------------------------- bf16 passes
-template <int D, bool kCols>
+template <int D, bool kCols, bool kRot>
 __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
     float* __restrict__ part, float* __restrict__ colp, const uint16_t* __restrict__ q,
     int64_t n_q_rows, const uint16_t* __restrict__ k, int64_t n_kv_rows, int64_t k_stride,
+    const int32_t* __restrict__ key_rot, const float2* __restrict__ rot_tab, int n_rot,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
     const int32_t* __restrict__ ctx_len, int hq, int hkv, int lg, int n_qt, int n_splits,
     int split_keys, int max_qv, int max_ctx, float scale2) {
@@ -92,6 +99,9 @@ __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
   constexpr int CPR = D / 8;                           // 16-byte pieces per K row
   constexpr int PER = kChunkKeys * CPR / (kW * 64);    // pieces per thread per chunk
   constexpr int SPL = kMaxSplits / 2;                  // splits per lane in the merge
+  constexpr int HP = CPR / 2;                          // 16-byte pieces per rotate-half
+  constexpr int PU = PER / 2;                          // piece pairs per thread per chunk
+  static_assert(PER % 2 == 0, "rotation works on whole piece pairs");
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kChunkKeys * KSTR];
   __shared__ float lse_l[kCols ? kQvTile : 1];
   __shared__ float red[kCols ? kW : 1][kCols ? kChunkKeys : 1];
@@ -123,13 +133,46 @@ __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
   // masked where their products are used, so the rows read for them only
   // have to be finite.
   uint4 buf[PER];
+  // with kRot a thread owns piece pairs (j .. j+7, j+D/2 .. j+D/2+7) of a key,
+  // and the key's rotation-table row is loaded ahead of its pieces, so its
+  // (cos, sin) can be fetched (fetch_cs) while the pieces are still in flight
+  int rot_i[kRot ? PU : 1];
+  uint4 csv[kRot ? 4 * PU : 1];
   auto fetch = [&](int c0) {
+    if constexpr (kRot) {
+      int64_t rows[PU];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * kW * 64;
-      const int key = min(c0 + c / CPR, key_hi - 1), ch = c % CPR;
-      const int64_t row = min(k0 + key, n_kv_rows - 1);
-      buf[i] = ld16(k + row * k_stride + (int64_t)g * D + ch * 8);
+      for (int i = 0; i < PU; ++i) {
+        const int c = threadIdx.x + i * kW * 64;
+        rows[i] = min(k0 + min(c0 + c / HP, key_hi - 1), n_kv_rows - 1);
+        rot_i[i] = key_rot[rows[i]];
+      }
+#pragma unroll
+      for (int i = 0; i < PU; ++i) {
+        const int ch = (threadIdx.x + i * kW * 64) % HP;
+        const uint16_t* kp = k + rows[i] * k_stride + (int64_t)g * D + ch * 8;
+        buf[2 * i] = ld16(kp);
+        buf[2 * i + 1] = ld16(kp + D / 2);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int c = threadIdx.x + i * kW * 64;
+        const int key = min(c0 + c / CPR, key_hi - 1), ch = c % CPR;
+        const int64_t row = min(k0 + key, n_kv_rows - 1);
+        buf[i] = ld16(k + row * k_stride + (int64_t)g * D + ch * 8);
+      }
+    }
+  };
+  auto fetch_cs = [&]() {
+    if constexpr (kRot) {
+#pragma unroll
+      for (int i = 0; i < PU; ++i) {
+        const int ch = (threadIdx.x + i * kW * 64) % HP;
+        const float2* cp = rot_tab + (int64_t)min(max(rot_i[i], 0), n_rot - 1) * (D / 2) + ch * 8;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) csv[4 * i + v] = ld16(cp + 2 * v);
+      }
     }
   };
   if (key_lo < key_hi) fetch(key_lo);
@@ -139,6 +182,7 @@ __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
 #pragma unroll
     for (int st = 0; st < D / 16; ++st) qreg[st] = as_bf16x8(ld16(qp + 16 * st));
   }
+  if (kRot && key_lo < key_hi) fetch_cs();
   float lse_v[kCols ? 16 : 1];
   if (kCols) {
     // the vector's base-2 log-sum-exp over every split: lanes l (even splits)
@@ -174,16 +218,39 @@ __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
   float m = -INFINITY, ls = 0.f;
   for (int c0 = key_lo; c0 < key_hi; c0 += kChunkKeys) {
     if (c0 > key_lo) __syncthreads();  // the previous chunk (and its sums) are no longer read
+    if constexpr (kRot) {
+      // the re-positioned key, rounded to bf16 as a stored re-positioned key is
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * kW * 64;
-      st16(&k_lds[(c / CPR) * KSTR + (c % CPR) * 8], buf[i]);
+      for (int i = 0; i < PU; ++i) {
+        const int c = threadIdx.x + i * kW * 64;
+        float x1[8], x2[8], y1[8], y2[8];
+        Vec16<uint16_t>::unpack(buf[2 * i], x1);
+        Vec16<uint16_t>::unpack(buf[2 * i + 1], x2);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint4 cv = csv[4 * i + e / 2];
+          const float2 cs = (e & 1) ? make_float2(__uint_as_float(cv.z), __uint_as_float(cv.w))
+                                    : make_float2(__uint_as_float(cv.x), __uint_as_float(cv.y));
+          rope_pair(x1[e], x2[e], cs, y1[e], y2[e]);
+        }
+        uint16_t* dst = &k_lds[(c / HP) * KSTR + (c % HP) * 8];
+        st16(dst, Vec16<uint16_t>::pack(y1));
+        st16(dst + D / 2, Vec16<uint16_t>::pack(y2));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int c = threadIdx.x + i * kW * 64;
+        st16(&k_lds[(c / CPR) * KSTR + (c % CPR) * 8], buf[i]);
+      }
     }
     __syncthreads();
-    if (c0 + kChunkKeys < key_hi) fetch(c0 + kChunkKeys);  // in flight during this chunk's work
+    const bool more = c0 + kChunkKeys < key_hi;
+    if (more) fetch(c0 + kChunkKeys);  // in flight during this chunk's work
     const int n_keys = min(key_hi - c0, kChunkKeys);
     const int n_grp = (n_keys + 31) / 32;
     for (int kg = 0; kg < n_grp; ++kg) {
+      if (kRot && more && kg == 1) fetch_cs();  // the next chunk's rotations, behind its pieces
       bf16x8 a[D / 16];
 #pragma unroll
       for (int st = 0; st < D / 16; ++st) a[st] = as_bf16x8(ld16(&k_lds[(kg * 32 + lq) * KSTR + 8 * hi + 16 * st]));
@@ -268,11 +335,30 @@ __global__ __launch_bounds__(kThreads) void scores_final(float* __restrict__ sco
 }
 
 // ---------------------------------------------------------------- fp32 path
-template <int D>
+// key row `row` into kr[D], turned by its rotation-table row when kRot
+template <int D, bool kRot>
+__device__ __forceinline__ void key_f32(float* kr, const float* __restrict__ kp, int64_t row,
+                                        const int32_t* __restrict__ key_rot,
+                                        const float2* __restrict__ rot_tab, int n_rot) {
+#pragma unroll
+  for (int e = 0; e < D; ++e) kr[e] = kp[e];
+  if constexpr (kRot) {
+    const float2* cs = rot_tab + (int64_t)min(max(key_rot[row], 0), n_rot - 1) * (D / 2);
+#pragma unroll
+    for (int j = 0; j < D / 2; ++j) {
+      const float x1 = kr[j], x2 = kr[j + D / 2];
+      rope_pair(x1, x2, cs[j], kr[j], kr[j + D / 2]);
+    }
+  }
+}
+
+template <int D, bool kRot>
 __global__ __launch_bounds__(64) void probe_stats_f32(float2* __restrict__ stats,
                                                       const float* __restrict__ q, int64_t n_q_rows,
                                                       const float* __restrict__ k, int64_t n_kv_rows,
-                                                      int64_t k_stride, const int32_t* __restrict__ cu_q,
+                                                      int64_t k_stride, const int32_t* __restrict__ key_rot,
+                                                      const float2* __restrict__ rot_tab, int n_rot,
+                                                      const int32_t* __restrict__ cu_q,
                                                       const int32_t* __restrict__ cu_kv,
                                                       const int32_t* __restrict__ ctx_len, int hq,
                                                       int hkv, int max_q_len, float scale2) {
@@ -288,9 +374,11 @@ __global__ __launch_bounds__(64) void probe_stats_f32(float2* __restrict__ stats
   float m = -INFINITY, ls = 0.f;
   for (int t = threadIdx.x; t < N; t += 64) {
     if (k0 + t >= n_kv_rows) break;
-    const float* kp = k + (k0 + t) * k_stride + (int64_t)g * D;
+    float kr[D];
+    key_f32<D, kRot>(kr, k + (k0 + t) * k_stride + (int64_t)g * D, k0 + t, key_rot, rot_tab, n_rot);
     float acc = 0.f;
-    for (int e = 0; e < D; ++e) acc += qs[e] * kp[e];
+#pragma unroll
+    for (int e = 0; e < D; ++e) acc += qs[e] * kr[e];
     const float x = acc * scale2;
     const float mn = fmaxf(m, x);
     ls = ls * exp2f(m - mn) + exp2f(x - mn);
@@ -304,11 +392,12 @@ __global__ __launch_bounds__(64) void probe_stats_f32(float2* __restrict__ stats
     stats[((int64_t)b * hq + h) * max_q_len + i] = make_float2(ml.x, ml.y > 0.f ? 1.f / ml.y : 0.f);
 }
 
-template <int D>
+template <int D, bool kRot>
 __global__ __launch_bounds__(kThreads) void probe_cols_f32(
     float* __restrict__ scores, int accumulate, const float2* __restrict__ stats,
     const float* __restrict__ q, int64_t n_q_rows, const float* __restrict__ k, int64_t n_kv_rows,
-    int64_t k_stride, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
+    int64_t k_stride, const int32_t* __restrict__ key_rot, const float2* __restrict__ rot_tab,
+    int n_rot, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_kv,
     const int32_t* __restrict__ ctx_len, int hq, int hkv, int max_q_len, float scale2) {
   const int t = blockIdx.x * kThreads + threadIdx.x;
   const int b = blockIdx.y;
@@ -323,8 +412,11 @@ __global__ __launch_bounds__(kThreads) void probe_cols_f32(
   for (int h = 0; h < hq; ++h) {
     if (h % grp == 0) {
       const int g = h / grp;
+      if (ok)
+        key_f32<D, kRot>(kr, k + (k0 + t) * k_stride + (int64_t)g * D, k0 + t, key_rot, rot_tab, n_rot);
+      else
 #pragma unroll
-      for (int e = 0; e < D; ++e) kr[e] = ok ? k[(k0 + t) * k_stride + (int64_t)g * D + e] : 0.f;
+        for (int e = 0; e < D; ++e) kr[e] = 0.f;
     }
     for (int i = 0; i < nq && i < max_q_len; ++i) {
       if (q0 + i >= n_q_rows) break;
@@ -351,37 +443,45 @@ size_t probe_scores_workspace(const ProbeShape& s) {
 
 hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
                                const void* k, int64_t n_kv_rows, int64_t k_row_stride,
-                               bool bf16, const int32_t* cu_q, const int32_t* cu_kv,
-                               const int32_t* ctx_len, const ProbeShape& s, float scale,
-                               void* ws, hipStream_t stream) {
+                               const KeyRot& rot, bool bf16, const int32_t* cu_q,
+                               const int32_t* cu_kv, const int32_t* ctx_len, const ProbeShape& s,
+                               float scale, void* ws, hipStream_t stream) {
   if (s.batch == 0 || s.max_ctx_len == 0) return hipSuccess;
   const float scale2 = scale * kLog2e;
   int lg = 0;
   while ((1 << lg) < s.hq / s.hkv) ++lg;
+  const bool rt = rot.row != nullptr;
+  const float2* tab = reinterpret_cast<const float2*>(rot.table);
+  const int n_rot = rt ? (int)rot.n : 1;
   if (!bf16) {
     float2* stats = static_cast<float2*>(ws);
+    const float* qf = static_cast<const float*>(q);
+    const float* kf = static_cast<const float*>(k);
     if (s.max_q_len > 0) {
       dim3 g1(s.max_q_len, s.hq, s.batch);
-      if (s.d == 64)
-        probe_stats_f32<64><<<g1, 64, 0, stream>>>(stats, (const float*)q, n_q_rows, (const float*)k,
-                                                   n_kv_rows, k_row_stride, cu_q, cu_kv, ctx_len,
-                                                   s.hq, s.hkv, s.max_q_len, scale2);
-      else
-        probe_stats_f32<128><<<g1, 64, 0, stream>>>(stats, (const float*)q, n_q_rows, (const float*)k,
-                                                    n_kv_rows, k_row_stride, cu_q, cu_kv, ctx_len,
-                                                    s.hq, s.hkv, s.max_q_len, scale2);
+#define QCF_STATS(D, R)                                                                           \
+  probe_stats_f32<D, R><<<g1, 64, 0, stream>>>(stats, qf, n_q_rows, kf, n_kv_rows, k_row_stride, \
+                                               rot.row, tab, n_rot, cu_q, cu_kv, ctx_len, s.hq,  \
+                                               s.hkv, s.max_q_len, scale2)
+      if (s.d == 64) {
+        if (rt) QCF_STATS(64, true); else QCF_STATS(64, false);
+      } else {
+        if (rt) QCF_STATS(128, true); else QCF_STATS(128, false);
+      }
+#undef QCF_STATS
     }
     dim3 g2((s.max_ctx_len + kThreads - 1) / kThreads, s.batch);
-    if (s.d == 64)
-      probe_cols_f32<64><<<g2, kThreads, 0, stream>>>(scores, accumulate, stats, (const float*)q,
-                                                      n_q_rows, (const float*)k, n_kv_rows,
-                                                      k_row_stride, cu_q, cu_kv, ctx_len, s.hq,
-                                                      s.hkv, s.max_q_len, scale2);
-    else
-      probe_cols_f32<128><<<g2, kThreads, 0, stream>>>(scores, accumulate, stats, (const float*)q,
-                                                       n_q_rows, (const float*)k, n_kv_rows,
-                                                       k_row_stride, cu_q, cu_kv, ctx_len, s.hq,
-                                                       s.hkv, s.max_q_len, scale2);
+#define QCF_COLS(D, R)                                                                             \
+  probe_cols_f32<D, R><<<g2, kThreads, 0, stream>>>(scores, accumulate, stats, qf, n_q_rows, kf,  \
+                                                    n_kv_rows, k_row_stride, rot.row, tab, n_rot, \
+                                                    cu_q, cu_kv, ctx_len, s.hq, s.hkv,            \
+                                                    s.max_q_len, scale2)
+    if (s.d == 64) {
+      if (rt) QCF_COLS(64, true); else QCF_COLS(64, false);
+    } else {
+      if (rt) QCF_COLS(128, true); else QCF_COLS(128, false);
+    }
+#undef QCF_COLS
     return hipGetLastError();
   }
   const WsLayout w = ws_layout(s);
@@ -395,19 +495,21 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
     const int64_t nblk = (int64_t)s.hkv * w.n_qt * w.n_splits * s.batch;
     if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
     dim3 grid((unsigned)nblk);
-#define QCF_PASS(D, C)                                                                             \
-  scores_pass_bf16<D, C><<<grid, kW * 64, 0, stream>>>(part, colp, qb, n_q_rows, kb, n_kv_rows,   \
-                                                       k_row_stride, cu_q, cu_kv, ctx_len, s.hq, \
-                                                       s.hkv, lg, w.n_qt, w.n_splits,            \
-                                                       w.split_keys, w.max_qv, s.max_ctx_len,    \
-                                                       scale2)
+#define QCF_PASS(D, C, R)                                                                          \
+  scores_pass_bf16<D, C, R><<<grid, kW * 64, 0, stream>>>(                                         \
+      part, colp, qb, n_q_rows, kb, n_kv_rows, k_row_stride, rot.row, tab, n_rot, cu_q, cu_kv,     \
+      ctx_len, s.hq, s.hkv, lg, w.n_qt, w.n_splits, w.split_keys, w.max_qv, s.max_ctx_len, scale2)
+#define QCF_PASSES(D, R) \
+  do {                   \
+    QCF_PASS(D, false, R); \
+    QCF_PASS(D, true, R);  \
+  } while (0)
     if (s.d == 64) {
-      QCF_PASS(64, false);
-      QCF_PASS(64, true);
+      if (rt) QCF_PASSES(64, true); else QCF_PASSES(64, false);
     } else {
-      QCF_PASS(128, false);
-      QCF_PASS(128, true);
+      if (rt) QCF_PASSES(128, true); else QCF_PASSES(128, false);
     }
+#undef QCF_PASSES
 #undef QCF_PASS
   }
   scores_final<<<dim3((s.max_ctx_len + kThreads - 1) / kThreads, s.batch), kThreads, 0, stream>>>(

@@ -63,6 +63,16 @@ __device__ __forceinline__ float2 rope_cs(double pos, int j, int d, double theta
   return make_float2((float)c, (float)s);
 }
 
+// One rotate-half pair (x1, x2) turned by the angle whose (cos, sin) is cs:
+// (x1 cos - x2 sin, x1 sin + x2 cos), each a product plus one fused
+// multiply-add in float32.  Every kernel that rotates keys or queries uses
+// this form, so a key rotated by one kernel equals the same key rotated by
+// another bit for bit.
+__device__ __forceinline__ void rope_pair(float x1, float x2, float2 cs, float& y1, float& y2) {
+  y1 = fmaf(x1, cs.x, -(x2 * cs.y));
+  y2 = fmaf(x1, cs.y, x2 * cs.x);
+}
+
 // Wave-wide reductions (64 lanes).
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -16,6 +16,9 @@ hipError_t launch_rerope(void* k_out, const void* k_in, void* v_out, const void*
                          const int32_t* src_start, int max_seg_len, double theta,
                          hipStream_t stream);
 
+hipError_t launch_rope_table(float* table, const int32_t* pos, int64_t n, int d, double theta,
+                             hipStream_t stream);
+
 hipError_t launch_gather_rows(void* dst, const void* src, const int32_t* idx, int64_t n_rows,
                               int64_t n_src_rows, int64_t row_bytes, int64_t src_stride,
                               int64_t dst_stride, hipStream_t stream);
@@ -55,12 +58,19 @@ hipError_t launch_assemble(const AssembleShape& s, const AssemblePtrs& p, hipStr
 struct ProbeShape {
   int batch, max_q_len, max_ctx_len, hq, hkv, d;
 };
+// Keys rotated on the fly: key row t is turned by table row key_rot[t]
+// (clamped into [0, n)); a null `row` reads the keys as stored.
+struct KeyRot {
+  const int32_t* row;
+  const float* table;
+  int64_t n;
+};
 size_t probe_scores_workspace(const ProbeShape& s);
 hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int64_t n_q_rows,
                                const void* k, int64_t n_kv_rows, int64_t k_row_stride,
-                               bool bf16, const int32_t* cu_q, const int32_t* cu_kv,
-                               const int32_t* ctx_len, const ProbeShape& s, float scale,
-                               void* ws, hipStream_t stream);
+                               const KeyRot& rot, bool bf16, const int32_t* cu_q,
+                               const int32_t* cu_kv, const int32_t* ctx_len, const ProbeShape& s,
+                               float scale, void* ws, hipStream_t stream);
 
 struct AttnShape {
   int batch, max_rows, max_kv, hq, hkv, d;

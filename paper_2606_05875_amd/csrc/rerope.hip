@@ -78,9 +78,7 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
       Vec16<T>::unpack(hi[k], x2);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float2 r = cs[jj[k] + e];
-        y1[e] = x1[e] * r.x - x2[e] * r.y;
-        y2[e] = x1[e] * r.y + x2[e] * r.x;
+        rope_pair(x1[e], x2[e], cs[jj[k] + e], y1[e], y2[e]);
       }
       st16(k_out + off_out[k], Vec16<T>::pack(y1));
       st16(k_out + off_out[k] + HALF, Vec16<T>::pack(y2));
@@ -130,7 +128,25 @@ hipError_t launch_t(void* k_out, const void* k_in, void* v_out, const void* v_in
   return hipGetLastError();
 }
 
+// table[i * d/2 + j] = the (cos, sin) that every rotation of this library
+// forms for offset pos[i] and frequency j (float64 angle, rounded to float32)
+__global__ __launch_bounds__(64) void rope_table_kernel(float2* __restrict__ table,
+                                                        const int32_t* __restrict__ pos, int d,
+                                                        double theta) {
+  const int64_t i = blockIdx.x;
+  if ((int)threadIdx.x < d / 2)
+    table[i * (d / 2) + threadIdx.x] = rope_cs((double)pos[i], threadIdx.x, d, theta);
+}
+
 }  // namespace
+
+hipError_t launch_rope_table(float* table, const int32_t* pos, int64_t n, int d, double theta,
+                             hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  rope_table_kernel<<<dim3((unsigned)n), 64, 0, stream>>>(reinterpret_cast<float2*>(table), pos, d,
+                                                          theta);
+  return hipGetLastError();
+}
 
 hipError_t launch_rerope(void* k_out, const void* k_in, void* v_out, const void* v_in, bool bf16,
                          int64_t n_out_rows, int64_t n_in_rows, int hkv, int d,

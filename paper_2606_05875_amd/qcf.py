@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import threading
 
 import torch
 
@@ -17,8 +18,9 @@ __all__ = [
     "QcfError", "lib", "lib_path", "qcf_version", "qcf_status_string", "qcf_recommended_row_stride",
     "qcf_rerope",
     "qcf_assemble", "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
+    "qcf_rope_table", "qcf_probe_scores_pic",
     "qcf_select_topk", "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
-    "EXPORTS",
+    "EXPORTS", "Prepared", "prepare",
 ]
 
 QCF_F32, QCF_BF16 = 0, 1
@@ -45,6 +47,9 @@ EXPORTS = {
     "qcf_probe_scores_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I]),
     "qcf_probe_scores": (_I, [_P, _I, _P, _I64, _P, _I64, _I64, _I, _I, _P, _P, _P, _I, _I, _I, _I,
                               _I, ctypes.c_float, _P, _SZ, _P]),
+    "qcf_rope_table": (_I, [_P, _P, _I64, _I, ctypes.c_double, _P]),
+    "qcf_probe_scores_pic": (_I, [_P, _I, _P, _I64, _P, _I64, _I64, _P, _P, _I64, _I, _I, _P, _P, _P,
+                                  _I, _I, _I, _I, _I, ctypes.c_float, _P, _SZ, _P]),
     "qcf_select_topk": (_I, [_P, _P, _I64, _P, _I64, _I, _P, _P, _P, _P, _P, _I, _P]),
     "qcf_sparse_prefill_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "qcf_sparse_prefill_attn": (_I, [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I, _I,
@@ -88,6 +93,52 @@ def _ptr(t):
 
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+class Prepared:
+    """One validated, marshalled libqcf call.  Calling it enqueues the same launch
+    again -- on `stream` (a raw HIP stream handle) or torch's current stream --
+    without repeating the argument checks and conversions; it keeps the tensors
+    of the call alive.  Buffers must not be reallocated while it is in use."""
+
+    __slots__ = ("name", "fn", "args", "keep")
+
+    def __init__(self, name, fn, args, keep):
+        self.name, self.fn, self.args, self.keep = name, fn, args, keep
+
+    def __call__(self, stream=None):
+        st = self.fn(*self.args, _stream() if stream is None else stream)
+        if st:
+            _check(st, self.name)
+
+
+class _Recorder(threading.local):
+    on = False
+    out = None
+    keep = None
+
+
+_REC = _Recorder()
+
+
+def _invoke(name, *args, keep=None):
+    fn = getattr(lib(), name)
+    if _REC.on:
+        _REC.out = Prepared(name, fn, args, (_REC.keep, keep))
+        return
+    _check(fn(*args, _stream()), name)
+
+
+def prepare(call, *args, **kwargs) -> Prepared:
+    """Validate and marshal ``call(*args, **kwargs)`` (a binding of this module) once and
+    return it as a Prepared call; a call with nothing to launch gives a no-op."""
+    _REC.on, _REC.out, _REC.keep = True, None, (args, kwargs)
+    try:
+        call(*args, **kwargs)
+    finally:
+        _REC.on, _REC.keep = False, None
+    out, _REC.out = _REC.out, None
+    return out if out is not None else Prepared(getattr(call, "__name__", "noop"), lambda *a: 0, (), None)
 
 
 def _dev(t, name, dtype=None):
@@ -152,12 +203,11 @@ def qcf_rerope(k_out, k_in, seg_start, seg_len, seg_delta, max_seg_len, rope_the
                               or v_out.stride(0) != k_out.stride(0) or v_in.stride(0) != k_in.stride(0)):
         raise QcfError("v_out/v_in must match k_out/k_in in shape and row stride")
     T_in, H, d = k_in.shape
-    st = lib().qcf_rerope(_ptr(k_out), _ptr(k_in), _ptr(v_out), _ptr(v_in), _dtype(k_in),
+    _invoke("qcf_rerope", _ptr(k_out), _ptr(k_in), _ptr(v_out), _ptr(v_in), _dtype(k_in),
                           k_out.shape[0], T_in, H, d, _rows(k_out, "k_out"), _rows(k_in, "k_in"),
                           seg_start.numel(),
                           _ptr(seg_start), _ptr(seg_len), _ptr(seg_delta), _ptr(src_start),
-                          int(max_seg_len), float(rope_theta), _stream())
-    _check(st, "qcf_rerope")
+                          int(max_seg_len), float(rope_theta))
 
 
 def qcf_assemble(k_cache, v_cache, k_pic, v_pic, seg_start, seg_len, seg_delta, max_seg_len,
@@ -197,14 +247,13 @@ def qcf_assemble(k_cache, v_cache, k_pic, v_pic, seg_start, seg_len, seg_delta, 
     if (probe_k.shape != (npb, hkv, d) or probe_v.shape != probe_k.shape
             or probe_delta.numel() != npb):
         raise QcfError("probe_k/probe_v must be [len(probe_src), H_kv, d]")
-    st = lib().qcf_assemble(_ptr(k_cache), _ptr(v_cache), T, rs, _ptr(k_pic), _ptr(v_pic),
+    _invoke("qcf_assemble", _ptr(k_cache), _ptr(v_cache), T, rs, _ptr(k_pic), _ptr(v_pic),
                             k_pic.shape[0], prs, seg_start.numel(), _ptr(seg_start), _ptr(seg_len),
                             _ptr(seg_delta), _ptr(src_start), int(max_seg_len), _ptr(q_new),
                             _ptr(k_new), _ptr(v_new), k_new.shape[0], nq, _ptr(query_row),
                             _ptr(query_pos), _ptr(query_src), _ptr(query_slot), _ptr(q_u),
                             _ptr(probe_k), _ptr(probe_v), npb, qrs, _ptr(probe_src), _ptr(probe_delta),
-                            _dtype(k_pic), hq, hkv, d, float(rope_theta), _stream())
-    _check(st, "qcf_assemble")
+                            _dtype(k_pic), hq, hkv, d, float(rope_theta))
 
 
 def qcf_gather_rows(dst, src, idx):
@@ -215,10 +264,9 @@ def qcf_gather_rows(dst, src, idx):
     if dst.shape[0] != idx.numel() or dst.shape[1:] != src.shape[1:]:
         raise QcfError("dst must be [len(idx), *src.shape[1:]]")
     row_bytes = src[0].numel() * src.element_size() if src.shape[0] else dst[0].numel() * dst.element_size()
-    st = lib().qcf_gather_rows(_ptr(dst), _ptr(src), _ptr(idx), idx.numel(), src.shape[0], row_bytes,
+    _invoke("qcf_gather_rows", _ptr(dst), _ptr(src), _ptr(idx), idx.numel(), src.shape[0], row_bytes,
                                _rows(src, "src") * src.element_size(),
-                               _rows(dst, "dst") * dst.element_size(), _stream())
-    _check(st, "qcf_gather_rows")
+                               _rows(dst, "dst") * dst.element_size())
 
 
 def qcf_scatter_kv(k_cache, v_cache, k_new, v_new, row_idx, row_pos, rope_theta, q_new=None,
@@ -245,11 +293,10 @@ def qcf_scatter_kv(k_cache, v_cache, k_new, v_new, row_idx, row_pos, rope_theta,
         hq = q_new.shape[1]
         if q_out.shape != (n, hq, d) or q_new.shape[1:] != (hq, d) or q_new.shape[0] != k_new.shape[0]:
             raise QcfError("q_out must be [n_rows, H_q, d] and q_new [n_src_rows, H_q, d]")
-    st = lib().qcf_scatter_kv(_ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"), _ptr(k_new),
+    _invoke("qcf_scatter_kv", _ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"), _ptr(k_new),
                               _ptr(v_new), _ptr(q_new), _ptr(q_out), k_new.shape[0], _ptr(src_idx),
                               _dtype(k_cache), n, _ptr(row_idx), _ptr(row_pos), hq, Hkv, d,
-                              float(rope_theta), _stream())
-    _check(st, "qcf_scatter_kv")
+                              float(rope_theta))
 
 
 def qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim):
@@ -275,11 +322,49 @@ def qcf_probe_scores(scores, q, k, cu_q, cu_kv, ctx_len, max_q_len, max_ctx_len,
     need = qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, hq, hkv, d)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
-    st = lib().qcf_probe_scores(_ptr(scores), int(bool(accumulate)), _ptr(q), nq, _ptr(k), T,
+    _invoke("qcf_probe_scores", _ptr(scores), int(bool(accumulate)), _ptr(q), nq, _ptr(k), T,
                                 _rows(k, "k"), _dtype(q), batch, _ptr(cu_q), _ptr(cu_kv), _ptr(ctx_len),
                                 int(max_q_len), int(max_ctx_len), hq, hkv, d, float(softmax_scale),
-                                _ptr(workspace), workspace.numel(), _stream())
-    _check(st, "qcf_probe_scores")
+                                _ptr(workspace), workspace.numel(), keep=workspace)
+
+
+def qcf_rope_table(table, pos, rope_theta):
+    """table [n, d/2, 2] float32 <- (cos, sin) of the rotations by pos[i] (int32 [n])."""
+    _dev(table, "table", torch.float32)
+    _i32(pos, "pos")
+    if table.dim() != 3 or table.shape[2] != 2 or table.shape[0] != pos.numel() or not table.is_contiguous():
+        raise QcfError("table must be a dense [n, head_dim/2, 2] float32 tensor with n = len(pos)")
+    _invoke("qcf_rope_table", _ptr(table), _ptr(pos), pos.numel(), 2 * table.shape[1],
+                              float(rope_theta))
+
+
+def qcf_probe_scores_pic(scores, q, k_pic, key_rot, rope_table, cu_q, cu_kv, ctx_len, max_q_len,
+                         max_ctx_len, softmax_scale, accumulate=False, workspace=None):
+    """qcf_probe_scores over k_pic's keys turned by rope_table[key_rot[t]] on the fly."""
+    _dev(scores, "scores", torch.float32)
+    _dev(q, "q")
+    _dev(k_pic, "k_pic", q.dtype)
+    _dev(rope_table, "rope_table", torch.float32)
+    for n, t in (("key_rot", key_rot), ("cu_q", cu_q), ("cu_kv", cu_kv), ("ctx_len", ctx_len)):
+        _i32(t, n)
+    if not q.is_contiguous() or not rope_table.is_contiguous():
+        raise QcfError("q and rope_table must be dense")
+    nq, hq, d = q.shape
+    T, hkv, d2 = k_pic.shape
+    if d2 != d or scores.numel() != T or key_rot.numel() != T:
+        raise QcfError("scores and key_rot need one entry per row of k_pic; head_dim must match")
+    if rope_table.dim() != 3 or tuple(rope_table.shape[1:]) != (d // 2, 2):
+        raise QcfError("rope_table must be [n_rot, head_dim/2, 2]")
+    batch = ctx_len.numel()
+    need = qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, hq, hkv, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _invoke("qcf_probe_scores_pic", _ptr(scores), int(bool(accumulate)), _ptr(q), nq, _ptr(k_pic), T,
+                                    _rows(k_pic, "k_pic"), _ptr(key_rot), _ptr(rope_table),
+                                    rope_table.shape[0], _dtype(q), batch, _ptr(cu_q), _ptr(cu_kv),
+                                    _ptr(ctx_len), int(max_q_len), int(max_ctx_len), hq, hkv, d,
+                                    float(softmax_scale), _ptr(workspace), workspace.numel(),
+                                    keep=workspace)
 
 
 def qcf_select_topk(out_idx, scores, seg_start, seg_len, seg_k, out_start, max_seg_len, out_pos=None,
@@ -292,10 +377,9 @@ def qcf_select_topk(out_idx, scores, seg_start, seg_len, seg_k, out_start, max_s
         _i32(t, n)
     if out_pos is not None and out_pos.numel() != out_idx.numel():
         raise QcfError("out_pos must match out_idx")
-    st = lib().qcf_select_topk(_ptr(out_idx), _ptr(out_pos), out_idx.numel(), _ptr(scores),
+    _invoke("qcf_select_topk", _ptr(out_idx), _ptr(out_pos), out_idx.numel(), _ptr(scores),
                                scores.numel(), seg_start.numel(), _ptr(seg_start), _ptr(seg_len),
-                               _ptr(seg_k), _ptr(out_start), _ptr(pos_base), int(max_seg_len), _stream())
-    _check(st, "qcf_select_topk")
+                               _ptr(seg_k), _ptr(out_start), _ptr(pos_base), int(max_seg_len))
 
 
 def qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, n_q_heads, n_kv_heads, head_dim,
@@ -328,9 +412,8 @@ def qcf_sparse_prefill_attn(out, q, row_pos, cu_rows, k_cache, v_cache, cu_kv, m
     need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, hq, hkv, d, q.dtype)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    st = lib().qcf_sparse_prefill_attn(_ptr(out), _ptr(lse), _ptr(q), _ptr(row_pos), n, _ptr(cu_rows),
+    _invoke("qcf_sparse_prefill_attn", _ptr(out), _ptr(lse), _ptr(q), _ptr(row_pos), n, _ptr(cu_rows),
                                        _ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"),
                                        _ptr(cu_kv), _ptr(kv_pos), _dtype(q), batch, int(max_rows),
                                        int(max_kv), hq, hkv, d, float(softmax_scale), _ptr(workspace),
-                                       0 if workspace is None else workspace.numel(), _stream())
-    _check(st, "qcf_sparse_prefill_attn")
+                                       0 if workspace is None else workspace.numel(), keep=workspace)

@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported(L):
                          "qcf_rerope", "qcf_assemble",
                          "qcf_gather_rows",
                          "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
-                         "qcf_select_topk", "qcf_sparse_prefill_attn_workspace_size",
+                         "qcf_rope_table", "qcf_probe_scores_pic", "qcf_select_topk", "qcf_sparse_prefill_attn_workspace_size",
                          "qcf_sparse_prefill_attn"}
     for name, nargs in decl.items():
         assert hasattr(L, name), name
@@ -49,7 +49,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.qcf_version() == 101
+    assert L.qcf_version() == 102
     for code in range(5):
         assert L.qcf_status_string(code)
     assert L.qcf_status_string(0) == b"ok"
@@ -148,6 +148,27 @@ def test_probe_scores_validation_and_workspace(L):
     assert L.qcf_probe_scores(*base(d=96)) == UNSUPPORTED
     assert L.qcf_probe_scores(*base(scale=0.0)) == INVALID
     assert L.qcf_probe_scores(*base(stride=1000)) == INVALID
+
+
+def test_rope_table_and_fused_scores_validation(L):
+    assert L.qcf_rope_table(A, A, -1, 128, 1e4, None) == INVALID
+    assert L.qcf_rope_table(A, A, 10, 96, 1e4, None) == UNSUPPORTED
+    assert L.qcf_rope_table(A, A, 10, 128, 0.0, None) == INVALID
+    assert L.qcf_rope_table(None, A, 10, 128, 1e4, None) == INVALID
+    assert L.qcf_rope_table(MIS, A, 10, 128, 1e4, None) == INVALID               # table not 16-aligned
+    assert L.qcf_rope_table(None, None, 0, 128, 1e4, None) == OK                 # empty: nothing launched
+    need = L.qcf_probe_scores_workspace_size(2, 64, 5120, 32, 8, 128)
+    base = lambda **kw: [A, 0, A, 128, A, 10368, kw.get("stride", 1024), kw.get("rot", A),
+                         kw.get("tab", A), kw.get("n_rot", 20), BF16, 2, A, A, A, 64, 5120, 32, 8,
+                         kw.get("d", 128), 0.088, A, kw.get("wsb", need), None]
+    assert L.qcf_probe_scores_pic(*base(rot=None)) == INVALID
+    assert L.qcf_probe_scores_pic(*base(tab=None)) == INVALID
+    assert L.qcf_probe_scores_pic(*base(tab=MIS)) == INVALID
+    assert L.qcf_probe_scores_pic(*base(n_rot=0)) == INVALID
+    assert L.qcf_probe_scores_pic(*base(n_rot=-1)) == INVALID
+    assert L.qcf_probe_scores_pic(*base(d=96)) == UNSUPPORTED
+    assert L.qcf_probe_scores_pic(*base(stride=1000)) == INVALID
+    assert L.qcf_probe_scores_pic(*base(wsb=need - 1)) == WORKSPACE
 
 
 def test_topk_and_attn_validation(L):

@@ -308,6 +308,89 @@ def test_probe_scores_workspace_reuse_across_shapes():
         assert torch.equal(a, b)
 
 
+def test_rope_table():
+    """The table holds float32 roundings of the float64 (cos, sin) of pos * theta^(-2j/d)."""
+    say("rope_table")
+    pos = np.array([0, 1, 7, 513, 4096, 31000, 123456], np.int32)
+    for d, theta in ((128, 1e6), (64, 1e4)):
+        tab = torch.empty((pos.size, d // 2, 2), dtype=torch.float32, device="cuda")
+        qcf.qcf_rope_table(tab, dev(pos), theta)
+        a = Q.rope_angles(pos, d, theta)
+        want = np.stack([np.cos(a), np.sin(a)], axis=-1)
+        got = tab.cpu().numpy()
+        # correctly rounded is within half a float32 step; the last float64 digits of two
+        # libm implementations may differ, so one step is allowed
+        step = np.abs(np.spacing(want.astype(np.float32))).astype(np.float64)
+        assert np.all(np.abs(got - want) <= step), "rope table off by more than one float32 step"
+        np.testing.assert_array_equal(got[0], np.stack([np.ones(d // 2), np.zeros(d // 2)], -1))
+
+
+@pytest.mark.parametrize("dtype,nqs,ctxs,hq,hkv,d,pad", [
+    ("bf16", [64], [5120], 32, 8, 128, 128),            # 10 x 512-token chunks, padded rows
+    ("bf16", [17, 1, 128], [700, 3000, 129], 32, 8, 128, 0),
+    ("bf16", [9], [1000], 8, 8, 64, 8),
+    ("bf16", [8, 3], [20000, 9000], 32, 8, 128, 0),     # several key chunks per split
+    ("f32", [32], [512], 8, 2, 64, 0),
+    ("f32", [5, 7], [300, 170], 8, 4, 128, 4),
+])
+def test_probe_scores_pic(dtype, nqs, ctxs, hq, hkv, d, pad):
+    """Scores over keys re-positioned in registers equal, bit for bit, qcf_rerope followed by
+    qcf_probe_scores, and match the oracle's scores of the re-positioned keys."""
+    say("probe_scores_pic", dtype, nqs, ctxs, hq, hkv, d, pad)
+    rng = np.random.default_rng(11)
+    B, theta = len(nqs), 1e6
+    rows = [c + q for c, q in zip(ctxs, nqs)]
+    cu_kv = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    cu_q = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    T = int(cu_kv[-1])
+    # ragged chunks tile each request's context; a chunk's offset is its first position
+    seg_start, seg_len, seg_delta = [], [], []
+    for b in range(B):
+        a = 0
+        while a < ctxs[b]:
+            n = min(ctxs[b] - a, int(rng.integers(1, 700)))
+            seg_start.append(int(cu_kv[b]) + a)
+            seg_len.append(n)
+            seg_delta.append(a)
+            a += n
+    seg_start, seg_len, seg_delta = (np.array(x, np.int32) for x in (seg_start, seg_len, seg_delta))
+    n_seg = seg_start.size
+    # table rows in shuffled order, so the per-row indirection is exercised
+    perm = rng.permutation(n_seg)
+    tab_pos = np.zeros(n_seg, np.int32)
+    tab_pos[perm] = seg_delta
+    key_rot = np.full(T, 10 ** 6, np.int32)          # query rows: never read as keys
+    for s in range(n_seg):
+        key_rot[seg_start[s]:seg_start[s] + seg_len[s]] = perm[s]
+    k_pic = draw(rng, (T, hkv, d), dtype, 1 / math.sqrt(d))
+    q = draw(rng, (int(cu_q[-1]), hq, d), dtype, 1.5 * math.sqrt(d))
+    table = torch.empty((n_seg, d // 2, 2), dtype=torch.float32, device="cuda")
+    qcf.qcf_rope_table(table, dev(tab_pos), theta)
+    kp = padded(k_pic, pad, DT[dtype])
+    scale = 1 / math.sqrt(d)
+    geo = (dev(cu_q), dev(cu_kv), dev(np.array(ctxs, np.int32)), max(nqs), max(ctxs), scale)
+    qd = dev(q, DT[dtype])
+    fused = torch.full((T,), -5.0, device="cuda")
+    qcf.qcf_probe_scores_pic(fused, qd, kp, dev(key_rot), table, *geo)
+    # the unfused path: re-position into a request cache, then score it
+    k_req = padded(np.zeros_like(k_pic), pad, DT[dtype])
+    qcf.qcf_rerope(k_req, kp, dev(seg_start), dev(seg_len), dev(seg_delta), int(seg_len.max()), theta)
+    ref = torch.full((T,), -5.0, device="cuda")
+    qcf.qcf_probe_scores(ref, qd, k_req, *geo)
+    assert torch.equal(fused, ref), "fused scores differ from re-position + scores"
+    got = fused.double().cpu().numpy()
+    krep = Q.rerope(k_pic, seg_start, seg_len, seg_delta, theta, dtype)
+    for b in range(B):
+        a = int(cu_kv[b])
+        want = Q.critical_scores(q[cu_q[b]:cu_q[b + 1]], krep[a:a + ctxs[b]], scale, hkv)
+        assert_scores(got[a:a + ctxs[b]], want, f"fused scores request {b}")
+        assert np.all(got[a + ctxs[b]:cu_kv[b + 1]] == -5.0)          # query slots untouched
+    # accumulate mode, as over several critical layers
+    qcf.qcf_probe_scores_pic(fused, qd, kp, dev(key_rot), table, *geo, accumulate=True)
+    qcf.qcf_probe_scores(ref, qd, k_req, *geo, accumulate=True)
+    assert torch.equal(fused, ref)
+
+
 @pytest.mark.parametrize("dtype,hq,hkv,d,n_kv,n_rows", [
     ("bf16", 32, 8, 128, 5184, 700),
     ("bf16", 64, 8, 128, 3000, 333),

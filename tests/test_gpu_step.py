@@ -107,11 +107,29 @@ def test_fused_assembly_matches_separate_calls(name):
     """qcf_assemble gives the same bits as qcf_rerope + qcf_scatter_kv + qcf_gather_rows."""
     w = make_workload(name)
     say(name, "fused vs separate assembly")
-    a = FusionStep(w)
+    a = FusionStep(w, fused=False)
     a.run(separate_assembly=True)
     g1 = a.results()
-    b = FusionStep(w)
+    b = FusionStep(w, fused=False)
     b.run()
+    g2 = b.results()
+    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u", "q_R"):
+        np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)
+    assert torch.equal(a.k_probe, b.k_probe) and torch.equal(a.v_probe, b.v_probe)
+
+
+@pytest.mark.parametrize("name,dtype", [("c2", "bf16"), ("c5", "bf16"), ("c1", "f32")])
+def test_fused_scores_flow_matches_unfused(name, dtype):
+    """The fused flow (scores straight from the stored chunk keys, re-positioning on the side
+    stream) gives the same bits as assemble -> scores, also over steps launched back to back."""
+    w = make_workload(name, dtype=dtype)
+    say(name, dtype, "fused vs unfused scores flow")
+    a = FusionStep(w, fused=False)
+    a.run()
+    g1 = a.results()
+    b = FusionStep(w, fused=True)
+    for _ in range(3):               # no synchronisation between the steps
+        b.run()
     g2 = b.results()
     for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u", "q_R"):
         np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)

@@ -235,6 +235,46 @@ def anchor_profile(args):
         "all_layers_recall": r_all, "all_layers_select_ms": t_all}), flush=True)
 
 
+def topk_study(args):
+    """qcf_select_topk alone: per-chunk selection and global (one segment per request)
+    selection on the contexts of the workloads, HIP events around 200 back-to-back calls."""
+    import torch
+    from paper_2606_05875_amd import qcf
+    from paper_2606_05875_amd.workloads import make_workload
+
+    torch.cuda.set_device(0)
+    rows = []
+    for name in ("c2", "c4", "c5"):
+        w = make_workload(name)
+        rng = np.random.default_rng(3)
+        sc = torch.from_numpy(rng.exponential(3.0, w.n_rows).astype(np.float32)).cuda()
+        for mode in ("chunk", "global"):
+            if mode == "chunk":
+                starts, lens, req = w.seg_start, w.seg_len, w.seg_req
+            else:
+                starts, lens, req = w.cu_kv[:-1], w.ctx_len, np.arange(w.batch)
+            ks = (int(w.rho_bp) * np.asarray(lens, np.int64)) // 10000
+            outs = np.concatenate([[0], np.cumsum(ks)[:-1]])
+            d = lambda a: torch.from_numpy(np.ascontiguousarray(np.asarray(a, np.int32))).cuda()
+            out = torch.empty(int(ks.sum()), dtype=torch.int32, device="cuda")
+            call = qcf.prepare(qcf.qcf_select_topk, out, sc, d(starts), d(lens), d(ks), d(outs),
+                               int(max(lens)))
+            for _ in range(10):
+                call()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(args.steps):
+                call()
+            b.record()
+            torch.cuda.synchronize()
+            rows.append({"workload": name, "selection": mode, "segments": int(len(lens)),
+                         "max_segment": int(max(lens)), "selected": int(ks.sum()),
+                         "us_per_call": a.elapsed_time(b) / args.steps * 1e3})
+    print(json.dumps({"study": "qcf_select_topk per-chunk vs global", "rho_bp": "per workload",
+                      "scores": "seeded exponential", "calls": args.steps, "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -253,6 +293,9 @@ def main():
                     help="with --stack: the stored chunk caches stream layer by layer from pinned host "
                          "memory (copy-only, compute-only and overlapped times)")
     ap.add_argument("--slots", type=int, default=3, help="with --pipeline: device staging slots")
+    ap.add_argument("--topk-study", action="store_true",
+                    help="time qcf_select_topk alone, per-chunk vs global selection, on the c2/c4/c5 "
+                         "contexts (one JSON line; not the headline metric)")
     ap.add_argument("--anchor-profile", action="store_true",
                     help="with --stack: Recall@10%% of planted evidence over anchor rules/ratios and "
                          "single scoring layers (a mechanism demonstration)")
@@ -273,6 +316,8 @@ def main():
         print(json.dumps({"calibration": "copy", "bytes_read": x.numel() * 4, "bytes_written": y.numel() * 4,
                           "launches": 20}), flush=True)
         return
+    if args.topk_study:
+        return topk_study(args)
     if args.stack:
         if args.anchor_profile:
             return anchor_profile(args)

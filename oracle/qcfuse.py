@@ -212,7 +212,7 @@ def select_per_chunk(scores_rows, seg_start, seg_len, rho_bp):
 # ---------------------------------------------------------------------------
 # one layer of the fusion step
 # ---------------------------------------------------------------------------
-def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True):
+def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True, selection="chunk"):
     """Run one layer's QCFuse fusion step on workload ``w`` (see the package's workloads).
 
     Steps, per request b:
@@ -222,7 +222,9 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True):
          request positions (eq. anchor_cache), probe attention of the query
          rows over [KV^A ; query K/V] (eq. anchor_query_state);
       4. scores I(t) of the context tokens (eq. single_layer_importance);
-      5. per-chunk top-k (eq. critical_mask) -> P; R = P U query rows;
+      5. top-k of the scores -> P (eq. critical_mask): per chunk, k_i = floor(rho n_i)
+         (``selection="chunk"``), or over the request's whole context, k = floor(rho N_b)
+         as the equation is written (``selection="global"``); R = P U query rows;
       6. rotate the fresh q/k of R at their positions and write fresh K/V into
          the cache rows R (eq. fuse_cache);
       7. causal attention of R over the fused cache (Section 2.1.3).
@@ -276,11 +278,16 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True):
         # scores over the request's context keys (re-positioned PIC keys)
         I = critical_scores(qU, K[base:base + N], scale, hkv)
         scores[base:base + N] = I
-        P = select_per_chunk(scores, w.seg_start[segs], w.seg_len[segs], rho_bp)
-        # near-tie band around each chunk's cut
+        if selection == "global":
+            sel = [(base, N)]
+        elif selection == "chunk":
+            sel = [(int(w.seg_start[s]), int(w.seg_len[s])) for s in segs]
+        else:
+            raise ValueError(f"selection must be 'chunk' or 'global', not {selection!r}")
+        P = select_per_chunk(scores, [a for a, _ in sel], [n for _, n in sel], rho_bp)
+        # near-tie band around each selection segment's cut
         band_rows = []
-        for s in segs:
-            a, n = int(w.seg_start[s]), int(w.seg_len[s])
+        for a, n in sel:
             k = per_chunk_k(n, rho_bp)
             if 0 < k < n:
                 srt = np.sort(scores[a:a + n])[::-1]

@@ -55,13 +55,13 @@ __all__ = ["FusionPlan", "FusionStep"]
 class FusionPlan:
     """Host-side layout of one layer's step for a batch (sizes only, no scores)."""
 
-    seg_k: np.ndarray        # [n_chunks] selection budget of each chunk
-    out_start: np.ndarray    # [n_chunks] first slot of each chunk's selection in R
+    seg_k: np.ndarray        # [n_sel] selection budget of each selection segment
+    out_start: np.ndarray    # [n_sel] first slot of each segment's selection in R
     cu_R: np.ndarray         # [B+1] recomputed-row slots per request: [P_b ; U_b]
     n_P: np.ndarray          # [B] |P_b|
     R_idx_init: np.ndarray   # [|R|] cache rows; query-row slots filled, P slots -1
     R_pos_init: np.ndarray   # [|R|] positions; query-row slots filled
-    pos_base: np.ndarray     # [n_chunks] first cache row of the chunk's request
+    pos_base: np.ndarray     # [n_sel] first cache row of the segment's request
     u_idx: np.ndarray        # [n_q] cache rows of all query tokens
     u_pos: np.ndarray        # [n_q] positions N_b + i
     probe_idx: np.ndarray    # [n_probe] cache rows held by the probe buffer
@@ -75,21 +75,37 @@ class FusionPlan:
     max_R: int
     max_probe: int
     max_seg: int
+    # selection segments (per chunk, or one per request in global mode)
+    sel_start: np.ndarray    # [n_sel] first cache row
+    sel_len: np.ndarray      # [n_sel]
+    max_sel: int
 
     @staticmethod
-    def build(w, rho_bp: int) -> "FusionPlan":
+    def build(w, rho_bp: int, selection: str = "chunk") -> "FusionPlan":
+        """``selection``: "chunk" (k_i = floor(rho n_i) per chunk) or "global" (one
+        floor(rho N_b) over each request's whole context, eq. critical_mask as written)."""
         B = w.batch
-        seg_k = (int(rho_bp) * w.seg_len.astype(np.int64)) // 10000
+        if selection == "chunk":
+            sel_start, sel_len, sel_req = w.seg_start, w.seg_len, w.seg_req
+        elif selection == "global":
+            has = np.asarray(w.ctx_len) > 0
+            sel_start = np.asarray(w.cu_kv[:-1])[has]
+            sel_len = np.asarray(w.ctx_len)[has]
+            sel_req = np.nonzero(has)[0]
+        else:
+            raise ValueError(f"selection must be 'chunk' or 'global', not {selection!r}")
+        n_sel = len(sel_start)
+        seg_k = (int(rho_bp) * np.asarray(sel_len, np.int64)) // 10000
         n_P = np.zeros(B, np.int64)
-        for s in range(w.n_chunks):
-            n_P[w.seg_req[s]] += seg_k[s]
+        for s in range(n_sel):
+            n_P[sel_req[s]] += seg_k[s]
         q_lens = np.array(w.q_lens, np.int64)
         cu_R = np.concatenate([[0], np.cumsum(n_P + q_lens)])
-        out_start = np.zeros(w.n_chunks, np.int64)
+        out_start = np.zeros(n_sel, np.int64)
         fill = cu_R[:-1].copy()
-        for s in range(w.n_chunks):
-            out_start[s] = fill[w.seg_req[s]]
-            fill[w.seg_req[s]] += seg_k[s]
+        for s in range(n_sel):
+            out_start[s] = fill[sel_req[s]]
+            fill[sel_req[s]] += seg_k[s]
         R_idx = np.full(int(cu_R[-1]), -1, np.int64)
         R_pos = np.full(int(cu_R[-1]), -1, np.int64)
         u_idx, u_pos, probe_idx, probe_pos, cu_probe = [], [], [], [], [0]
@@ -115,7 +131,7 @@ class FusionPlan:
             query_slot.append(cu_probe[-1] + arows.size + np.arange(nq))
             cu_probe.append(cu_probe[-1] + arows.size + nq)
         cat = lambda xs: np.concatenate(xs).astype(np.int32) if xs else np.zeros(0, np.int32)
-        pos_base = w.cu_kv[w.seg_req].astype(np.int32)
+        pos_base = np.asarray(w.cu_kv)[np.asarray(sel_req, np.int64)].astype(np.int32)
         return FusionPlan(
             seg_k=seg_k.astype(np.int32), out_start=out_start.astype(np.int32),
             cu_R=cu_R.astype(np.int32), n_P=n_P, R_idx_init=R_idx.astype(np.int32),
@@ -126,7 +142,9 @@ class FusionPlan:
             max_ctx=int(w.ctx_len.max() if B else 0),
             max_R=int(np.diff(cu_R).max() if B else 0),
             max_probe=int(np.diff(cu_probe).max() if B else 0),
-            max_seg=int(w.seg_len.max() if w.n_chunks else 0))
+            max_seg=int(w.seg_len.max() if w.n_chunks else 0),
+            sel_start=np.asarray(sel_start, np.int32), sel_len=np.asarray(sel_len, np.int32),
+            max_sel=int(max(sel_len) if n_sel else 0))
 
 
 def kv_buffer(rows, hkv, d, dtype, device, zero=False):
@@ -145,11 +163,13 @@ class FusionStep:
     rows, so ``run()`` can be repeated with identical results.
     """
 
-    def __init__(self, w, rho_bp: int | None = None, device="cuda", fused: bool = False):
+    def __init__(self, w, rho_bp: int | None = None, device="cuda", fused: bool = False,
+                 selection: str = "chunk"):
         self.w = w
         self.fused = bool(fused)
+        self.selection = selection
         self.rho_bp = w.rho_bp if rho_bp is None else int(rho_bp)
-        self.plan = p = FusionPlan.build(w, self.rho_bp)
+        self.plan = p = FusionPlan.build(w, self.rho_bp, selection)
         dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.dtype = dt
         dev = torch.device(device)
@@ -167,6 +187,7 @@ class FusionStep:
         # layout (int32)
         self.seg_start, self.seg_len, self.seg_delta = t(w.seg_start), t(w.seg_len), t(w.seg_delta)
         self.seg_k, self.out_start, self.pos_base = t(p.seg_k), t(p.out_start), t(p.pos_base)
+        self.sel_start, self.sel_len = t(p.sel_start), t(p.sel_len)
         self.cu_kv, self.ctx_len, self.cu_q = t(w.cu_kv), t(w.ctx_len), t(w.cu_q)
         self.cu_R, self.cu_probe = t(p.cu_R), t(p.cu_probe)
         self.u_idx, self.u_pos = t(p.u_idx), t(p.u_pos)
@@ -283,8 +304,8 @@ class FusionStep:
 
     def stage_select(self):
         p = self.plan
-        self._call("select", qcf.qcf_select_topk, self.R_idx, self.scores, self.seg_start,
-                   self.seg_len, self.seg_k, self.out_start, p.max_seg, out_pos=self.R_pos,
+        self._call("select", qcf.qcf_select_topk, self.R_idx, self.scores, self.sel_start,
+                   self.sel_len, self.seg_k, self.out_start, p.max_sel, out_pos=self.R_pos,
                    pos_base=self.pos_base)
 
     def stage_scatter(self):

@@ -54,13 +54,19 @@ def assert_scores(got, want, what="scores"):
     assert not bad.any(), f"{what}: {bad.sum()} entries off, worst {np.max(np.abs(got - want)):.3g}"
 
 
-def check_selection(w, P_gpu, scores_orc, P_orc):
-    """Per chunk: same count; swapped rows only across near-ties (gap < 1e-3)."""
+def selection_segments(w, selection="chunk"):
+    """(first row, length) of every selection segment: the chunks, or each request's context."""
+    if selection == "global":
+        return [(int(w.cu_kv[b]), int(w.ctx_len[b])) for b in range(w.batch) if w.ctx_len[b] > 0]
+    return [(int(w.seg_start[s]), int(w.seg_len[s])) for s in range(w.n_chunks)]
+
+
+def check_selection(w, P_gpu, scores_orc, P_orc, selection="chunk"):
+    """Per selection segment: same count; swapped rows only across near-ties (gap < 1e-3)."""
     Pg = np.sort(np.concatenate(P_gpu)) if len(P_gpu) else np.zeros(0, int)
     Po = np.sort(np.concatenate(P_orc)) if len(P_orc) else np.zeros(0, int)
     swaps = 0
-    for s in range(w.n_chunks):
-        a, n = int(w.seg_start[s]), int(w.seg_len[s])
+    for s, (a, n) in enumerate(selection_segments(w, selection)):
         g = Pg[(Pg >= a) & (Pg < a + n)]
         o = Po[(Po >= a) & (Po < a + n)]
         assert g.size == o.size, f"chunk {s}: {g.size} selected, oracle {o.size}"
@@ -74,7 +80,7 @@ def check_selection(w, P_gpu, scores_orc, P_orc):
     return swaps
 
 
-def check_step(w, g, o, sampled=False):
+def check_step(w, g, o, sampled=False, selection="chunk"):
     """Compare a GPU step (``FusionStep.results()``) with the oracle's ``fusion_step``."""
     dt = w.dtype
     report = {}
@@ -84,7 +90,7 @@ def check_step(w, g, o, sampled=False):
         ctx[w.seg_start[s]:w.seg_start[s] + w.seg_len[s]] = True
     assert_scores(g["scores"][ctx], o["scores"][ctx])
     # selection
-    report["swaps"] = check_selection(w, g["P"], o["scores"], o["P"])
+    report["swaps"] = check_selection(w, g["P"], o["scores"], o["P"], selection)
     # R layout: per request, P ascending then the query rows
     for b in range(w.batch):
         Rg = g["R"][g["cu_R"][b]:g["cu_R"][b + 1]] if "cu_R" in g else None

@@ -224,9 +224,14 @@ def test_scatter_kv(dtype, hq, hkv, d):
 
 
 @pytest.mark.parametrize("lens,ks", [
-    ([512, 511, 1, 1024, 700], [153, 0, 1, 1024, 699]),
-    ([20000], [6000]),                      # one big segment: global top-k, global-memory path
-    ([8192, 8193], [2457, 100]),
+    ([512, 511, 1, 1024, 700], [153, 0, 1, 1024, 699]),      # per chunk, 256 x 4 slots
+    ([4096, 3000, 17], [1228, 3000, 16]),                     # 256 x 16
+    ([8192, 8191], [2457, 1]),                                # 512 x 16
+    ([16384, 9000], [4915, 8999]),                            # 1024 x 16
+    ([20000], [6000]),                                        # global top-k of one request, 1024 x 32
+    ([32768, 31000], [9830, 31000]),                          # 1024 x 32, k = n
+    ([65536, 40000], [19660, 1]),                             # 1024 x 64
+    ([70000, 300], [21000, 90]),                              # longer than the register path
 ])
 def test_select_topk_exact(lens, ks):
     say("topk", lens, ks)
@@ -249,6 +254,17 @@ def test_select_topk_exact(lens, ks):
     want = np.concatenate([a + Q.select_topk(s[a:a + n_], k) for a, n_, k in zip(starts, lens, ks)])
     np.testing.assert_array_equal(got, want)
     np.testing.assert_array_equal(pos.cpu().numpy(), want - 3)
+
+
+@pytest.mark.parametrize("n,k", [(32768, 9830), (65536, 1), (5000, 4999)])
+def test_select_topk_all_equal(n, k):
+    """Every score equal: the k lowest rows, in order (the tie rule alone decides)."""
+    say("topk all equal", n, k)
+    s = torch.full((n,), 0.5, device="cuda")
+    out = torch.full((k,), -7, dtype=torch.int32, device="cuda")
+    one = lambda v: dev(np.array([v], np.int32))
+    qcf.qcf_select_topk(out, s, one(0), one(n), one(k), one(0), n)
+    np.testing.assert_array_equal(out.cpu().numpy(), np.arange(k))
 
 
 @pytest.mark.parametrize("dtype,nqs,ctxs,hq,hkv,d", [

@@ -134,3 +134,26 @@ def test_fused_scores_flow_matches_unfused(name, dtype):
     for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u", "q_R"):
         np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)
     assert torch.equal(a.k_probe, b.k_probe) and torch.equal(a.v_probe, b.v_probe)
+
+
+@pytest.mark.parametrize("name,kw,rho_bp", [
+    ("c2", {}, None),                                                   # one 5120-token context
+    ("c5", {}, None),                                                   # 16 requests, up to ~16K each
+    ("c2", dict(chunk_lens=[[300, 212], [64], [129, 1, 511, 40]], q_lens=[5, 64, 17],
+                anchors_per_chunk=3, dtype="f32"), 2500),
+])
+def test_global_selection(name, kw, rho_bp):
+    """Global mode: floor(rho N_b) rows over each request's whole context (one top-k segment
+    per request), against the oracle's global selection."""
+    w = make_workload(name, **kw)
+    say(w.name, w.dtype, "global selection, rows", w.n_rows, "requests", w.batch)
+    step = FusionStep(w, rho_bp, selection="global")
+    step.run()
+    g = step.results()
+    big = w.n_rows > 20000
+    o = oracle.fusion_step(w, rho_bp=rho_bp, attn_rows=6 if big else None, band_attention=not big,
+                           selection="global")
+    rep = check_step(w, g, o, sampled=big, selection="global")
+    say("  ", rep)
+    for b in range(w.batch):
+        assert len(g["P"][b]) == ((rho_bp or w.rho_bp) * int(w.ctx_len[b])) // 10000

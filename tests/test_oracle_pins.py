@@ -239,6 +239,24 @@ def test_per_chunk_counts_and_endpoints():
     np.testing.assert_array_equal(Q.select_per_chunk(s, [0], [300], 2500), brute_topk(list(s), 75))
 
 
+def test_global_selection_mode():
+    """selection="global" takes floor(rho N_b) rows over each request's whole context (eq.
+    critical_mask as written): a brute-force stable sort of the request's scores; with one
+    chunk per request it is the per-chunk selection."""
+    w = make_workload("c2", chunk_lens=[[100, 37, 60], [80]], q_lens=[5, 3], anchors_per_chunk=3,
+                      dtype="f32")
+    o = Q.fusion_step(w, rho_bp=2500, selection="global")
+    c = Q.fusion_step(w, rho_bp=2500)
+    for b in range(w.batch):
+        base, N = int(w.cu_kv[b]), int(w.ctx_len[b])
+        sc = list(o["scores"][base:base + N])
+        want = np.array(brute_topk(sc, (2500 * N) // 10000)) + base
+        np.testing.assert_array_equal(o["P"][b], want)
+    assert o["P"][0].size == (2500 * 197) // 10000 == 49              # 25 + 9 + 15 = 49 per chunk too
+    np.testing.assert_array_equal(o["P"][1], c["P"][1])                # a one-chunk request
+    np.testing.assert_array_equal(o["scores"], c["scores"])            # selection does not touch scores
+
+
 # ---------------------------------------------------------------- the fusion step
 def _full_prefill(w):
     """Dense causal attention of every row over fresh rotated K/V (independent formulation)."""

@@ -235,6 +235,50 @@ def anchor_profile(args):
         "all_layers_recall": r_all, "all_layers_select_ms": t_all}), flush=True)
 
 
+def rerope_rate(steps, hkv, d, reps=40):
+    """qcf_rerope (keys re-positioned, values stitched) alone: HIP events around back-to-back
+    calls, (a) on the step's own context, cycling through the buffer sets, and (b) on a
+    32 x 1024-token context whose 268 MB per call cannot stay in the 256 MB last-level cache.
+    Algorithmic bytes: each context row's K and V read once and written once."""
+    import torch
+    from paper_2606_05875_amd import qcf
+    from paper_2606_05875_amd.step import kv_buffer
+
+    def timed(calls):
+        for c in calls[:4]:
+            c()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for i in range(reps):
+            calls[i % len(calls)]()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+
+    out = {}
+    ctx = int(steps[0].w.ctx_len.sum())
+    t = timed([st.stage_rerope for st in steps])
+    nbytes = 4 * ctx * hkv * d * 2
+    out["step_context"] = {"rows": ctx, "bytes_per_call": nbytes, "us_per_call": t * 1e6,
+                           "GBs": nbytes / t / 1e9, "hbm_frac": nbytes / t / 1e9 / PEAK_HBM_GBS}
+    n_seg, seg = 32, 1024
+    T = n_seg * seg
+    dev = steps[0].device
+    k_in = (torch.randn((T, hkv * d), device=dev) * 0.1).to(torch.bfloat16).view(T, hkv, d)
+    v_in = torch.randn_like(k_in)
+    k_out, v_out = kv_buffer(T, hkv, d, torch.bfloat16, dev), kv_buffer(T, hkv, d, torch.bfloat16, dev)
+    i32 = lambda a: torch.tensor(a, dtype=torch.int32, device=dev)
+    starts = i32([s * seg for s in range(n_seg)])
+    call = qcf.prepare(qcf.qcf_rerope, k_out, k_in, starts, i32([seg] * n_seg), starts, seg, 5e5,
+                       v_out=v_out, v_in=v_in)
+    t = timed([call])
+    nbytes = 4 * T * hkv * d * 2
+    out["context_32x1024"] = {"rows": T, "bytes_per_call": nbytes, "us_per_call": t * 1e6,
+                              "GBs": nbytes / t / 1e9, "hbm_frac": nbytes / t / 1e9 / PEAK_HBM_GBS}
+    return out
+
+
 def topk_study(args):
     """qcf_select_topk alone: per-chunk selection and global (one segment per request)
     selection on the contexts of the workloads, HIP events around 200 back-to-back calls."""
@@ -403,6 +447,7 @@ def main():
         torch.cuda.synchronize()
         stage_ms[name] = a.elapsed_time(b) / reps
     asm_gbs = assemble_bytes(first) / (stage_ms["assemble"] * 1e-3) / 1e9
+    rerope = rerope_rate(steps, w.n_kv_heads, w.head_dim)
 
     out = {
         "metric": "selected-token fused-prefill tokens/s per layer",
@@ -430,6 +475,7 @@ def main():
         "stage_ms": stage_ms,
         "assemble_GBs": asm_gbs,
         "assemble_hbm_frac": asm_gbs / PEAK_HBM_GBS,
+        "rerope_hbm": rerope,
     }
 
     if not args.no_cpu:

@@ -13,84 +13,13 @@
 // block (constant per chunk) or once per row.
 #include "qcf_device.h"
 #include "qcf_launch.h"
+#include "qcf_remap.h"
 
 namespace qcf {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kUnits = 4;  // 16-byte units per thread per pass
-
-// rotate `nrows` rows (src rows s0.., dst rows d0..) of hkv heads by the angle
-// table cs; rows outside the bounds are skipped; V is copied alongside when
-// vdst is set.  A round covers kUnits key units (rotate-half pairs) and
-// 2 kUnits value units per thread; all of its loads are issued, unmasked from
-// clamped rows, before its first store (a load under a lane condition gets a
-// wait of its own, which would serialise the round trips).
-template <typename T, int D>
-__device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride, const T* ksrc,
-                                           const T* vsrc, int64_t src_stride, int64_t s0,
-                                           int64_t d0, int nrows, int hkv, int64_t n_src,
-                                           int64_t n_dst, const float2* cs) {
-  constexpr int HALF = D / 2;
-  constexpr int VEC = Vec16<T>::N;
-  constexpr int UPH = HALF / VEC;
-  const int upr = hkv * UPH;           // key units per row (rotate-half pairs)
-  const int vpr = 2 * upr;             // value units per row
-  const int64_t s_hi = n_src - 1;
-  const int total_k = nrows * upr, total_v = vdst ? nrows * vpr : 0;
-  for (int kb = 0, vb = 0; kb < total_k || vb < total_v;
-       kb += kThreads * kUnits, vb += 2 * kThreads * kUnits) {
-    uint4 a[kUnits], b[kUnits], va[2 * kUnits];
-    int64_t kofs[kUnits], vofs[2 * kUnits];
-    int jj[kUnits];
-    bool kok[kUnits], vok[2 * kUnits];
-#pragma unroll
-    for (int k = 0; k < kUnits; ++k) {
-      const int u = kb + threadIdx.x + k * kThreads;
-      const int uc = min(u, max(total_k - 1, 0));
-      const int r = uc / upr, c = uc - r * upr;
-      const int h = c / UPH;
-      const int64_t s = s0 + r, d = d0 + r;
-      kok[k] = u < total_k && s >= 0 && s < n_src && d >= 0 && d < n_dst;
-      jj[k] = (c - h * UPH) * VEC;
-      const int64_t so = min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)h * D + jj[k];
-      kofs[k] = d * dst_stride + (int64_t)h * D + jj[k];
-      a[k] = ld16(ksrc + so);
-      b[k] = ld16(ksrc + so + HALF);
-    }
-    if (vdst) {
-#pragma unroll
-      for (int k = 0; k < 2 * kUnits; ++k) {
-        const int u = vb + threadIdx.x + k * kThreads;
-        const int uc = min(u, max(total_v - 1, 0));
-        const int r = uc / vpr, c = uc - r * vpr;
-        const int64_t s = s0 + r, d = d0 + r;
-        vok[k] = u < total_v && s >= 0 && s < n_src && d >= 0 && d < n_dst;
-        vofs[k] = d * dst_stride + (int64_t)c * VEC;
-        va[k] = ld16(vsrc + min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)c * VEC);
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < kUnits; ++k) {
-      float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
-      Vec16<T>::unpack(a[k], x1);
-      Vec16<T>::unpack(b[k], x2);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        rope_pair(x1[e], x2[e], cs[jj[k] + e], y1[e], y2[e]);
-      }
-      if (kok[k]) {
-        st16(kdst + kofs[k], Vec16<T>::pack(y1));
-        st16(kdst + kofs[k] + HALF, Vec16<T>::pack(y2));
-      }
-    }
-    if (vdst) {
-#pragma unroll
-      for (int k = 0; k < 2 * kUnits; ++k)
-        if (vok[k]) st16(vdst + vofs[k], va[k]);
-    }
-  }
-}
 
 template <typename T, int D>
 struct AssembleArgs {
@@ -130,10 +59,13 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     if (r0 >= len) return;
     const int64_t d0 = (int64_t)A.seg_start[s] + r0;
     const int64_t s0 = (A.src_start ? (int64_t)A.src_start[s] : (int64_t)A.seg_start[s]) + r0;
+    // the angle table first: forming it while this kernel's loads are in flight
+    // holds them across the float64 work and costs occupancy (measured slower)
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.seg_delta[s], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D>(A.k_cache, A.v_cache, A.row_stride, A.k_pic, A.v_pic, A.pic_stride, s0, d0,
-                     min(A.rows_per_block, len - r0), A.hkv, A.n_pic_rows, A.n_rows, cs);
+    remap_rows<T, D, kThreads, kUnits>(A.k_cache, A.v_cache, A.row_stride, A.k_pic, A.v_pic,
+                                       A.pic_stride, s0, d0, min(A.rows_per_block, len - r0),
+                                       A.hkv, A.n_pic_rows, A.n_rows, cs, [] {});
     return;
   }
   if (bid < n_remap + A.n_query) {
@@ -146,11 +78,11 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     const int64_t slot = A.query_slot ? (int64_t)A.query_slot[i] : -1;
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.query_pos[i], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D>(A.k_cache, A.v_cache, A.row_stride, A.k_new, A.v_new, kvw, src, row, 1, A.hkv,
-                     A.n_src_rows, A.n_rows, cs);
+    remap_rows<T, D, kThreads, kUnits>(A.k_cache, A.v_cache, A.row_stride, A.k_new, A.v_new, kvw,
+                                       src, row, 1, A.hkv, A.n_src_rows, A.n_rows, cs, [] {});
     if (slot >= 0)
-      remap_rows<T, D>(A.probe_k, A.probe_v, A.probe_stride, A.k_new, A.v_new, kvw, src, slot, 1, A.hkv,
-                       A.n_src_rows, A.n_probe, cs);
+      remap_rows<T, D, kThreads, kUnits>(A.probe_k, A.probe_v, A.probe_stride, A.k_new, A.v_new, kvw,
+                                         src, slot, 1, A.hkv, A.n_src_rows, A.n_probe, cs, [] {});
     // q: hq heads rotated into q_u[i]
     constexpr int VEC = Vec16<T>::N;
     constexpr int UPH = HALF / VEC;
@@ -176,12 +108,13 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     const int64_t p = p0 + pr;
     if (p >= A.n_probe) break;
     const int64_t src = A.probe_src[p];
-    __syncthreads();  // previous row's angle table is no longer read
+    if (pr > 0) __syncthreads();  // the previous row's angle table is no longer read
     if (src < 0) continue;  // a query slot (written by that query row's block)
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.probe_delta[p], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D>(A.probe_k, A.probe_v, A.probe_stride, A.k_pic, A.v_pic, A.pic_stride, src, p, 1, A.hkv,
-                     A.n_pic_rows, A.n_probe, cs);
+    remap_rows<T, D, kThreads, kUnits>(A.probe_k, A.probe_v, A.probe_stride, A.k_pic, A.v_pic,
+                                       A.pic_stride, src, p, 1, A.hkv, A.n_pic_rows, A.n_probe, cs,
+                                       [] {});
   }
 }
 

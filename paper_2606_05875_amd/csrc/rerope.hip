@@ -4,19 +4,20 @@
 // A stored chunk key is rotated at its chunk-local position; moving the chunk
 // to request offset o_i is one more rotation by o_i, and its values are copied
 // in the same token order.  The rotation is the same for every row of a chunk,
-// so a block works inside one chunk: its first threads form the chunk's d/2
-// (cos, sin) pairs once (float64 angle), and every thread then streams 16-byte
-// vectors of the rotate-half pairs (j .. j+v, j+d/2 .. j+d/2+v) of one head of
-// one row, then 16-byte vectors of the value rows.  HBM-bound: every byte is
-// read once and written once with coalesced 16-byte accesses.
+// so a block works inside one chunk: every thread issues its 16-byte loads of
+// rotate-half pairs (j .. j+v, j+d/2 .. j+d/2+v) of one head of one row and of
+// the value rows, the block forms the chunk's d/2 (cos, sin) pairs (float64
+// angle) while they are in flight, then rotates and stores.  HBM-bound: every
+// byte is read once and written once with coalesced 16-byte accesses.
 #include "qcf_device.h"
 #include "qcf_launch.h"
+#include "qcf_remap.h"
 
 namespace qcf {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnitsPerThread = 4;  // (row, head, j-vector) units each thread owns
+constexpr int kUnitsPerThread = 4;  // key units (rotate-half pairs) per thread per round
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void rerope_kernel(
@@ -26,8 +27,6 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
     const int32_t* __restrict__ seg_len, const int32_t* __restrict__ seg_delta,
     const int32_t* __restrict__ src_start, double theta) {
   constexpr int HALF = D / 2;
-  constexpr int VEC = Vec16<T>::N;
-  constexpr int UPH = HALF / VEC;  // key units per head
   __shared__ float2 cs[HALF];
 
   const int s = blockIdx.y;
@@ -36,80 +35,14 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
   if (r0 >= len) return;
   const int64_t dst0 = (int64_t)seg_start[s] + r0;
   const int64_t src0 = (src_start ? (int64_t)src_start[s] : (int64_t)seg_start[s]) + r0;
-  if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)seg_delta[s], threadIdx.x, D, theta);
-  __syncthreads();
-
-  const int rows = min(rows_per_block, len - r0);
-  const int units_per_row = hkv * UPH;
-  const int total = rows * units_per_row;
-
-  // Loads of all owned units are issued before any store: in-place calls
-  // (k_out == k_in, src == dst) stay correct because every unit is read and
-  // written by the same thread.
-  for (int base = 0; base < total; base += kThreads * kUnitsPerThread) {
-    uint4 lo[kUnitsPerThread], hi[kUnitsPerThread];
-    int64_t off_in[kUnitsPerThread], off_out[kUnitsPerThread];
-    int jj[kUnitsPerThread];
-#pragma unroll
-    for (int k = 0; k < kUnitsPerThread; ++k) {
-      const int u = base + threadIdx.x + k * kThreads;
-      off_in[k] = -1;
-      jj[k] = 0;
-      if (u < total) {
-        const int rr = u / units_per_row;
-        const int c = u - rr * units_per_row;
-        const int h = c / UPH;
-        jj[k] = (c - h * UPH) * VEC;
-        const int64_t src = src0 + rr, dst = dst0 + rr;
-        if (src >= 0 && src < n_in_rows && dst >= 0 && dst < n_out_rows) {
-          const int64_t in_head = (int64_t)h * D + jj[k];
-          off_in[k] = src * in_stride + in_head;
-          off_out[k] = dst * out_stride + in_head;
-          lo[k] = ld16(k_in + off_in[k]);
-          hi[k] = ld16(k_in + off_in[k] + HALF);
-        }
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < kUnitsPerThread; ++k) {
-      if (off_in[k] < 0) continue;
-      float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
-      Vec16<T>::unpack(lo[k], x1);
-      Vec16<T>::unpack(hi[k], x2);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        rope_pair(x1[e], x2[e], cs[jj[k] + e], y1[e], y2[e]);
-      }
-      st16(k_out + off_out[k], Vec16<T>::pack(y1));
-      st16(k_out + off_out[k] + HALF, Vec16<T>::pack(y2));
-    }
-  }
-  // values: stitched unchanged, in the same token order
-  if (v_out == nullptr || v_out == v_in) return;
-  const int vchunks = hkv * D / VEC;
-  const int vtotal = rows * vchunks;
-  for (int base = 0; base < vtotal; base += kThreads * kUnitsPerThread) {
-    uint4 buf[kUnitsPerThread];
-    int64_t oi[kUnitsPerThread], oo[kUnitsPerThread];
-#pragma unroll
-    for (int k = 0; k < kUnitsPerThread; ++k) {
-      const int u = base + threadIdx.x + k * kThreads;
-      oi[k] = -1;
-      if (u < vtotal) {
-        const int rr = u / vchunks;
-        const int c = u - rr * vchunks;
-        const int64_t src = src0 + rr, dst = dst0 + rr;
-        if (src >= 0 && src < n_in_rows && dst >= 0 && dst < n_out_rows) {
-          oi[k] = src * in_stride + (int64_t)c * VEC;
-          oo[k] = dst * out_stride + (int64_t)c * VEC;
-          buf[k] = ld16(v_in + oi[k]);
-        }
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < kUnitsPerThread; ++k)
-      if (oi[k] >= 0) st16(v_out + oo[k], buf[k]);
-  }
+  // values are stitched unchanged, in the same token order (nothing to do in place)
+  T* vdst = (v_out == nullptr || v_out == v_in) ? nullptr : v_out;
+  remap_rows<T, D, kThreads, kUnitsPerThread>(
+      k_out, vdst, out_stride, k_in, v_in, in_stride, src0, dst0, min(rows_per_block, len - r0),
+      hkv, n_in_rows, n_out_rows, cs, [&] {
+        if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)seg_delta[s], threadIdx.x, D, theta);
+        __syncthreads();
+      });
 }
 
 template <typename T, int D>

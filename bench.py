@@ -74,6 +74,14 @@ def assemble_bytes(step):
     return 4.0 * kv * n_ctx + n_q * (2 * qb + 6 * kv) + 4.0 * kv * n_anchor
 
 
+def scatter_bytes(step):
+    """Fresh rows of R: q, k, v read, rotated q and k plus v written."""
+    w = step.w
+    n = int(step.R_idx.numel())
+    es = step.k.element_size()
+    return n * (2 * w.n_q_heads + 4 * w.n_kv_heads) * w.head_dim * es
+
+
 def probe_attn_flops(step):
     w, p = step.w, step.plan
     tot = 0.0
@@ -238,7 +246,8 @@ def anchor_profile(args):
 def rerope_rate(steps, hkv, d, reps=40):
     """qcf_rerope (keys re-positioned, values stitched) alone: HIP events around back-to-back
     calls, (a) on the step's own context, cycling through the buffer sets, and (b) on a
-    32 x 1024-token context whose 268 MB per call cannot stay in the 256 MB last-level cache.
+    32 x 1024-token context (268 MB per call, three sets cycled so that no call finds its inputs
+    in the 256 MB last-level cache).
     Algorithmic bytes: each context row's K and V read once and written once."""
     import torch
     from paper_2606_05875_amd import qcf
@@ -265,18 +274,70 @@ def rerope_rate(steps, hkv, d, reps=40):
     n_seg, seg = 32, 1024
     T = n_seg * seg
     dev = steps[0].device
-    k_in = (torch.randn((T, hkv * d), device=dev) * 0.1).to(torch.bfloat16).view(T, hkv, d)
-    v_in = torch.randn_like(k_in)
-    k_out, v_out = kv_buffer(T, hkv, d, torch.bfloat16, dev), kv_buffer(T, hkv, d, torch.bfloat16, dev)
     i32 = lambda a: torch.tensor(a, dtype=torch.int32, device=dev)
-    starts = i32([s * seg for s in range(n_seg)])
-    call = qcf.prepare(qcf.qcf_rerope, k_out, k_in, starts, i32([seg] * n_seg), starts, seg, 5e5,
-                       v_out=v_out, v_in=v_in)
-    t = timed([call])
+    starts, lens = i32([s * seg for s in range(n_seg)]), i32([seg] * n_seg)
+    calls = []
+    for _ in range(3):  # three sets (~800 MB): a call never finds its inputs still cached
+        k_in = (torch.randn((T, hkv * d), device=dev) * 0.1).to(torch.bfloat16).view(T, hkv, d)
+        v_in = torch.randn_like(k_in)
+        k_out = kv_buffer(T, hkv, d, torch.bfloat16, dev)
+        v_out = kv_buffer(T, hkv, d, torch.bfloat16, dev)
+        calls.append(qcf.prepare(qcf.qcf_rerope, k_out, k_in, starts, lens, starts, seg, 5e5,
+                                 v_out=v_out, v_in=v_in))
+    t = timed(calls)
     nbytes = 4 * T * hkv * d * 2
     out["context_32x1024"] = {"rows": T, "bytes_per_call": nbytes, "us_per_call": t * 1e6,
                               "GBs": nbytes / t / 1e9, "hbm_frac": nbytes / t / 1e9 / PEAK_HBM_GBS}
     return out
+
+
+def memory_study(args):
+    """The HBM-bound kernels alone on the c2 step (a few buffer sets cycled): qcf_assemble,
+    qcf_rerope, qcf_scatter_kv; plus qcf_rerope on a 32 x 1024-token context.  One JSON line
+    (events around back-to-back calls); run it under rocprofv3 for kernel durations."""
+    import torch
+    from paper_2606_05875_amd.step import FusionStep
+    from paper_2606_05875_amd.workloads import make_workload
+
+    torch.cuda.set_device(0)
+    w = make_workload("c2")
+    steps = [FusionStep(w) for _ in range(5)]
+    for st in steps:
+        st.run()
+    torch.cuda.synchronize()
+    out = {"study": "HBM-bound kernels", "workload": "c2: " + w.meta["desc"]}
+    for name, nbytes in (("assemble", assemble_bytes(steps[0])),
+                         ("scatter", scatter_bytes(steps[0]))):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(args.steps):
+            getattr(steps[i % len(steps)], "stage_" + name)()
+        b.record()
+        torch.cuda.synchronize()
+        t = a.elapsed_time(b) / args.steps * 1e-3
+        out[name] = {"bytes_per_call": nbytes, "us_per_call": t * 1e6, "GBs": nbytes / t / 1e9,
+                     "hbm_frac": nbytes / t / 1e9 / PEAK_HBM_GBS}
+    out["rerope"] = rerope_rate(steps, w.n_kv_heads, w.head_dim, reps=args.steps)
+    # for scale: a plain device copy with the long-context re-position's bytes (134 MB each way)
+    pairs = []
+    for _ in range(3):  # three sets, as for the re-position
+        src = torch.empty(32 * 1024 * w.n_kv_heads * w.head_dim, dtype=torch.float32, device="cuda")
+        src.uniform_()
+        pairs.append((src, torch.empty_like(src)))
+    for i in range(4):
+        pairs[i % 3][1].copy_(pairs[i % 3][0])
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for i in range(args.steps):
+        pairs[i % 3][1].copy_(pairs[i % 3][0])
+    b.record()
+    torch.cuda.synchronize()
+    t = a.elapsed_time(b) / args.steps * 1e-3
+    nbytes = 2 * pairs[0][0].numel() * 4
+    out["device_copy"] = {"bytes_per_call": nbytes, "us_per_call": t * 1e6, "GBs": nbytes / t / 1e9,
+                          "hbm_frac": nbytes / t / 1e9 / PEAK_HBM_GBS}
+    print(json.dumps(out), flush=True)
 
 
 def topk_study(args):
@@ -337,6 +398,9 @@ def main():
                     help="with --stack: the stored chunk caches stream layer by layer from pinned host "
                          "memory (copy-only, compute-only and overlapped times)")
     ap.add_argument("--slots", type=int, default=3, help="with --pipeline: device staging slots")
+    ap.add_argument("--memory-study", action="store_true",
+                    help="the HBM-bound kernels alone (assemble, rerope, scatter on c2; rerope on a "
+                         "32 x 1024-token context), one JSON line; not the headline metric")
     ap.add_argument("--topk-study", action="store_true",
                     help="time qcf_select_topk alone, per-chunk vs global selection, on the c2/c4/c5 "
                          "contexts (one JSON line; not the headline metric)")
@@ -362,6 +426,8 @@ def main():
         return
     if args.topk_study:
         return topk_study(args)
+    if args.memory_study:
+        return memory_study(args)
     if args.stack:
         if args.anchor_profile:
             return anchor_profile(args)

@@ -126,6 +126,39 @@ def stack_study(args):
                          P=np.concatenate(out["P"]), n_R=int(out["R"].size))
         del st
         torch.cuda.empty_cache()
+    # recompute-ratio sweep on the compact view (the PIC caches and inputs shared); 100% is a
+    # full prefill of every token through the same kernels
+    sweep = {}
+    base = FusionStack(sw)
+    base.build_pic()
+    for rho in (1500, 3000, 5000, 10000):
+        st = FusionStack(sw, rho_bp=rho, share=base)
+        for _ in range(max(1, args.warmup)):
+            st.run()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        t_sel, t_rec = [], []
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            ev[0].record()
+            st.select()
+            ev[1].record()
+            st.recompute()
+            ev[2].record()
+            torch.cuda.synchronize()
+            t_sel.append(ev[0].elapsed_time(ev[1]))
+            t_rec.append(ev[1].elapsed_time(ev[2]))
+        n_R = int(st.R_idx.numel())
+        sel, rec = float(np.median(t_sel)), float(np.median(t_rec))
+        sweep[rho] = dict(recomputed_rows=n_R, select_ms=sel, recompute_ms=rec,
+                          tokens_per_s=n_R * sw.n_layers / ((sel + rec) * 1e-3))
+        del st
+    # full prefill = every token through every layer with no selection: the 100% recompute
+    full = sweep[10000]["recompute_ms"]
+    for rho, r in sweep.items():
+        if rho != 10000:
+            r["speedup_vs_full_prefill"] = full / (r["select_ms"] + r["recompute_ms"])
+    del base
+    torch.cuda.empty_cache()
     a, f = res["anchors"], res["full"]
     overlap = np.intersect1d(a["P"], f["P"]).size / max(f["P"].size, 1)
     L = sw.n_layers
@@ -139,7 +172,9 @@ def stack_study(args):
         "select_ms": {"anchors_critical_layers": a["select_ms"], "full_view_all_layers": f["select_ms"]},
         "recompute_ms": a["recompute_ms"],
         "select_speedup": f["select_ms"] / a["select_ms"],
-        "P_overlap_with_full_view": overlap}), flush=True)
+        "P_overlap_with_full_view": overlap,
+        "ratio_sweep": {f"{rho / 100:g}%": r for rho, r in sweep.items()},
+        "full_prefill_ms": full}), flush=True)
 
 
 def pipeline_study(args):

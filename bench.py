@@ -526,7 +526,8 @@ def main():
         ev[i][1].record()
         s.join()
     torch.cuda.synchronize()
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    attn_all = np.array([a.elapsed_time(b) for a, b in ev])
+    attn_ms = float(np.mean(attn_all))
 
     R_pos = first.R_pos.cpu().numpy()
     n_R = int(R_pos.size)
@@ -571,8 +572,15 @@ def main():
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(int(first.k.stride(0))) if args.config == "c2" else None,
                      "traffic_unit": "bytes per launch (HBM, calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE)",
-                     "flops_per_launch": flops, "avg_launch_ms": attn_ms},
+                     "flops_per_launch": flops, "avg_launch_ms": attn_ms,
+                     "launch_ms_p10_p50_p90": [float(np.percentile(attn_all, q)) for q in (10, 50, 90)]},
         "ms_per_step_fused_scores_flow": ms_step_fused,
+        # the step split as fusion kernels (re-position, fresh-row scatter, row attention) and
+        # selector (probe attention, scores, top-k), from the per-stage timings below
+        "fusion_kernels_ms": stage_ms["rerope"] + stage_ms["scatter"] + stage_ms["attn"],
+        "fusion_kernels_tokens_per_s": n_R / ((stage_ms["rerope"] + stage_ms["scatter"]
+                                               + stage_ms["attn"]) * 1e-3),
+        "selector_ms": stage_ms["probe_attn"] + stage_ms["scores"] + stage_ms["select"],
         "stage_ms": stage_ms,
         "assemble_GBs": asm_gbs,
         "assemble_hbm_frac": asm_gbs / PEAK_HBM_GBS,
@@ -582,6 +590,17 @@ def main():
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_baseline(w, budget_s):
@@ -605,7 +624,8 @@ def cpu_baseline(w, budget_s):
     sec = float(np.median(times))
     return {"value": n_R / sec, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{len(times)} whole oracle steps of the same workload ({sec:.2f} s each, median)",
-            "host_cpus": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+            "host_cpus": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+            "cpu_model": _cpu_model()}
 
 
 if __name__ == "__main__":

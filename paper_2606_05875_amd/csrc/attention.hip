@@ -391,6 +391,11 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
 // last segment) that attn_stream_merge_kernel combines.
 constexpr int kMaxStreamTiles = 256;  // row tiles (requests x tiles) of a stream-mode call
 constexpr int kStreamBlocks = 256;    // persistent blocks (one per CU of MI355X)
+// stream-mode plan in the workspace (int32): step prefix sums [0, kMaxStreamTiles],
+// key ends, then the first cost-line unit of every block of a head [0, nbg]
+constexpr int kPlanEndOff = kMaxStreamTiles + 1;
+constexpr int kPlanBndOff = 2 * kMaxStreamTiles + 1;
+constexpr int kPlanInts = kPlanBndOff + kStreamBlocks + 1;
 // Start-up cost of a segment (row positions, Q and the first key tiles in
 // flight before the first product, plus its output stores), in key steps:
 // each row tile counts as this many extra steps when the ranges are cut, so
@@ -811,7 +816,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   __syncthreads();
   if (blockIdx.x == 0) {  // the merge kernel reads the same plan
     for (int i = threadIdx.x; i <= n_tiles; i += kW8 * 64) plan_out[i] = plan_cum[i];
-    for (int i = threadIdx.x; i < n_tiles; i += kW8 * 64) plan_out[kMaxStreamTiles + 1 + i] = plan_end[i];
+    for (int i = threadIdx.x; i < n_tiles; i += kW8 * 64) plan_out[kPlanEndOff + i] = plan_end[i];
   }
   // this block's range [lo, hi_s) of the head's cost line; tile i occupies
   // [plan_cum[i], plan_cum[i+1]): kSegCost start-up units, then its key steps
@@ -819,6 +824,10 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   const int64_t S = plan_cum[n_tiles];
   int lo = (int)(r * S / nbg);
   const int hi_s = (int)((r + 1) * S / nbg);
+  if (g == 0 && threadIdx.x == 0) {  // the range boundaries, for the merge
+    plan_out[kPlanBndOff + r] = lo;
+    if (r == nbg - 1) plan_out[kPlanBndOff + nbg] = hi_s;
+  }
   int i = 0;
   bool first = true;
   while (lo < hi_s) {
@@ -855,21 +864,25 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
   __shared__ float wgt[WS][QQ];
   __shared__ float mxq[QQ], invq[QQ];
   __shared__ int64_t slot_l[kStreamBlocks];
+  __shared__ int bnd_l[kStreamBlocks + 1];
   __shared__ int nsp_l;
   const int quarter = blockIdx.x & 3;
   const int i = (blockIdx.x >> 2) / hkv, g = (blockIdx.x >> 2) % hkv;
   const int n_tiles = batch * max_tiles;
   if (i >= n_tiles) return;
-  const int64_t S = plan[n_tiles];
+  // the blocks' range boundaries go to LDS while the tile's own entries load
+  for (int t = threadIdx.x; t <= nbg; t += kThreads) bnd_l[t] = plan[kPlanBndOff + t];
+  const int S = plan[n_tiles];
   const int c0 = plan[i], c1 = plan[i + 1];
   if (c1 <= c0 || S == 0) return;
+  __syncthreads();
   const int a = c0 + kSegCost;  // the tile's first key step on the cost line
-  // block holding step x: the largest r with floor(r S / nbg) <= x
+  // block holding step x: the largest r whose range starts at or before x
   auto owner = [&](int x) {
     int a = 0, z = nbg - 1;
     while (a < z) {
       const int mid = (a + z + 1) >> 1;
-      if ((int)((int64_t)mid * S / nbg) <= x) a = mid; else z = mid - 1;
+      if (bnd_l[mid] <= x) a = mid; else z = mid - 1;
     }
     return a;
   };
@@ -882,7 +895,7 @@ __global__ __launch_bounds__(kThreads) void attn_stream_merge_kernel(
   if (threadIdx.x == 0) {
     int n = 0;
     for (int rr = rf; rr <= rlst; ++rr) {
-      const int lo_r = (int)((int64_t)rr * S / nbg), hi_r = (int)((int64_t)(rr + 1) * S / nbg);
+      const int lo_r = bnd_l[rr], hi_r = bnd_l[rr + 1];
       if (hi_r <= lo_r) continue;
       slot_l[n++] = (int64_t)(g * nbg + rr) * 2 + (lo_r < c0 ? 1 : 0);
     }
@@ -1070,7 +1083,7 @@ StreamLayout stream_layout(const AttnShape& s) {
   const size_t slots = (size_t)L.nbg * s.hkv * 2;
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   L.plan_off = 0;
-  L.o_off = a256((2 * kMaxStreamTiles + 1) * sizeof(int32_t));
+  L.o_off = a256(kPlanInts * sizeof(int32_t));
   L.ml_off = L.o_off + a256(slots * kW8Qv * s.d * sizeof(uint16_t));
   L.bytes = L.ml_off + a256(slots * kW8Qv * sizeof(float2));
   return L;

@@ -715,10 +715,26 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   };
 
   if (!kStream) {
-    // plain: this block's row tile, all of its keys (up to its largest row position)
+    // plain: this block's row tile, all of its keys (up to its largest row
+    // position).  The blocks of one KV head run the requests one after another,
+    // longest (most keys) first, each request's tiles last row tile first:
+    // the blocks that share an XCD then stream the same request's keys through
+    // its L2, and the shortest work comes last.
     const int rest = blockIdx.x / hkv;
-    const int b = rest % batch;
-    const int tile = max_tiles - 1 - rest / batch;
+    const int rank = rest / max_tiles;
+    const int tile = max_tiles - 1 - (rest - rank * max_tiles);
+    int b = rank;
+    if (batch > 1 && batch <= 64) {
+      // rank of lane j's request: requests with more keys, or as many and a lower index
+      const int nk = l < batch ? cu_kv[l + 1] - cu_kv[l] : -1;
+      int rk = 0;
+      for (int x = 0; x < batch; ++x) {
+        const int nx = __shfl(nk, x, 64);
+        rk += (nx > nk || (nx == nk && x < l)) ? 1 : 0;
+      }
+      const uint64_t hit = __ballot(l < batch && rk == rank);
+      b = __builtin_amdgcn_readfirstlane(hit ? (int)__builtin_ctzll(hit) : rank);
+    }
     const int64_t r0 = cu_rows[b];
     const int nr = cu_rows[b + 1] - (int)r0;
     if (tile * rpb >= nr) return;

@@ -19,7 +19,7 @@
 //    the causal limit masks only tiles that reach past the wave's smallest
 //    position, and waves skip tiles past their largest position.
 // Recomputed rows run on attn_w8_kernel (8 waves, 256 query vectors, a
-// 4-stage K/V ring filled through registers; a persistent "stream" grid when the
+// 4-stage K/V ring filled by buffer loads; a persistent "stream" grid when the
 // row tiles are few and unequal), the probe on attn_pos_kernel (4 waves, K/V
 // by global->LDS loads two and one tiles ahead, key positions from a table).
 // fp32 path (vector ALUs): one wave per (row, head).
@@ -334,15 +334,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_pos_kernel(
 // 256 query vectors per block (256/G rows x the G heads of one KV head), 32
 // per wave, with the same per-wave tile step as attn_pos_kernel.  One block
 // fills a CU (two waves per SIMD), which leaves LDS for a 4-stage ring of
-// K/V tiles.  A segment's first two tiles arrive by buffer loads with an LDS
-// destination; every later tile passes through registers: each thread loads
-// four 16-byte pieces of tile t+3 during step t and writes them into the ring
-// at the start of step t+1, so a load has a whole step to land and the
-// compiler tracks its wait (the global->LDS form measured 7% slower on a
-// 1594-row call: its transfers cost more LDS time than plain 16-byte writes).
-// A per-(request, head) buffer descriptor bounds the key range, so rows past
-// the last key, tiles past the segment and the LDS padding chunks read as
-// zeros without touching memory, and a tile only moves a row offset.
+// K/V tiles: K is fetched three tiles ahead and V two tiles ahead, and a step
+// ends by waiting only for the tiles fetched one step earlier, so every
+// global->LDS transfer has two steps to land.  The transfers are buffer loads
+// with an LDS destination: a per-(request, head) descriptor bounds the key
+// range, so rows past the last key and the LDS padding chunks read as zeros
+// without touching memory, and a tile only moves a scalar row offset.  (Tiles
+// staged through registers -- 16-byte loads one step ahead, then plain LDS
+// writes -- measured 3% slower on the c2 call with its inputs cold in the
+// caches: one step of latency cover instead of two.)
 constexpr int kW8 = 8;                // waves per block
 constexpr int kW8Qv = 32 * kW8;       // query vectors per block
 constexpr int kStages = 4;            // LDS ring depth
@@ -490,39 +490,12 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
           dma16(rv, off, v_base + (uint32_t)(sg * VST + (j - KCH) * 512) * 2u);
       }
     };
-    // Tiles 2, 3, ... pass through registers: each thread loads four 16-byte
-    // pieces of a tile (K and V rows trow and trow + 32, column tcol) one step
-    // before it writes them into the tile's ring stage.  Rows past the keys and
-    // tiles past the segment read as zeros (buffer range).
-    const int trow = threadIdx.x >> 4, tcol = threadIdx.x & 15;
-    const __amdgpu_buffer_rsrc_t brk = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(kc + kv0 * kv_stride + (int64_t)g * D), 0, (int)range, 0x00020000);
-    const __amdgpu_buffer_rsrc_t brv = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(vc + kv0 * kv_stride + (int64_t)g * D), 0, (int)range, 0x00020000);
-    i32x4 stg[4];
-    auto gload = [&](int r) {
-      const uint32_t o0 = r < nt ? (uint32_t)((t0 + r) * kKT + trow) * row_b + tcol * 16 : kOob;
-      const uint32_t o1 = r < nt ? o0 + 32 * row_b : kOob;
-      stg[0] = __builtin_amdgcn_raw_buffer_load_b128(brk, o0, 0, 0);
-      stg[1] = __builtin_amdgcn_raw_buffer_load_b128(brk, o1, 0, 0);
-      stg[2] = __builtin_amdgcn_raw_buffer_load_b128(brv, o0, 0, 0);
-      stg[3] = __builtin_amdgcn_raw_buffer_load_b128(brv, o1, 0, 0);
-    };
-    auto lstore = [&](int r) {
-      const int sg = r & (kStages - 1);
-      uint16_t* kd = k_lds + sg * KST + trow * KSTR + tcol * 8;
-      uint16_t* vd = v_lds + sg * VST + trow * VSTR + tcol * 8;
-      *reinterpret_cast<i32x4*>(kd) = stg[0];
-      *reinterpret_cast<i32x4*>(kd + 32 * KSTR) = stg[1];
-      *reinterpret_cast<i32x4*>(vd) = stg[2];
-      *reinterpret_cast<i32x4*>(vd + 32 * VSTR) = stg[3];
-    };
-    // The first two key tiles go out (global->LDS) and the third into
-    // registers before anything waits on memory (every LDS read of the
-    // previous segment ended at its last barrier), then the row positions and Q.
+    // The first three key tiles go out before anything waits on memory (every
+    // LDS read of the previous segment ended at its last barrier), then the
+    // row positions and Q.
     issue(0);
     issue(1);
-    gload(2);
+    issue(2);
     // unconditional loads from a real row (a load under a lane condition gets a
     // wait of its own, which would also wait for the tiles above); a padding
     // lane's Q only has to be finite: its keys are all masked
@@ -548,7 +521,8 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     // (and every LDS read) are complete, then the block meets
     auto step_barrier = [&]() {
       asm volatile("" ::: "memory");
-      wait_vm_lgkm0<63>();
+      if (w < NFULL) wait_vm_lgkm0<SPW>();
+      else wait_vm_lgkm0<SPW - 1>();
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
     };
@@ -633,13 +607,12 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       }
     };
 
-    // Ring: K(t) and V(t) live in stage t % 4.  Step t writes tile t+2 (loaded
-    // during step t-1) into the stage of tile t-2, whose K was last read in
-    // step t-3 and its V in step t-2, and loads tile t+3 into registers; it
-    // computes S(t+1) while the softmax of tile t runs, then O += P(t) V(t),
-    // and ends at a barrier after its LDS writes completed, so K(t+2) is in
-    // place for step t+1.  Past the last tile the loads still go out (zeros,
-    // no memory traffic).
+    // Ring: K(t) and V(t) live in stage t % 4.  Step t issues tile t+3 into the
+    // stage of tile t-1 (its K was last read in step t-2, its V in step t-1),
+    // computes S(t+1) while the softmax of tile t runs, then O += P(t) V(t); at
+    // its end everything issued before step t -- K(t+2) and V(t+1) among it --
+    // has landed.  Past the last tile the transfers still go out (zeros, no
+    // memory traffic), so every step issues the same number of them.
     f32x16 sa[2], sb[2];
     asm volatile("" ::: "memory");
     wait_vm_lgkm0<0>();
@@ -651,8 +624,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     }
     auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
       const int kt0 = kt_lo + t * kKT;
-      lstore(t + 2);
-      gload(t + 3);
+      issue(t + 3);
       const bool do_cur = kt0 < wave_end;
       const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
       bf16x8 pb[2][2];

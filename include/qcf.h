@@ -266,6 +266,39 @@ qcf_status qcf_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
                            const int32_t* pos_base, int max_seg_len, hipStream_t stream);
 
 /*
+ * qcf_probe_scores_select -- qcf_probe_scores followed by qcf_select_topk on
+ * the scores it finishes (eq. single_layer_importance, or the last term of
+ * eq. critical_layer_importance with accumulate != 0, then eq. critical_mask),
+ * with the final summation of the scores done inside the selection when no
+ * segment is longer than 1024 rows (chunks), so the two steps cost one launch
+ * less; longer segments take the separate final pass.  The results are bit for bit those of the
+ * two calls: `scores` holds the same values afterwards and the same rows are
+ * chosen in the same order.
+ *   scores, q, k, cu_q, cu_kv, ctx_len, max_q_len, max_ctx_len, heads,
+ *   softmax_scale, workspace  as for qcf_probe_scores (same workspace size)
+ *   out_idx, out_pos, n_out, n_seg, seg_start, seg_len, seg_k, out_start,
+ *   max_seg_len  as for qcf_select_topk
+ *   seg_req  int32 [n_seg]: the request b whose context holds segment s;
+ *            out_pos gets row - cu_kv[seg_req[s]] (the position in the request)
+ * A segment whose seg_req is outside [0, batch) is skipped.  A segment's rows
+ * must lie in its request's context (rows cu_kv[b] ..
+ * cu_kv[b] + ctx_len[b] - 1); other rows are ranked by their stored scores.
+ * Errors as for the two calls; nothing is launched when any argument is
+ * rejected.
+ */
+qcf_status qcf_probe_scores_select(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                                   const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                                   qcf_dtype dtype, int batch, const int32_t* cu_q,
+                                   const int32_t* cu_kv, const int32_t* ctx_len, int max_q_len,
+                                   int max_ctx_len, int n_q_heads, int n_kv_heads, int head_dim,
+                                   float softmax_scale, int32_t* out_idx, int32_t* out_pos,
+                                   int64_t n_out, int n_seg, const int32_t* seg_start,
+                                   const int32_t* seg_len, const int32_t* seg_k,
+                                   const int32_t* out_start, const int32_t* seg_req,
+                                   int max_seg_len, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
  * qcf_sparse_prefill_attn -- causal grouped-query attention of the selected
  * rows over the fused cache (Section 2.1.3: a recomputed row at position p
  * reads every prefix key j <= p, itself included); with an explicit kv_pos it

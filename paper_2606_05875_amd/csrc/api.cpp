@@ -240,7 +240,8 @@ qcf_status probe_scores_impl(float* scores, int accumulate, const void* q, int64
                              const int32_t* cu_q, const int32_t* cu_kv, const int32_t* ctx_len,
                              int max_q_len, int max_ctx_len, int n_q_heads, int n_kv_heads,
                              int head_dim, float softmax_scale, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream) {
+                             size_t workspace_bytes, hipStream_t stream,
+                             const qcf::SelectArgs* sel = nullptr) {
   if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
   qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
   if (st != QCF_OK) return st;
@@ -256,7 +257,15 @@ qcf_status probe_scores_impl(float* scores, int accumulate, const void* q, int64
     return QCF_ERR_INVALID_ARG;
   if (!index_ok(cu_q, batch == 0) || !index_ok(cu_kv, batch == 0) || !index_ok(ctx_len, batch == 0))
     return QCF_ERR_INVALID_ARG;
-  if (empty) return QCF_OK;
+  if (empty) {
+    if (!sel || sel->n_seg == 0 || sel->max_seg_len == 0) return QCF_OK;
+    // no scores to compute: the selection runs on the stored ones
+    return hip_status(qcf::launch_select_topk(sel->out_idx, sel->out_pos, sel->n_out, scores,
+                                              n_kv_rows, sel->n_seg, sel->seg_start, sel->seg_len,
+                                              sel->seg_k, sel->out_start, nullptr,
+                                              sel->max_seg_len, stream, sel->seg_req, cu_kv,
+                                              batch));
+  }
   const size_t need = qcf_probe_scores_workspace_size(batch, max_q_len, max_ctx_len, n_q_heads,
                                                       n_kv_heads, head_dim);
   if (workspace_bytes < need || (need > 0 && (!workspace || !aligned256(workspace))))
@@ -264,7 +273,7 @@ qcf_status probe_scores_impl(float* scores, int accumulate, const void* q, int64
   qcf::ProbeShape s{batch, max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim};
   return hip_status(qcf::launch_probe_scores(scores, accumulate, q, n_q_rows, k, n_kv_rows,
                                              k_row_stride, rot, dtype == QCF_BF16, cu_q, cu_kv,
-                                             ctx_len, s, softmax_scale, workspace, stream));
+                                             ctx_len, s, softmax_scale, workspace, stream, sel));
 }
 
 }  // namespace
@@ -281,6 +290,36 @@ qcf_status qcf_probe_scores(float* scores, int accumulate, const void* q, int64_
                            qcf::KeyRot{nullptr, nullptr, 0}, dtype, batch, cu_q, cu_kv, ctx_len,
                            max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim, softmax_scale,
                            workspace, workspace_bytes, stream);
+}
+
+qcf_status qcf_probe_scores_select(float* scores, int accumulate, const void* q, int64_t n_q_rows,
+                                   const void* k, int64_t n_kv_rows, int64_t k_row_stride,
+                                   qcf_dtype dtype, int batch, const int32_t* cu_q,
+                                   const int32_t* cu_kv, const int32_t* ctx_len, int max_q_len,
+                                   int max_ctx_len, int n_q_heads, int n_kv_heads, int head_dim,
+                                   float softmax_scale, int32_t* out_idx, int32_t* out_pos,
+                                   int64_t n_out, int n_seg, const int32_t* seg_start,
+                                   const int32_t* seg_len, const int32_t* seg_k,
+                                   const int32_t* out_start, const int32_t* seg_req,
+                                   int max_seg_len, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  if (n_out < 0 || n_seg < 0 || max_seg_len < 0 || n_out > INT32_MAX) return QCF_ERR_INVALID_ARG;
+  if (n_seg > INT32_MAX / 2) return QCF_ERR_UNSUPPORTED;
+  const bool none = n_seg == 0 || max_seg_len == 0;
+  if (!index_ok(out_idx, none || n_out == 0)) return QCF_ERR_INVALID_ARG;
+  if (out_pos && !index_ok(out_pos, false)) return QCF_ERR_INVALID_ARG;
+  if (!index_ok(seg_start, n_seg == 0) || !index_ok(seg_len, n_seg == 0) ||
+      !index_ok(seg_k, n_seg == 0) || !index_ok(out_start, n_seg == 0) ||
+      !index_ok(seg_req, n_seg == 0))
+    return QCF_ERR_INVALID_ARG;
+  if (!none && (batch <= 0 || !index_ok(cu_kv, false) || !index_ok(scores, n_kv_rows == 0)))
+    return QCF_ERR_INVALID_ARG;
+  const qcf::SelectArgs sel{out_idx, out_pos, n_out, n_seg, seg_start, seg_len,
+                            seg_k, out_start, seg_req, max_seg_len};
+  return probe_scores_impl(scores, accumulate, q, n_q_rows, k, n_kv_rows, k_row_stride,
+                           qcf::KeyRot{nullptr, nullptr, 0}, dtype, batch, cu_q, cu_kv, ctx_len,
+                           max_q_len, max_ctx_len, n_q_heads, n_kv_heads, head_dim, softmax_scale,
+                           workspace, workspace_bytes, stream, none ? nullptr : &sel);
 }
 
 qcf_status qcf_rope_table(float* table, const int32_t* pos, int64_t n, int head_dim,

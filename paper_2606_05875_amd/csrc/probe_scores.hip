@@ -445,7 +445,7 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
                                const void* k, int64_t n_kv_rows, int64_t k_row_stride,
                                const KeyRot& rot, bool bf16, const int32_t* cu_q,
                                const int32_t* cu_kv, const int32_t* ctx_len, const ProbeShape& s,
-                               float scale, void* ws, hipStream_t stream) {
+                               float scale, void* ws, hipStream_t stream, const SelectArgs* sel) {
   if (s.batch == 0 || s.max_ctx_len == 0) return hipSuccess;
   const float scale2 = scale * kLog2e;
   int lg = 0;
@@ -482,6 +482,14 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
       if (rt) QCF_COLS(128, true); else QCF_COLS(128, false);
     }
 #undef QCF_COLS
+    if (sel) {
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      return launch_select_topk(sel->out_idx, sel->out_pos, sel->n_out, scores, n_kv_rows,
+                                sel->n_seg, sel->seg_start, sel->seg_len, sel->seg_k,
+                                sel->out_start, nullptr, sel->max_seg_len, stream, sel->seg_req,
+                                cu_kv, s.batch);
+    }
     return hipGetLastError();
   }
   const WsLayout w = ws_layout(s);
@@ -512,9 +520,24 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
 #undef QCF_PASSES
 #undef QCF_PASS
   }
+  if (sel && sel->max_seg_len <= 1024) {
+    // the column sums are added per key by the selection itself (same order)
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const ScoreCols c{colp, cu_q, cu_kv, ctx_len, n_kv_rows, s.batch, s.hkv, lg,
+                      std::max(1, w.n_qt), w.max_qv, s.max_ctx_len, kQvTile, accumulate};
+    return launch_select_topk_cols(scores, n_kv_rows, c, *sel, stream);
+  }
   scores_final<<<dim3((s.max_ctx_len + kThreads - 1) / kThreads, s.batch), kThreads, 0, stream>>>(
       scores, accumulate, colp, cu_q, cu_kv, ctx_len, n_kv_rows, s.hkv, lg, std::max(1, w.n_qt),
       w.max_qv, s.max_ctx_len);
+  if (sel) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_select_topk(sel->out_idx, sel->out_pos, sel->n_out, scores, n_kv_rows,
+                              sel->n_seg, sel->seg_start, sel->seg_len, sel->seg_k, sel->out_start,
+                              nullptr, sel->max_seg_len, stream, sel->seg_req, cu_kv, s.batch);
+  }
   return hipGetLastError();
 }
 

@@ -30,11 +30,38 @@ hipError_t launch_scatter_kv(void* k_cache, void* v_cache, int64_t n_cache_rows,
                              const int32_t* row_idx, const int32_t* row_pos, int hq, int hkv,
                              int d, double theta, hipStream_t stream);
 
+// Per-segment selection.  out_pos gets row - pos_base[s] when pos_base is set,
+// else row - req_base[seg_req[s]] when seg_req is set (a segment whose request
+// is outside [0, n_req) is skipped), else row.
 hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
                               const float* scores, int64_t n_scores, int n_seg,
                               const int32_t* seg_start, const int32_t* seg_len,
                               const int32_t* seg_k, const int32_t* out_start,
-                              const int32_t* pos_base, int max_seg_len, hipStream_t stream);
+                              const int32_t* pos_base, int max_seg_len, hipStream_t stream,
+                              const int32_t* seg_req = nullptr, const int32_t* req_base = nullptr,
+                              int n_req = 0);
+
+// A selection run on the scores of the same call, right after they are final
+// (segment s lies in request seg_req[s]; out_pos relative to cu_kv[seg_req[s]]).
+struct SelectArgs {
+  int32_t* out_idx;
+  int32_t* out_pos;
+  int64_t n_out;
+  int n_seg;
+  const int32_t *seg_start, *seg_len, *seg_k, *out_start, *seg_req;
+  int max_seg_len;
+};
+// The per-(KV head, query tile) column sums of the bf16 score passes, which the
+// fused selection adds per key (in the order the separate final pass uses).
+struct ScoreCols {
+  const float* colp;
+  const int32_t *cu_q, *cu_kv, *ctx_len;
+  int64_t n_kv_rows;
+  int batch, hkv, lg, n_qt, max_qv, max_ctx, qv_tile, accumulate;
+};
+// hipErrorNotSupported when a segment is longer than 1024 rows
+hipError_t launch_select_topk_cols(float* scores, int64_t n_scores, const ScoreCols& c,
+                                   const SelectArgs& a, hipStream_t stream);
 
 struct AssembleShape {
   int64_t n_rows, row_stride, pic_row_stride, probe_row_stride, n_pic_rows, n_src_rows, n_query,
@@ -70,7 +97,8 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
                                const void* k, int64_t n_kv_rows, int64_t k_row_stride,
                                const KeyRot& rot, bool bf16, const int32_t* cu_q,
                                const int32_t* cu_kv, const int32_t* ctx_len, const ProbeShape& s,
-                               float scale, void* ws, hipStream_t stream);
+                               float scale, void* ws, hipStream_t stream,
+                               const SelectArgs* sel = nullptr);
 
 struct AttnShape {
   int batch, max_rows, max_kv, hq, hkv, d;

@@ -26,6 +26,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kColsMaxSeg = 1024;  // longest segment of the fused score + selection kernel
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   uint32_t b = __float_as_uint(x);
@@ -143,12 +144,18 @@ __device__ __forceinline__ void scan_cells(uint32_t* cells) {
   }
 }
 
-template <int NT, int KPT>
+// With kCols the scores are first made final here: each context row's column
+// sums (ScoreCols) are added in the order of the separate final pass and, with
+// accumulate, onto the row's previous score, then written back; rows outside
+// the request's context keep their stored score.
+template <int NT, int KPT, bool kCols>
 __global__ __launch_bounds__(NT) void topk_reg_kernel(
     int32_t* __restrict__ out_idx, int32_t* __restrict__ out_pos, int64_t n_out,
-    const float* __restrict__ scores, int64_t n_scores, const int32_t* __restrict__ seg_start,
+    float* __restrict__ scores, int64_t n_scores, const int32_t* __restrict__ seg_start,
     const int32_t* __restrict__ seg_len, const int32_t* __restrict__ seg_k,
-    const int32_t* __restrict__ out_start, const int32_t* __restrict__ pos_base) {
+    const int32_t* __restrict__ out_start, const int32_t* __restrict__ pos_base,
+    const int32_t* __restrict__ seg_req, const int32_t* __restrict__ req_base, int n_req,
+    ScoreCols cols) {
   static_assert(NT >= 256 && NT % 64 == 0 && KPT >= 1 && KPT <= 64, "block shape");
   constexpr int NW = NT / 64;
   constexpr int NC = KPT * NW;  // (slot, wave) cells, slot-major = index order
@@ -161,24 +168,74 @@ __global__ __launch_bounds__(NT) void topk_reg_kernel(
   const int n = seg_len[s];
   int k = seg_k[s];
   const int64_t o = out_start[s];
-  const int pb = pos_base ? pos_base[s] : 0;
-  if (n <= 0 || k <= 0 || start < 0 || start + n > n_scores || n > NT * KPT) return;
-  if (k > n) k = n;
-  if (o < 0 || o + k > n_out) return;
+  const int rq = seg_req ? seg_req[s] : 0;
+  if (seg_req && (rq < 0 || rq >= n_req)) return;
+  const int pb = pos_base ? pos_base[s] : (seg_req ? req_base[rq] : 0);
+  if (n <= 0 || start < 0 || start + n > n_scores || n > NT * KPT) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const float* sc = scores + start;
+  float* sc = scores + start;
 
   // Every slot loads (clamped index, so all loads are issued at once).  Slots
   // at or past n get key 0, the smallest key: the top k of the padded slots
   // are those of the segment, since k <= n and equal keys go to the lower
   // index, so no slot needs a validity test later.
   uint32_t key[KPT];
+  if constexpr (kCols) {
+    // (head, query tile) terms in groups of kG, all of a group's loads in flight
+    constexpr int kG = 8;
+    const int b = rq;
+    const int64_t kv0 = cols.cu_kv[b];
+    const int nctx = cols.ctx_len[b];
+    const int nqv = min((cols.cu_q[b + 1] - cols.cu_q[b]) << cols.lg, cols.max_qv);
+    const int nterm = cols.hkv * ((nqv + cols.qv_tile - 1) / cols.qv_tile);
+    const int ntl = max(1, (nqv + cols.qv_tile - 1) / cols.qv_tile);
+    const float* cp = cols.colp + (int64_t)b * cols.hkv * cols.n_qt * cols.max_ctx;
+    float acc[KPT], prev[KPT];
+    int tcl[KPT];
+    bool ctx[KPT];
 #pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    const int i = tid + j * NT;
-    const uint32_t kv = order_key(sc[min(i, n - 1)]);
-    key[j] = i < n ? kv : 0u;
+    for (int j = 0; j < KPT; ++j) {
+      const int i = min(tid + j * NT, n - 1);
+      const int64_t t = start + i - kv0;
+      ctx[j] = t >= 0 && t < nctx && start + i < cols.n_kv_rows;
+      tcl[j] = (int)min(max(t, (int64_t)0), (int64_t)cols.max_ctx - 1);
+      prev[j] = sc[i];
+      acc[j] = 0.f;
+    }
+    for (int e0 = 0; e0 < nterm; e0 += kG) {
+      float v[KPT][kG];
+#pragma unroll
+      for (int e = 0; e < kG; ++e) {
+        const int ec = min(e0 + e, nterm - 1);
+        const int g = ec / ntl, tl = ec - g * ntl;
+        const float* cpe = cp + ((int64_t)g * cols.n_qt + tl) * cols.max_ctx;
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) v[j][e] = cpe[tcl[j]];
+      }
+#pragma unroll
+      for (int e = 0; e < kG; ++e)
+#pragma unroll
+        for (int j = 0; j < KPT; ++j)
+          if (e0 + e < nterm) acc[j] += v[j][e];
+    }
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const int i = tid + j * NT;
+      const float x = ctx[j] ? (cols.accumulate ? prev[j] + acc[j] : acc[j]) : prev[j];
+      if (i < n && ctx[j]) sc[i] = x;
+      key[j] = i < n ? order_key(x) : 0u;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const int i = tid + j * NT;
+      const uint32_t kv = order_key(sc[min(i, n - 1)]);
+      key[j] = i < n ? kv : 0u;
+    }
   }
+  if (k <= 0) return;
+  if (k > n) k = n;
+  if (o < 0 || o + k > n_out) return;
 
   const bool take_all = (k == n);
   uint32_t tau = 0u;
@@ -256,7 +313,8 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(
     int32_t* __restrict__ out_idx, int32_t* __restrict__ out_pos, int64_t n_out,
     const float* __restrict__ scores, int64_t n_scores, const int32_t* __restrict__ seg_start,
     const int32_t* __restrict__ seg_len, const int32_t* __restrict__ seg_k,
-    const int32_t* __restrict__ out_start, const int32_t* __restrict__ pos_base) {
+    const int32_t* __restrict__ out_start, const int32_t* __restrict__ pos_base,
+    const int32_t* __restrict__ seg_req, const int32_t* __restrict__ req_base, int n_req) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t wave_tot[kWaves];
   __shared__ uint32_t sh[2];
@@ -266,7 +324,9 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(
   int n = seg_len[s];
   int k = seg_k[s];
   const int64_t o = out_start[s];
-  const int pb = pos_base ? pos_base[s] : 0;
+  const int rq = seg_req ? seg_req[s] : 0;
+  if (seg_req && (rq < 0 || rq >= n_req)) return;
+  const int pb = pos_base ? pos_base[s] : (seg_req ? req_base[rq] : 0);
   if (n <= 0 || k <= 0 || start < 0 || start + n > n_scores) return;
   if (k > n) k = n;
   if (o < 0 || o + k > n_out) return;
@@ -307,12 +367,16 @@ hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
                               const float* scores, int64_t n_scores, int n_seg,
                               const int32_t* seg_start, const int32_t* seg_len,
                               const int32_t* seg_k, const int32_t* out_start,
-                              const int32_t* pos_base, int max_seg_len, hipStream_t stream) {
+                              const int32_t* pos_base, int max_seg_len, hipStream_t stream,
+                              const int32_t* seg_req, const int32_t* req_base, int n_req) {
   if (n_seg == 0 || max_seg_len == 0) return hipSuccess;
   const dim3 grid(n_seg);
-#define QCF_TOPK(NT, KPT)                                                                        \
-  topk_reg_kernel<NT, KPT><<<grid, NT, 0, stream>>>(out_idx, out_pos, n_out, scores, n_scores,  \
-                                                    seg_start, seg_len, seg_k, out_start, pos_base)
+  float* sw = const_cast<float*>(scores);  // only the kCols form writes scores
+#define QCF_TOPK(NT, KPT)                                                                         \
+  topk_reg_kernel<NT, KPT, false><<<grid, NT, 0, stream>>>(out_idx, out_pos, n_out, sw, n_scores, \
+                                                           seg_start, seg_len, seg_k, out_start,  \
+                                                           pos_base, seg_req, req_base, n_req,    \
+                                                           ScoreCols{})
   if (max_seg_len <= 1024) QCF_TOPK(256, 4);
   else if (max_seg_len <= 4096) QCF_TOPK(256, 16);
   else if (max_seg_len <= 8192) QCF_TOPK(512, 16);
@@ -321,8 +385,25 @@ hipError_t launch_select_topk(int32_t* out_idx, int32_t* out_pos, int64_t n_out,
   else if (max_seg_len <= 65536) QCF_TOPK(1024, 64);
   else
     select_topk_kernel<<<grid, kThreads, 0, stream>>>(out_idx, out_pos, n_out, scores, n_scores,
-                                                      seg_start, seg_len, seg_k, out_start, pos_base);
+                                                      seg_start, seg_len, seg_k, out_start, pos_base,
+                                                      seg_req, req_base, n_req);
 #undef QCF_TOPK
+  return hipGetLastError();
+}
+
+hipError_t launch_select_topk_cols(float* scores, int64_t n_scores, const ScoreCols& c,
+                                   const SelectArgs& a, hipStream_t stream) {
+  if (a.n_seg == 0 || a.max_seg_len == 0) return hipSuccess;
+  const dim3 grid(a.n_seg);
+#define QCF_TOPKC(NT, KPT)                                                                      \
+  topk_reg_kernel<NT, KPT, true><<<grid, NT, 0, stream>>>(                                      \
+      a.out_idx, a.out_pos, a.n_out, scores, n_scores, a.seg_start, a.seg_len, a.seg_k,         \
+      a.out_start, nullptr, a.seg_req, c.cu_kv, c.batch, c)
+  // segments of up to 1024 rows (chunks): every thread sums four rows' terms with all
+  // their loads in flight; longer segments take the separate final pass
+  if (a.max_seg_len <= kColsMaxSeg) QCF_TOPKC(256, 4);
+  else return hipErrorNotSupported;
+#undef QCF_TOPKC
   return hipGetLastError();
 }
 

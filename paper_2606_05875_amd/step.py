@@ -62,6 +62,7 @@ class FusionPlan:
     R_idx_init: np.ndarray   # [|R|] cache rows; query-row slots filled, P slots -1
     R_pos_init: np.ndarray   # [|R|] positions; query-row slots filled
     pos_base: np.ndarray     # [n_sel] first cache row of the segment's request
+    sel_req: np.ndarray      # [n_sel] request of each selection segment
     u_idx: np.ndarray        # [n_q] cache rows of all query tokens
     u_pos: np.ndarray        # [n_q] positions N_b + i
     probe_idx: np.ndarray    # [n_probe] cache rows held by the probe buffer
@@ -135,7 +136,8 @@ class FusionPlan:
         return FusionPlan(
             seg_k=seg_k.astype(np.int32), out_start=out_start.astype(np.int32),
             cu_R=cu_R.astype(np.int32), n_P=n_P, R_idx_init=R_idx.astype(np.int32),
-            R_pos_init=R_pos.astype(np.int32), pos_base=pos_base, u_idx=cat(u_idx),
+            R_pos_init=R_pos.astype(np.int32), pos_base=pos_base,
+            sel_req=np.asarray(sel_req, np.int32), u_idx=cat(u_idx),
             u_pos=cat(u_pos), probe_idx=cat(probe_idx), probe_pos=cat(probe_pos),
             probe_src=cat(probe_src), probe_delta=cat(probe_delta), query_slot=cat(query_slot),
             cu_probe=np.array(cu_probe, np.int32), max_q=int(max(w.q_lens) if B else 0),
@@ -164,9 +166,11 @@ class FusionStep:
     """
 
     def __init__(self, w, rho_bp: int | None = None, device="cuda", fused: bool = False,
-                 selection: str = "chunk"):
+                 selection: str = "chunk", fused_select: bool = True):
         self.w = w
         self.fused = bool(fused)
+        # scores and selection through qcf_probe_scores_select (one launch less) or the two calls
+        self.fused_select = bool(fused_select)
         self.selection = selection
         self.rho_bp = w.rho_bp if rho_bp is None else int(rho_bp)
         self.plan = p = FusionPlan.build(w, self.rho_bp, selection)
@@ -187,7 +191,7 @@ class FusionStep:
         # layout (int32)
         self.seg_start, self.seg_len, self.seg_delta = t(w.seg_start), t(w.seg_len), t(w.seg_delta)
         self.seg_k, self.out_start, self.pos_base = t(p.seg_k), t(p.out_start), t(p.pos_base)
-        self.sel_start, self.sel_len = t(p.sel_start), t(p.sel_len)
+        self.sel_start, self.sel_len, self.sel_req = t(p.sel_start), t(p.sel_len), t(p.sel_req)
         self.cu_kv, self.ctx_len, self.cu_q = t(w.cu_kv), t(w.ctx_len), t(w.cu_q)
         self.cu_R, self.cu_probe = t(p.cu_R), t(p.cu_probe)
         self.u_idx, self.u_pos = t(p.u_idx), t(p.u_pos)
@@ -302,6 +306,16 @@ class FusionStep:
                    self.cu_q, self.cu_kv, self.ctx_len, p.max_q, p.max_ctx, self.scale,
                    accumulate=accumulate, workspace=self.ws_scores)
 
+    def stage_scores_select(self, accumulate=False):
+        """Scores and the selection in one call (the last score pass and the selection share a
+        launch); results identical to stage_scores then stage_select."""
+        p = self.plan
+        self._call(("scores_select", accumulate), qcf.qcf_probe_scores_select, self.scores,
+                   self.q_u, self.k, self.cu_q, self.cu_kv, self.ctx_len, p.max_q, p.max_ctx,
+                   self.scale, self.R_idx, self.sel_start, self.sel_len, self.seg_k,
+                   self.out_start, self.sel_req, p.max_sel, out_pos=self.R_pos,
+                   accumulate=accumulate, workspace=self.ws_scores)
+
     def stage_select(self):
         p = self.plan
         self._call("select", qcf.qcf_select_topk, self.R_idx, self.scores, self.sel_start,
@@ -319,7 +333,7 @@ class FusionStep:
                    self.k, self.v, self.cu_kv, p.max_R, self.max_kv, self.scale,
                    workspace=self.ws_attn)
 
-    STAGES = ("assemble", "probe_attn", "scores", "select", "scatter", "attn")
+    STAGES = ("assemble", "probe_attn", "scores_select", "scatter", "attn")
     STAGES_FUSED = ("rope_table", "rerope", "query_assemble", "probe_attn", "scores_pic", "select",
                     "scatter", "attn")
 
@@ -375,8 +389,11 @@ class FusionStep:
             self.ev_probed.record(self.side)
         else:
             self.stage_probe_attn()
-        self.stage_scores()
-        self.stage_select()
+        if self.fused_select:
+            self.stage_scores_select()
+        else:
+            self.stage_scores()
+            self.stage_select()
         self.stage_scatter()
 
     def join(self, overlap=True):

@@ -40,7 +40,8 @@ def test_every_declared_symbol_is_exported(L):
                          "qcf_rerope", "qcf_assemble",
                          "qcf_gather_rows",
                          "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
-                         "qcf_rope_table", "qcf_probe_scores_pic", "qcf_select_topk", "qcf_sparse_prefill_attn_workspace_size",
+                         "qcf_rope_table", "qcf_probe_scores_pic", "qcf_select_topk",
+                         "qcf_probe_scores_select", "qcf_sparse_prefill_attn_workspace_size",
                          "qcf_sparse_prefill_attn"}
     for name, nargs in decl.items():
         assert hasattr(L, name), name
@@ -169,6 +170,23 @@ def test_rope_table_and_fused_scores_validation(L):
     assert L.qcf_probe_scores_pic(*base(d=96)) == UNSUPPORTED
     assert L.qcf_probe_scores_pic(*base(stride=1000)) == INVALID
     assert L.qcf_probe_scores_pic(*base(wsb=need - 1)) == WORKSPACE
+
+
+def test_scores_select_validation(L):
+    need = L.qcf_probe_scores_workspace_size(2, 64, 5120, 32, 8, 128)
+    base = lambda **kw: [A, 0, A, 128, A, 10368, 1024, BF16, 2, A, A, A, 64, 5120, 32, 8,
+                         kw.get("d", 128), 0.088, kw.get("out", A), None, kw.get("n_out", 300),
+                         kw.get("n_seg", 20), A, A, A, A, kw.get("req", A), kw.get("msl", 512),
+                         A, kw.get("wsb", need), None]
+    assert L.qcf_probe_scores_select(*base(out=None)) == INVALID
+    assert L.qcf_probe_scores_select(*base(out=MIS + 1)) == INVALID
+    assert L.qcf_probe_scores_select(*base(req=None)) == INVALID
+    assert L.qcf_probe_scores_select(*base(n_out=-1)) == INVALID
+    assert L.qcf_probe_scores_select(*base(msl=-1)) == INVALID
+    assert L.qcf_probe_scores_select(*base(d=96)) == UNSUPPORTED
+    assert L.qcf_probe_scores_select(*base(wsb=need - 1)) == WORKSPACE
+    # no segments: the scores' own checks alone apply
+    assert L.qcf_probe_scores_select(*base(n_seg=0, out=None, req=None, wsb=need - 1)) == WORKSPACE
 
 
 def test_topk_and_attn_validation(L):

@@ -179,3 +179,28 @@ def test_c1_matches_stored_oracle_values():
     for r, want in zip(gold["sample_rows"], gold["o_sample"]):
         if r in R:  # a near-tie swap may leave a sampled context row out of the GPU's R
             assert_close(g["o"][R.index(r)].ravel(), np.asarray(want), "f32", f"o[{r}]")
+
+
+@pytest.mark.parametrize("name,selection,rho_bp", [
+    ("c1", "chunk", None), ("c2", "chunk", None), ("c2", "chunk", 0), ("c2", "global", None),
+    ("c5", "chunk", None), ("c4", "global", None)])
+def test_scores_select_matches_separate_calls(name, selection, rho_bp):
+    """qcf_probe_scores_select gives bit for bit the scores and selection of
+    qcf_probe_scores followed by qcf_select_topk (also when it accumulates)."""
+    w = make_workload(name)
+    say(name, selection, "rho_bp", rho_bp, "fused scores+select vs separate calls")
+    a = FusionStep(w, rho_bp, selection=selection, fused_select=True)
+    b = FusionStep(w, rho_bp, selection=selection, fused_select=False)
+    a.run()
+    b.run()
+    ga, gb = a.results(), b.results()
+    for key in ("scores", "R", "R_pos", "k_fuse", "v_fuse", "o"):
+        np.testing.assert_array_equal(ga[key], gb[key], err_msg=key)
+    # a second critical layer's importance accumulated on top of the first
+    a.stage_scores_select(accumulate=True)
+    b.stage_scores(accumulate=True)
+    b.stage_select()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(a.scores.cpu().numpy(), b.scores.cpu().numpy())
+    np.testing.assert_array_equal(a.R_idx.cpu().numpy(), b.R_idx.cpu().numpy())
+    np.testing.assert_array_equal(a.R_pos.cpu().numpy(), b.R_pos.cpu().numpy())

@@ -477,3 +477,37 @@ def test_empty_calls():
     qcf.qcf_sparse_prefill_attn(qz, qz, zi, torch.zeros(2, dtype=torch.int32, device="cuda"), k, k,
                                 torch.tensor([0, 10], dtype=torch.int32, device="cuda"), 0, 10, 0.1)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("n_kv,n_rows,plain", [
+    ([2500, 2500, 400, 3100, 1200, 64], [700, 700, 90, 650, 0, 64], True),
+    ([300, 1200, 50, 1200], [100, 400, 10, 0], False)])
+def test_attention_ragged_batch(n_kv, n_rows, plain):
+    """A ragged batch on both grids: one block per row tile (many tiles; requests taken longest
+    first) and the persistent grid (few tiles; cut tiles merged); equal-length requests, a
+    request with no rows and a short one; sampled rows against the oracle."""
+    say("attention ragged batch", n_kv, n_rows, "plain" if plain else "persistent")
+    rng = np.random.default_rng(8)
+    hq, hkv, d = 32, 8, 128
+    cu_kv = np.concatenate([[0], np.cumsum(n_kv)]).astype(np.int32)
+    cu_r = np.concatenate([[0], np.cumsum(n_rows)]).astype(np.int32)
+    k = draw(rng, (cu_kv[-1], hkv, d), "bf16", 1 / math.sqrt(d))
+    v = draw(rng, (cu_kv[-1], hkv, d), "bf16", 1 / math.sqrt(d))
+    q = draw(rng, (cu_r[-1], hq, d), "bf16", math.sqrt(d))
+    rpos = np.concatenate([np.sort(rng.choice(nk, nr, replace=False)) for nk, nr in zip(n_kv, n_rows)])
+    rpos = rpos.astype(np.int32)
+    # the grid choice: one block per (row tile, request, KV head) from 512 such blocks on
+    assert ((max(n_rows) + 63) // 64 * len(n_kv) * hkv >= 512) == plain
+    out = torch.empty((cu_r[-1], hq, d), dtype=torch.bfloat16, device="cuda")
+    scale = 1 / math.sqrt(d)
+    qcf.qcf_sparse_prefill_attn(out, dev(q, torch.bfloat16), dev(rpos), dev(cu_r), dev(k, torch.bfloat16),
+                                dev(v, torch.bfloat16), dev(cu_kv), max(n_rows), max(n_kv), scale)
+    got = host(out)
+    for b in range(len(n_kv)):
+        a, e, ka, ke = cu_r[b], cu_r[b + 1], cu_kv[b], cu_kv[b + 1]
+        if e == a:
+            continue
+        pick = np.unique(np.concatenate([[a, e - 1], rng.integers(a, e, 4)]))
+        want = Q.round_storage(Q.attention(q[pick], rpos[pick], k[ka:ke], v[ka:ke], np.arange(ke - ka),
+                                           scale, hkv), "bf16")
+        assert_close(got[pick], want, "bf16", f"request {b}")

@@ -19,7 +19,7 @@ namespace qcf {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnits = 4;  // 16-byte units per thread per pass
+constexpr int kUnits = 2;  // 16-byte units per thread per pass (swept: 1, 2, 4)
 
 template <typename T, int D>
 struct AssembleArgs {

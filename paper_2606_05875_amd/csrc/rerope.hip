@@ -17,7 +17,7 @@ namespace qcf {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnitsPerThread = 4;  // key units (rotate-half pairs) per thread per round
+constexpr int kUnitsPerThread = 1;  // key units (rotate-half pairs) per thread per round (swept: 1, 2, 4)
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void rerope_kernel(

@@ -49,6 +49,7 @@ constexpr int kQvTile = 32 * kW;   // query vectors per block
 constexpr int kChunkKeys = 128;    // keys staged in LDS at a time
 constexpr int kMaxSplits = 64;     // key splits per query tile
 constexpr int kPassBlocks = 512;   // blocks aimed for when choosing the splits
+constexpr int kCUs = 256;          // compute units of MI355X
 
 struct WsLayout {
   size_t part_off, col_off, total;
@@ -62,13 +63,26 @@ WsLayout ws_layout(const ProbeShape& s) {
   const int grp = s.hq / s.hkv;
   w.max_qv = s.max_q_len * grp;
   w.n_qt = (w.max_qv + kQvTile - 1) / kQvTile;
-  // key splits of whole 32-key groups, about kPassBlocks blocks per pass
+  // key splits of whole 32-key groups, about kPassBlocks blocks per pass -- or half as
+  // many when rounding the splits to 32 keys would leave more of the last round of
+  // kCUs-block slots idle (blocks of equal work then finish together)
   const int64_t per_split = (int64_t)std::max(1, w.n_qt) * s.hkv * std::max(1, s.batch);
-  const int want = (int)std::min<int64_t>(
-      kMaxSplits, std::max<int64_t>(1, (kPassBlocks + per_split - 1) / per_split));
   const int ctx = std::max(1, s.max_ctx_len);
-  w.split_keys = ((ctx + want - 1) / want + 31) / 32 * 32;
-  w.n_splits = (ctx + w.split_keys - 1) / w.split_keys;
+  auto splits_for = [&](int64_t target, int& keys) {
+    const int want = (int)std::min<int64_t>(
+        kMaxSplits, std::max<int64_t>(1, (target + per_split - 1) / per_split));
+    keys = ((ctx + want - 1) / want + 31) / 32 * 32;
+    return (ctx + keys - 1) / keys;
+  };
+  auto idle = [&](int splits) {
+    const int64_t blocks = per_split * splits;
+    return (double)(((blocks + kCUs - 1) / kCUs) * kCUs - blocks) / (double)blocks;
+  };
+  int keys_a = 0, keys_b = 0;
+  const int sa = splits_for(kPassBlocks, keys_a), sb = splits_for(kPassBlocks / 2, keys_b);
+  const bool half = idle(sb) < idle(sa);
+  w.split_keys = half ? keys_b : keys_a;
+  w.n_splits = half ? sb : sa;
   const size_t nb = (size_t)s.batch * s.hkv;
   // both regions grow with the shape (the split region is sized for the most
   // splits), so a workspace sized for one call serves any smaller one

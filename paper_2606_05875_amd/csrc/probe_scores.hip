@@ -79,7 +79,11 @@ WsLayout ws_layout(const ProbeShape& s) {
     return (double)(((blocks + kCUs - 1) / kCUs) * kCUs - blocks) / (double)blocks;
   };
   int keys_a = 0, keys_b = 0;
-  const int sa = splits_for(kPassBlocks, keys_a), sb = splits_for(kPassBlocks / 2, keys_b);
+  // a batch aims at four times as many blocks: the splits are cut from the longest context,
+  // so shorter requests leave splits empty, and shorter splits even out the busy blocks
+  // (ragged 16-request batch: scores + selection 0.34 -> 0.30 ms)
+  const int64_t target = (int64_t)kPassBlocks * (s.batch > 1 ? 4 : 1);
+  const int sa = splits_for(target, keys_a), sb = splits_for(target / 2, keys_b);
   const bool half = idle(sb) < idle(sa);
   w.split_keys = half ? keys_b : keys_a;
   w.n_splits = half ? sb : sa;

@@ -50,11 +50,12 @@ class FusionStack:
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         f = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
         if share is not None:
-            self.embed, self.wq, self.wk, self.wv, self.wo = (share.embed, share.wq, share.wk, share.wv,
-                                                              share.wo)
+            self.embed, self.wqkv, self.wo = share.embed, share.wqkv, share.wo
         else:
             self.embed = f(sw.embed)
-            self.wq, self.wk, self.wv, self.wo = f(sw.wq), f(sw.wk), f(sw.wv), f(sw.wo)
+            # W_q | W_k | W_v side by side: one product per layer gives q, k and v
+            self.wqkv = torch.cat([f(sw.wq), f(sw.wk), f(sw.wv)], dim=2)
+            self.wo = f(sw.wo)
         # layout
         self.seg_start, self.seg_len, self.seg_delta = t(sw.seg_start), t(sw.seg_len), t(sw.seg_delta)
         self.seg_k, self.out_start, self.pos_base = t(p.seg_k), t(p.out_start), t(p.pos_base)
@@ -110,9 +111,11 @@ class FusionStack:
         n = h.shape[0]
         hf = h.float()
         x = (hf * torch.rsqrt((hf * hf).mean(-1, keepdim=True) + sw.rms_eps)).to(self.dtype)
-        q = (x @ self.wq[l]).view(n, sw.n_q_heads, sw.head_dim)
-        k = (x @ self.wk[l]).view(n, sw.n_kv_heads, sw.head_dim)
-        v = (x @ self.wv[l]).view(n, sw.n_kv_heads, sw.head_dim)
+        y = x @ self.wqkv[l]
+        nq, nkv = sw.n_q_heads * sw.head_dim, sw.n_kv_heads * sw.head_dim
+        q = y[:, :nq].reshape(n, sw.n_q_heads, sw.head_dim)
+        k = y[:, nq:nq + nkv].reshape(n, sw.n_kv_heads, sw.head_dim)
+        v = y[:, nq + nkv:].reshape(n, sw.n_kv_heads, sw.head_dim)
         return q.contiguous(), k.contiguous(), v.contiguous()
 
     def _residual(self, l, h, o):

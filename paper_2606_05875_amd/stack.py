@@ -27,6 +27,7 @@ import math
 
 import numpy as np
 import torch
+import torch.nn.functional as F
 
 from . import qcf
 from .step import FusionPlan, kv_buffer
@@ -109,8 +110,7 @@ class FusionStack:
     def _qkv(self, l, h):
         sw = self.sw
         n = h.shape[0]
-        hf = h.float()
-        x = (hf * torch.rsqrt((hf * hf).mean(-1, keepdim=True) + sw.rms_eps)).to(self.dtype)
+        x = F.rms_norm(h.float(), (h.shape[-1],), eps=sw.rms_eps).to(self.dtype)
         y = x @ self.wqkv[l]
         nq, nkv = sw.n_q_heads * sw.head_dim, sw.n_kv_heads * sw.head_dim
         q = y[:, :nq].reshape(n, sw.n_q_heads, sw.head_dim)
@@ -119,7 +119,7 @@ class FusionStack:
         return q.contiguous(), k.contiguous(), v.contiguous()
 
     def _residual(self, l, h, o):
-        return h + (o.reshape(o.shape[0], -1) @ self.wo[l])
+        return torch.addmm(h, o.reshape(o.shape[0], -1), self.wo[l])
 
     # -- offline: PIC caches --------------------------------------------------
     def build_pic(self):

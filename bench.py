@@ -444,8 +444,8 @@ def main():
                          "single scoring layers (a mechanism demonstration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the step shards by request or KV-head group; see the design notes)", file=sys.stderr)
+        print("bench.py measures one GPU only: the fusion step has no multi-GPU path; it would "
+              "shard by request or by KV-head group, one process per GPU", file=sys.stderr)
         sys.exit(2)
 
     import torch

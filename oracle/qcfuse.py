@@ -114,43 +114,47 @@ def rerope(k_pic, seg_start, seg_len, seg_delta, theta, dtype):
 # ---------------------------------------------------------------------------
 # attention with explicit key positions  (Section 2.1.3 causal rule; eq. anchor_query_state)
 # ---------------------------------------------------------------------------
-def _transpose_kv(k, v):
-    """K as [H_kv, d, n] and V as [H_kv, n, d] (float64, contiguous)."""
-    kt = np.ascontiguousarray(np.asarray(k, np.float64).transpose(1, 2, 0))
-    vt = np.ascontiguousarray(np.asarray(v, np.float64).transpose(1, 0, 2))
-    return kt, vt
-
-
-def _attend_row(q_row, kt, vt, m, scale):
-    """One query row [H_q, d] against keys 0..m-1 of kt/vt; float64 [H_q, d]."""
-    hkv, d = kt.shape[0], kt.shape[1]
-    hq = q_row.shape[0]
-    if m == 0:
-        return np.zeros((hq, d), np.float64)
-    qr = np.asarray(q_row, np.float64).reshape(hkv, hq // hkv, d)
-    logits = np.matmul(qr, kt[:, :, :m]) * scale            # [H_kv, g, m]
-    logits -= logits.max(axis=-1, keepdims=True)
-    p = np.exp(logits)
-    p /= p.sum(axis=-1, keepdims=True)
-    return np.matmul(p, vt[:, :m]).reshape(hq, d)
-
-
-def attention(q, qpos, k, v, kpos, scale, n_kv_heads):
+def attention(q, qpos, k, v, kpos, scale, n_kv_heads, rows_per_pass=16):
     """softmax(q k^T * scale) v per query row and head, over keys with kpos <= qpos.
 
     q [R, H_q, d]; k, v [n, H_kv, d]; kpos ascending.  Query head h reads KV
     head h // (H_q / H_kv) (grouped-query attention).  A row that sees no key
     returns zeros.  Returns float64 [R, H_q, d].
+
+    The rows are taken a few at a time (``rows_per_pass``) only to bound the
+    memory of the logit matrix; every row's softmax runs over all of its
+    visible keys at once, with the invisible ones masked out.
     """
     q = np.asarray(q, np.float64)
+    qpos = np.asarray(qpos)
     kpos = np.asarray(kpos)
     assert np.all(np.diff(kpos) >= 0), "key positions must be ascending"
     assert k.shape[1] == n_kv_heads and q.shape[1] % n_kv_heads == 0
-    kt, vt = _transpose_kv(k, v)
+    R, hq, d = q.shape
+    g = hq // n_kv_heads
+    kh = np.ascontiguousarray(np.asarray(k, np.float64).transpose(1, 0, 2))   # [H_kv, n, d]
+    vh = np.ascontiguousarray(np.asarray(v, np.float64).transpose(1, 0, 2))   # [H_kv, n, d]
     out = np.zeros(q.shape, np.float64)
-    for r in range(q.shape[0]):
-        m = int(np.searchsorted(kpos, qpos[r], side="right"))   # keys 0..m-1 are visible
-        out[r] = _attend_row(q[r], kt, vt, m, scale)
+    for r0 in range(0, R, rows_per_pass):
+        rows = np.arange(r0, min(R, r0 + rows_per_pass))
+        nvis = np.searchsorted(kpos, qpos[rows], side="right")    # row i sees keys 0..nvis[i]-1
+        m = int(nvis.max())
+        if m == 0:
+            continue
+        # [H_kv, rows * g, d] @ [H_kv, d, m]: the logits of every (row, head) pair
+        qb = q[rows].reshape(rows.size, n_kv_heads, g, d).transpose(1, 0, 2, 3).reshape(n_kv_heads, -1, d)
+        s = np.matmul(qb, kh[:, :m].transpose(0, 2, 1))
+        s *= scale
+        hidden = np.repeat(np.arange(m)[None, :] >= nvis[:, None], g, axis=0)   # [rows * g, m]
+        if hidden.any():
+            s[:, hidden] = -np.inf
+        mx = s.max(axis=-1, keepdims=True)
+        s -= np.where(np.isfinite(mx), mx, 0.0)
+        np.exp(s, out=s)                                               # exp(-inf) = 0
+        den = s.sum(axis=-1, keepdims=True)
+        np.divide(s, den, out=s, where=den > 0)
+        o = np.matmul(s, vh[:, :m])                                    # [H_kv, rows * g, d]
+        out[rows] = o.reshape(n_kv_heads, rows.size, g, d).transpose(1, 0, 2, 3).reshape(rows.size, hq, d)
     return out
 
 
@@ -212,7 +216,7 @@ def select_per_chunk(scores_rows, seg_start, seg_len, rho_bp):
 # ---------------------------------------------------------------------------
 # one layer of the fusion step
 # ---------------------------------------------------------------------------
-def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True, selection="chunk"):
+def fusion_step(w, rho_bp=None, attn_rows=None, selection="chunk", P=None):
     """Run one layer's QCFuse fusion step on workload ``w`` (see the package's workloads).
 
     Steps, per request b:
@@ -222,21 +226,24 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True, 
          request positions (eq. anchor_cache), probe attention of the query
          rows over [KV^A ; query K/V] (eq. anchor_query_state);
       4. scores I(t) of the context tokens (eq. single_layer_importance);
-      5. top-k of the scores -> P (eq. critical_mask): per chunk, k_i = floor(rho n_i)
+      5. top-k of the scores (eq. critical_mask): per chunk, k_i = floor(rho n_i)
          (``selection="chunk"``), or over the request's whole context, k = floor(rho N_b)
-         as the equation is written (``selection="global"``); R = P U query rows;
-      6. rotate the fresh q/k of R at their positions and write fresh K/V into
-         the cache rows R (eq. fuse_cache);
+         as the equation is written (``selection="global"``);
+      6. R = P + query rows: rotate the fresh q/k of R at their positions and
+         write the fresh K/V into the cache rows R (eq. fuse_cache);
       7. causal attention of R over the fused cache (Section 2.1.3).
 
-    ``attn_rows``: None (all of R) or an int m -> attention only for m rows of
-    R per request picked deterministically from the oracle's own R (for big
-    configs).  Rows of the near-tie band (|I - I_kth| < band inside a chunk)
-    that are not in P are also evaluated so that a swap of near-tied rows can
-    be checked (``band_attention``; off for configs whose band is large).
-    ``fresh_k`` holds the rotated fresh key of EVERY row (what any row of the
-    fused cache holds if it is recomputed).  Returns a dict of float64 arrays /
-    int arrays.
+    ``P``: None, or the recomputed context rows to use instead of the
+    selection of step 5 (one ascending array of cache rows per request).  The
+    selection of step 5 is still computed and returned as ``P_select``; steps 6
+    and 7 follow ``P``.  Where scores tie within rounding, several selections
+    are correct; a caller that has accepted another selection against
+    ``P_select`` and ``scores`` gets here the fused cache and the attention
+    that the definitions give for that selection.
+    ``attn_rows``: None (every row of R) or the cache rows (a subset of R)
+    whose attention output is evaluated, for large configurations.
+    Returns a dict of float64 / integer arrays; ``o`` maps a cache row to its
+    attention output [H_q, d].
     """
     dt = w.dtype
     d, hq, hkv = w.head_dim, w.n_q_heads, w.n_kv_heads
@@ -244,110 +251,75 @@ def fusion_step(w, rho_bp=None, attn_rows=None, band=1e-3, band_attention=True, 
     scale = 1.0 / np.sqrt(d)
     rho_bp = w.rho_bp if rho_bp is None else int(rho_bp)
     T = w.n_rows
+    if selection not in ("chunk", "global"):
+        raise ValueError(f"selection must be 'chunk' or 'global', not {selection!r}")
 
     K = rerope(w.k_pic, w.seg_start, w.seg_len, w.seg_delta, theta, dt)
     k_rerope = K.copy()
     V = np.array(w.v_pic, np.float64, copy=True)
     scores = np.zeros(T, np.float64)
-    res = dict(k_rerope=k_rerope, o_probe=[], q_u=[], P=[], R=[], R_pos=[], o={},
-               band_rows=[], q_fresh={})
+    res = dict(k_rerope=k_rerope, o_probe=[], q_u=[], P=[], P_select=[], R=[], R_pos=[], o={})
 
-    # fresh, rotated tensors for any row (used for R and for the near-tie band)
     def fresh_row(rows, pos):
+        """The recomputed rows' q and k rotated at their positions, and their v."""
         qr = round_storage(rope(w.q_new[rows], pos, theta), dt)
         kr = round_storage(rope(w.k_new[rows], pos, theta), dt)
-        vr = np.asarray(w.v_new[rows], np.float64)
-        return qr, kr, vr
+        return qr, kr, np.asarray(w.v_new[rows], np.float64)
 
-    per_req = []
     for b in range(w.batch):
         base, N, nq = int(w.cu_kv[b]), int(w.ctx_len[b]), int(w.q_lens[b])
         urows = np.arange(base + N, base + N + nq)
         upos = np.arange(N, N + nq)
         qU, kU, vU = fresh_row(urows, upos)
-        K[urows] = kU
-        V[urows] = vU
-        # anchor cache with request positions
+        # anchor cache with request positions, then the probe over [KV^A ; query K/V]
         segs = np.nonzero(w.seg_req == b)[0]
-        arows = np.concatenate([w.seg_start[s] + w.anchor_local[s] for s in segs]) if segs.size else np.zeros(0, int)
-        apos = arows - base
+        arows = (np.concatenate([w.seg_start[s] + w.anchor_local[s] for s in segs])
+                 if segs.size else np.zeros(0, np.int64))
         kp = np.concatenate([K[arows], kU])
         vp = np.concatenate([V[arows], vU])
-        ppos = np.concatenate([apos, upos])
-        o_probe = round_storage(attention(qU, upos, kp, vp, ppos, scale, hkv), dt)
-        # scores over the request's context keys (re-positioned PIC keys)
-        I = critical_scores(qU, K[base:base + N], scale, hkv)
-        scores[base:base + N] = I
+        ppos = np.concatenate([arows - base, upos])
+        res["o_probe"].append(round_storage(attention(qU, upos, kp, vp, ppos, scale, hkv), dt))
+        res["q_u"].append(qU)
+        # scores over the request's context keys (re-positioned PIC keys), then the selection
+        scores[base:base + N] = critical_scores(qU, K[base:base + N], scale, hkv)
         if selection == "global":
             sel = [(base, N)]
-        elif selection == "chunk":
-            sel = [(int(w.seg_start[s]), int(w.seg_len[s])) for s in segs]
         else:
-            raise ValueError(f"selection must be 'chunk' or 'global', not {selection!r}")
-        P = select_per_chunk(scores, [a for a, _ in sel], [n for _, n in sel], rho_bp)
-        # near-tie band around each selection segment's cut
-        band_rows = []
-        for a, n in sel:
-            k = per_chunk_k(n, rho_bp)
-            if 0 < k < n:
-                srt = np.sort(scores[a:a + n])[::-1]
-                cut_hi, cut_lo = srt[k - 1], srt[k]
-                near = np.nonzero((np.abs(scores[a:a + n] - cut_hi) < band) |
-                                  (np.abs(scores[a:a + n] - cut_lo) < band))[0] + a
-                band_rows.append(near)
-        band_rows = np.unique(np.concatenate(band_rows)) if band_rows else np.zeros(0, int)
-        R = np.concatenate([P, urows])
-        res["o_probe"].append(o_probe)
-        res["q_u"].append(qU)
-        res["P"].append(P)
+            sel = [(int(w.seg_start[s]), int(w.seg_len[s])) for s in segs]
+        P_sel = select_per_chunk(scores, [a for a, _ in sel], [n for _, n in sel], rho_bp)
+        P_b = P_sel if P is None else np.asarray(P[b], np.int64)
+        assert np.all(np.diff(P_b) > 0) and np.all((P_b >= base) & (P_b < base + N))
+        res["P_select"].append(P_sel)
+        res["P"].append(P_b)
+        R = np.concatenate([P_b, urows])
         res["R"].append(R)
         res["R_pos"].append(R - base)
-        res["band_rows"].append(band_rows)
-        per_req.append((base, N, nq, P, R, band_rows))
 
-    # fused cache: write every request's fresh K/V for P (query rows already written)
-    for (base, N, nq, P, R, band_rows) in per_req:
-        if P.size:
-            _, kP, vP = fresh_row(P, P - base)
-            K[P] = kP
-            V[P] = vP
-
-    # attention of R (and the near-tie band) over the fused cache
-    for b, (base, N, nq, P, R, band_rows) in enumerate(per_req):
-        rows = R
-        if attn_rows is not None and R.size > attn_rows:
-            pick = np.unique(np.linspace(0, R.size - 1, attn_rows).round().astype(int))
-            rows = R[pick]
-        extra = np.setdiff1d(band_rows, P) if band_attention else np.zeros(0, np.int64)
-        rows_all = np.concatenate([rows, extra])
-        pos_all = rows_all - base
-        q_all, k_all, v_all = fresh_row(rows_all, pos_all)
-        Kb = K[base:base + N + nq]
-        Vb = V[base:base + N + nq]
-        kpos = np.arange(N + nq)
-        o_main = round_storage(attention(q_all[:rows.size], pos_all[:rows.size], Kb, Vb, kpos, scale, hkv), dt)
-        for i, r in enumerate(rows):
-            res["o"][int(r)] = o_main[i]
-        # a band row that the other side may pick instead sees the fused cache
-        # with its own fresh K/V in place of its re-positioned PIC entry
-        if rows_all.size > rows.size:
-            kt, vt = _transpose_kv(Kb, Vb)
-            for i in range(rows.size, rows_all.size):
-                r = int(rows_all[i])
-                j = r - base
-                keep_k, keep_v = kt[:, :, j].copy(), vt[:, j].copy()
-                kt[:, :, j], vt[:, j] = k_all[i], v_all[i]
-                o_x = _attend_row(q_all[i], kt, vt, j + 1, scale)
-                kt[:, :, j], vt[:, j] = keep_k, keep_v
-                res["o"][r] = round_storage(o_x, dt)
-        for i, r in enumerate(rows_all):
-            res["q_fresh"][int(r)] = q_all[i]
-
-    fresh_k = np.zeros_like(K)
+    # fused cache: every recomputed row holds its fresh K/V (eq. fuse_cache)
     for b in range(w.batch):
-        base, n = int(w.cu_kv[b]), int(w.cu_kv[b + 1] - w.cu_kv[b])
-        fresh_k[base:base + n] = round_storage(rope(w.k_new[base:base + n], np.arange(n), theta), dt)
-    res["fresh_k"] = fresh_k
+        base = int(w.cu_kv[b])
+        R = res["R"][b]
+        _, kR, vR = fresh_row(R, R - base)
+        K[R] = kR
+        V[R] = vR
+
+    # attention of R (or of the requested rows of R) over the fused cache
+    want = None if attn_rows is None else set(int(r) for r in np.asarray(attn_rows).ravel())
+    for b in range(w.batch):
+        base, n_b = int(w.cu_kv[b]), int(w.cu_kv[b + 1] - w.cu_kv[b])
+        R = res["R"][b]
+        rows = R if want is None else np.array([r for r in R if int(r) in want], np.int64)
+        if rows.size == 0:
+            continue
+        qr, _, _ = fresh_row(rows, rows - base)
+        o = round_storage(attention(qr, rows - base, K[base:base + n_b], V[base:base + n_b],
+                                    np.arange(n_b), scale, hkv), dt)
+        for i, r in enumerate(rows):
+            res["o"][int(r)] = o[i]
+    if want is not None:
+        inR = set(int(r) for b in range(w.batch) for r in res["R"][b])
+        assert want <= inR, "attn_rows must be recomputed rows"
+
     res["scores"] = scores
     res["k_fuse"] = K
     res["v_fuse"] = V

@@ -9,7 +9,7 @@ import torch
 import oracle
 from paper_2606_05875_amd.step import FusionStep
 from paper_2606_05875_amd.workloads import make_workload
-from parity import check_step
+from parity import check_step, oracle_for
 
 pytestmark = pytest.mark.gpu
 
@@ -19,13 +19,14 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_case(w, rho_bp=None, attn_rows=None, band_attention=True):
-    say(w.name, w.dtype, "rows", w.n_rows, "chunks", w.n_chunks, "rho_bp", rho_bp or w.rho_bp)
-    step = FusionStep(w, rho_bp)
+def run_case(w, rho_bp=None, sampled=False, selection="chunk"):
+    say(w.name, w.dtype, "rows", w.n_rows, "chunks", w.n_chunks, "rho_bp", rho_bp or w.rho_bp,
+        "selection", selection, "sampled" if sampled else "all rows")
+    step = FusionStep(w, rho_bp, selection=selection)
     step.run()
     g = step.results()
-    o = oracle.fusion_step(w, rho_bp=rho_bp, attn_rows=attn_rows, band_attention=band_attention)
-    rep = check_step(w, g, o, sampled=attn_rows is not None or not band_attention)
+    o = oracle_for(w, g, rho_bp, selection, sampled)
+    rep = check_step(w, g, o, selection)
     say("  ", {k: v for k, v in rep.items()})
     rec = oracle.recall(np.concatenate(g["P"]), w.evidence_rows) if w.evidence_rows.size else 1.0
     return step, g, o, rep, rec
@@ -39,13 +40,16 @@ def test_config_full(name):
 
 
 def test_config_c4_sampled():
+    # attention on every row tile of the GPU grid (a seeded row and the tile's last row)
     w = make_workload("c4")
-    run_case(w, attn_rows=48, band_attention=False)
+    _, _, _, rep, rec = run_case(w, sampled=True)
+    assert rec == 1.0 and rep["o_rows"] >= 600
 
 
 def test_config_c5_sampled():
     w = make_workload("c5")
-    run_case(w, attn_rows=6, band_attention=False)
+    _, _, _, rep, rec = run_case(w, sampled=True)
+    assert rec == 1.0 and rep["o_rows"] >= 700
 
 
 @pytest.mark.parametrize("rho_bp", [0, 10000])
@@ -138,23 +142,16 @@ def test_fused_scores_flow_matches_unfused(name, dtype):
 
 @pytest.mark.parametrize("name,kw,rho_bp", [
     ("c2", {}, None),                                                   # one 5120-token context
+    ("c4", {}, None),                                                   # one 32768-token context
     ("c5", {}, None),                                                   # 16 requests, up to ~16K each
     ("c2", dict(chunk_lens=[[300, 212], [64], [129, 1, 511, 40]], q_lens=[5, 64, 17],
                 anchors_per_chunk=3, dtype="f32"), 2500),
 ])
 def test_global_selection(name, kw, rho_bp):
     """Global mode: floor(rho N_b) rows over each request's whole context (one top-k segment
-    per request), against the oracle's global selection."""
+    per request), against the oracle's global selection (eq. critical_mask as written)."""
     w = make_workload(name, **kw)
-    say(w.name, w.dtype, "global selection, rows", w.n_rows, "requests", w.batch)
-    step = FusionStep(w, rho_bp, selection="global")
-    step.run()
-    g = step.results()
-    big = w.n_rows > 20000
-    o = oracle.fusion_step(w, rho_bp=rho_bp, attn_rows=6 if big else None, band_attention=not big,
-                           selection="global")
-    rep = check_step(w, g, o, sampled=big, selection="global")
-    say("  ", rep)
+    _, g, _, _, _ = run_case(w, rho_bp, sampled=w.n_rows > 20000, selection="global")
     for b in range(w.batch):
         assert len(g["P"][b]) == ((rho_bp or w.rho_bp) * int(w.ctx_len[b])) // 10000
 

@@ -316,6 +316,74 @@ def test_fused_cache_rows():
         np.testing.assert_array_equal(r["v_fuse"][t], w.v_new[t])
 
 
+def _near_tie_swap(w, r):
+    """P with one selected row of the chunk with the smallest cut gap exchanged for the
+    best unselected row of that chunk (a near-tied alternative selection)."""
+    best = None
+    for s in range(w.n_chunks):
+        a, n = int(w.seg_start[s]), int(w.seg_len[s])
+        sel = [int(t) for t in r["P"][0] if a <= t < a + n]
+        rest = [t for t in range(a, a + n) if t not in sel]
+        if not sel or not rest:
+            continue
+        x = min(sel, key=lambda t: (r["scores"][t], -t))          # the last one taken
+        y = max(rest, key=lambda t: (r["scores"][t], -t))         # the first one left out
+        gap = r["scores"][x] - r["scores"][y]
+        if best is None or gap < best[0]:
+            best = (gap, x, y)
+    _, x, y = best
+    return np.sort(np.array([t for t in r["P"][0] if t != x] + [y], np.int64)), x, y
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_given_selection_is_the_definition_on_that_selection(dtype):
+    # an alternative selection (one near-tied row swapped) handed to the oracle: the fused
+    # cache and every recomputed row's output must be what the definitions give for that
+    # selection, built here by hand (complex rotation, torch SDPA in float64)
+    w = make_workload("c1", dtype=dtype)
+    own = Q.fusion_step(w)
+    P, x, y = _near_tie_swap(w, own)
+    r = Q.fusion_step(w, P=[P])
+    np.testing.assert_array_equal(r["P_select"][0], own["P"][0])     # its own selection is kept
+    np.testing.assert_array_equal(r["P"][0], P)
+    N, T = int(w.ctx_len[0]), w.n_rows
+    rd = (lambda a: np.asarray(a, np.float32).astype(np.float64)) if dtype == "f32" else Q.round_bf16
+    pos = np.arange(T)
+    local = np.concatenate([np.arange(n) for n in w.seg_len] + [np.zeros(T - N, int)])
+    delta = np.concatenate([np.full(n, o) for n, o in zip(w.seg_len, w.seg_delta)] + [np.zeros(T - N, int)])
+    # stored keys are rotated at their local positions: one more rotation by the offset
+    k_pic = rd(rope_complex(w.k_pic, delta, w.rope_theta))
+    k_pic[N:] = 0.0
+    R = np.concatenate([P, np.arange(N, T)])
+    fused_k = k_pic.copy()
+    fused_v = np.array(w.v_pic, np.float64)
+    fused_k[R] = rd(rope_complex(w.k_new[R], R, w.rope_theta))
+    fused_v[R] = w.v_new[R]
+    np.testing.assert_allclose(r["k_fuse"], fused_k, atol=2e-6 if dtype == "f32" else 1e-2)
+    np.testing.assert_array_equal(r["v_fuse"], fused_v)
+    assert not np.array_equal(r["k_fuse"][x], own["k_fuse"][x])     # x went back to its PIC entry
+    q = rd(rope_complex(w.q_new[R], R, w.rope_theta))
+    want = sdpa(q, fused_k, fused_v, mask=pos[None, :] <= R[:, None])
+    got = np.stack([r["o"][int(t)] for t in R])
+    tol = 2e-6 if dtype == "f32" else 1.6e-2
+    np.testing.assert_allclose(got, want, atol=tol)
+    # rows after y see y's fresh key: their outputs differ from those on the own selection
+    later = [t for t in R if t > y and t in own["o"]]
+    assert any(not np.array_equal(r["o"][t], own["o"][t]) for t in later)
+
+
+def test_attention_rows_subset_equals_full_run():
+    # evaluating only some rows gives those rows' outputs of the full evaluation, bit for bit
+    w = make_workload("c1")
+    full = Q.fusion_step(w)
+    R = full["R"][0]
+    some = R[::7]
+    part = Q.fusion_step(w, attn_rows=some)
+    assert sorted(part["o"]) == sorted(int(t) for t in some)
+    for t in some:
+        np.testing.assert_array_equal(part["o"][int(t)], full["o"][int(t)])
+
+
 def test_anchor_probe_endpoints():
     # all positions as anchors: the probe is the query's attention over the full
     # re-positioned context (the full-view probe); no anchors: query-only probing
@@ -339,7 +407,7 @@ def test_anchor_probe_endpoints():
 def test_scores_step_invariant_and_recall():
     for name in ("c1", "c2"):
         w = make_workload(name)
-        r = Q.fusion_step(w, attn_rows=8)
+        r = Q.fusion_step(w, attn_rows=np.arange(int(w.ctx_len[0]), w.n_rows))
         assert abs(r["scores"].sum() - w.n_q_heads * sum(w.q_lens)) < 1e-6 * w.n_rows
         assert Q.recall(np.concatenate(r["P"]), w.evidence_rows) == 1.0
 

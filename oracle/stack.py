@@ -29,7 +29,9 @@ Readings (the paper fixes none of them for a synthetic stack): attention-only
 blocks without an MLP, RMSNorm without a learned gain, residual in the
 storage dtype.  Where the GPU stores a tensor in the storage dtype (normed
 input, projections, rotated q/k, attention output, hidden state) the oracle
-rounds it once to that dtype; the arithmetic in between is float64.
+rounds it once to that dtype; the arithmetic in between is float64.  The
+output projection and the residual sum form one stored tensor (the product
+is added into the hidden state before it is rounded).
 """
 from __future__ import annotations
 
@@ -37,7 +39,7 @@ import numpy as np
 
 from .qcfuse import (attention, critical_scores, round_storage, rope, select_per_chunk, select_topk)
 
-__all__ = ["rms_norm", "block_qkv", "full_forward", "build_pic", "stack_fusion", "anchor_count",
+__all__ = ["rms_norm", "block_proj", "block_qkv", "full_forward", "build_pic", "stack_fusion", "anchor_count",
            "anchors_sink", "anchors_knorm"]
 
 
@@ -47,24 +49,32 @@ def rms_norm(h, eps):
     return h / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps)
 
 
-def block_qkv(sw, l, h, pos):
-    """Rotated q [n, H_q, d], rotated k and v [n, H_kv, d] of layer l for hidden states h."""
+def block_proj(sw, l, h):
+    """Un-rotated q [n, H_q, d], k and v [n, H_kv, d] of layer l for hidden states h:
+    RMSNorm(h) and the three products, each stored in the storage dtype."""
     dt, d = sw.dtype, sw.head_dim
     n = h.shape[0]
     x = round_storage(rms_norm(h, sw.rms_eps), dt)
     q = round_storage(x @ np.asarray(sw.wq[l], np.float64), dt).reshape(n, sw.n_q_heads, d)
     k = round_storage(x @ np.asarray(sw.wk[l], np.float64), dt).reshape(n, sw.n_kv_heads, d)
     v = round_storage(x @ np.asarray(sw.wv[l], np.float64), dt).reshape(n, sw.n_kv_heads, d)
+    return q, k, v
+
+
+def block_qkv(sw, l, h, pos):
+    """Rotated q [n, H_q, d], rotated k and v [n, H_kv, d] of layer l for hidden states h."""
+    dt = sw.dtype
+    q, k, v = block_proj(sw, l, h)
     q = round_storage(rope(q, pos, sw.rope_theta), dt)
     k = round_storage(rope(k, pos, sw.rope_theta), dt)
     return q, k, v
 
 
 def residual(sw, l, h, o):
-    """h + o Wo_l, each product and sum stored in the storage dtype."""
-    dt = sw.dtype
-    y = round_storage(o.reshape(o.shape[0], -1) @ np.asarray(sw.wo[l], np.float64), dt)
-    return round_storage(np.asarray(h, np.float64) + y, dt)
+    """h + o Wo_l, stored once in the storage dtype (the product and the sum are one
+    step, as a projection that adds into its output does it)."""
+    y = o.reshape(o.shape[0], -1) @ np.asarray(sw.wo[l], np.float64)
+    return round_storage(np.asarray(h, np.float64) + y, sw.dtype)
 
 
 def full_forward(sw, h0, pos):

@@ -105,6 +105,10 @@ class FusionStack:
                                    dtype=torch.uint8, device=dev)
         self.pic_built = share.pic_built if share is not None else False
         self.no_seg = torch.zeros(0, dtype=torch.int32, device=dev)
+        # layers whose per-layer inputs and outputs are kept (device copies) for inspection:
+        # tr_pic[l] (offline chunk pass), tr_sel[l] (query probe), tr_rec[l] (recompute)
+        self.trace: set = set()
+        self.tr_pic, self.tr_sel, self.tr_rec = {}, {}, {}
 
     # -- glue: RMSNorm, projections, residual (torch) ---------------------------
     def _qkv(self, l, h):
@@ -137,7 +141,11 @@ class FusionStack:
                                         self.v_pic[l], self.cu_chunk_kv,
                                         int(sw.seg_len.max()), self.max_chunk_kv, self.scale,
                                         workspace=self.ws_attn)
+            h_in = h
             h = self._residual(l, h, o)
+            if l in self.trace:
+                self.tr_pic[l] = dict(h=h_in.clone(), q_raw=q.clone(), k_raw=k.clone(), q=q_rot.clone(),
+                                      o=o.clone(), h_out=h.clone())
         self.pic_built = True
 
     # -- where the stored chunk caches come from ---------------------------------
@@ -188,7 +196,12 @@ class FusionStack:
                                      self.ctx_len, p.max_q, p.max_ctx, self.scale,
                                      accumulate=not first, workspace=self.ws_scores)
                 first = False
+            h_in = hU
             hU = self._residual(l, hU, self.o_probe)
+            if l in self.trace:
+                self.tr_sel[l] = dict(h=h_in.clone(), q_raw=q.clone(), k_raw=k.clone(), q=self.q_u.clone(),
+                                      k_probe=self.k_probe.clone(), v_probe=self.v_probe.clone(),
+                                      o=self.o_probe.clone(), h_out=hU.clone())
         self.h_probe = hU
         # one selection for every layer
         self.R_idx.copy_(self.R_idx_init)
@@ -214,10 +227,15 @@ class FusionStack:
             qcf.qcf_sparse_prefill_attn(self.o_R, self.q_R, self.R_pos, self.cu_R, self.k_req[l],
                                         self.v_req[l], self.cu_kv, p.max_R, self.max_kv, self.scale,
                                         workspace=self.ws_attn)
+            h_in = hR
             hR = self._residual(l, hR, self.o_R)
+            if l in self.trace:
+                self.tr_rec[l] = dict(h=h_in.clone(), q_raw=q.clone(), k_raw=k.clone(), q=self.q_R.clone(),
+                                      o=self.o_R.clone(), h_out=hR.clone())
         self.h_R = hR
 
-    def results(self):
+    def results(self, caches: bool = True):
+        """Host copies of the outputs; ``caches=False`` leaves out the per-layer fused caches."""
         torch.cuda.synchronize()
         c = lambda x: x.float().cpu().numpy().astype(np.float64)
         p = self.plan
@@ -225,11 +243,13 @@ class FusionStack:
         hR = c(self.h_R)
         hP = c(self.h_probe)
         cq = self.sw.cu_q
-        return dict(scores=self.scores.double().cpu().numpy(), R=R, cu_R=p.cu_R,
-                    P=[R[p.cu_R[b]:p.cu_R[b] + p.n_P[b]] for b in range(self.sw.batch)],
-                    h_R=[hR[p.cu_R[b]:p.cu_R[b + 1]] for b in range(self.sw.batch)],
-                    h_probe=[hP[cq[b]:cq[b + 1]] for b in range(self.sw.batch)],
-                    k_fuse=[c(k) for k in self.k_req], v_fuse=[c(v) for v in self.v_req])
+        out = dict(scores=self.scores.double().cpu().numpy(), R=R, cu_R=p.cu_R,
+                   P=[R[p.cu_R[b]:p.cu_R[b] + p.n_P[b]] for b in range(self.sw.batch)],
+                   h_R=[hR[p.cu_R[b]:p.cu_R[b + 1]] for b in range(self.sw.batch)],
+                   h_probe=[hP[cq[b]:cq[b + 1]] for b in range(self.sw.batch)])
+        if caches:
+            out.update(k_fuse=[c(k) for k in self.k_req], v_fuse=[c(v) for v in self.v_req])
+        return out
 
 
 class HostPicPipeline:

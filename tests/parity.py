@@ -35,16 +35,19 @@ def assert_close(got, want, dtype, what):
     return mx, rl
 
 
-def assert_ulp(got, want, dtype, what, rel_slack=2.0 ** -20):
-    """Each element within one storage-dtype step of the correctly rounded value
+def assert_ulp(got, want, dtype, what, rel_slack=2.0 ** -20, steps=1):
+    """Each element within ``steps`` storage-dtype steps of the correctly rounded value
     (plus a float32 cancellation slack relative to the tensor's largest value)."""
     got = np.asarray(got, np.float64)
     want = np.asarray(want, np.float64)
+    assert got.shape == want.shape, (what, got.shape, want.shape)
+    if got.size == 0:
+        return
     bits = 8 if dtype == "bf16" else 24
     step = np.ldexp(1.0, np.frexp(np.abs(want))[1] - bits)
-    slack = rel_slack * float(np.max(np.abs(want))) if want.size else 0.0
-    bad = np.abs(got - want) > np.maximum(step * 1.0001, slack)
-    assert not bad.any(), f"{what}: {bad.sum()} elements more than one step off"
+    slack = rel_slack * float(np.max(np.abs(want)))
+    bad = np.abs(got - want) > np.maximum(steps * step * 1.0001, slack)
+    assert not bad.any(), f"{what}: {bad.sum()} elements more than {steps} step(s) off"
 
 
 def assert_scores(got, want, what="scores"):

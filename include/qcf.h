@@ -299,6 +299,35 @@ qcf_status qcf_probe_scores_select(float* scores, int accumulate, const void* q,
                                    hipStream_t stream);
 
 /*
+ * qcf_probe_scores_select_noalloc -- qcf_probe_scores_select for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments and results, minus
+ * the workspace: its scratch space is a fixed array of
+ * QCF_NOALLOC_SCRATCH_BYTES in the library's device image, one per GPU, held
+ * until the process ends.  The call allocates nothing (its first call on a
+ * device looks the array's address up once).
+ *   Shapes whose qcf_probe_scores_workspace_size exceeds
+ *   QCF_NOALLOC_SCRATCH_BYTES are rejected with QCF_ERR_WORKSPACE before
+ *   anything is launched.  The kernels read back only scratch words written
+ *   earlier in the same call, so the array is never cleared.
+ *   All calls on one GPU share its array: calls that may overlap on that GPU
+ *   (several streams, several host threads) race and must be serialised by
+ *   the caller, e.g. by issuing them on one stream.
+ */
+#define QCF_NOALLOC_SCRATCH_BYTES (48 << 20)
+qcf_status qcf_probe_scores_select_noalloc(float* scores, int accumulate, const void* q,
+                                           int64_t n_q_rows, const void* k, int64_t n_kv_rows,
+                                           int64_t k_row_stride, qcf_dtype dtype, int batch,
+                                           const int32_t* cu_q, const int32_t* cu_kv,
+                                           const int32_t* ctx_len, int max_q_len, int max_ctx_len,
+                                           int n_q_heads, int n_kv_heads, int head_dim,
+                                           float softmax_scale, int32_t* out_idx, int32_t* out_pos,
+                                           int64_t n_out, int n_seg, const int32_t* seg_start,
+                                           const int32_t* seg_len, const int32_t* seg_k,
+                                           const int32_t* out_start, const int32_t* seg_req,
+                                           int max_seg_len, hipStream_t stream);
+
+/*
  * qcf_sparse_prefill_attn -- causal grouped-query attention of the selected
  * rows over the fused cache (Section 2.1.3: a recomputed row at position p
  * reads every prefix key j <= p, itself included); with an explicit kv_pos it

@@ -19,7 +19,8 @@ __all__ = [
     "qcf_rerope",
     "qcf_assemble", "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
     "qcf_rope_table", "qcf_probe_scores_pic",
-    "qcf_select_topk", "qcf_probe_scores_select", "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
+    "qcf_select_topk", "qcf_probe_scores_select", "qcf_probe_scores_select_noalloc",
+    "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
     "EXPORTS", "Prepared", "prepare",
 ]
 
@@ -54,6 +55,9 @@ EXPORTS = {
     "qcf_probe_scores_select": (_I, [_P, _I, _P, _I64, _P, _I64, _I64, _I, _I, _P, _P, _P, _I, _I, _I,
                                      _I, _I, ctypes.c_float, _P, _P, _I64, _I, _P, _P, _P, _P, _P,
                                      _I, _P, _SZ, _P]),
+    "qcf_probe_scores_select_noalloc": (_I, [_P, _I, _P, _I64, _P, _I64, _I64, _I, _I, _P, _P, _P, _I,
+                                             _I, _I, _I, _I, ctypes.c_float, _P, _P, _I64, _I, _P, _P,
+                                             _P, _P, _P, _I, _P]),
     "qcf_sparse_prefill_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
     "qcf_sparse_prefill_attn": (_I, [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I, _I,
                                      _I, _I, _I, _I, _I, ctypes.c_float, _P, _SZ, _P]),
@@ -416,6 +420,35 @@ def qcf_probe_scores_select(scores, q, k, cu_q, cu_kv, ctx_len, max_q_len, max_c
             out_idx.numel(), seg_start.numel(), _ptr(seg_start), _ptr(seg_len), _ptr(seg_k),
             _ptr(out_start), _ptr(seg_req), int(max_seg_len), _ptr(workspace), workspace.numel(),
             keep=workspace)
+
+
+def qcf_probe_scores_select_noalloc(scores, q, k, cu_q, cu_kv, ctx_len, max_q_len, max_ctx_len,
+                                    softmax_scale, out_idx, seg_start, seg_len, seg_k, out_start,
+                                    seg_req, max_seg_len, out_pos=None, accumulate=False):
+    """qcf_probe_scores_select with the library's fixed device scratch array instead of a
+    workspace (nothing is allocated; calls that overlap on one GPU race)."""
+    _dev(scores, "scores", torch.float32)
+    _dev(q, "q")
+    _dev(k, "k", q.dtype)
+    for n, t in (("cu_q", cu_q), ("cu_kv", cu_kv), ("ctx_len", ctx_len), ("out_idx", out_idx),
+                 ("seg_start", seg_start), ("seg_len", seg_len), ("seg_k", seg_k),
+                 ("out_start", out_start), ("seg_req", seg_req), ("out_pos", out_pos)):
+        _i32(t, n)
+    if not q.is_contiguous():
+        raise QcfError("q must be dense")
+    nq, hq, d = q.shape
+    T, hkv, d2 = k.shape
+    if d2 != d or scores.numel() != T:
+        raise QcfError("scores must have one entry per row of k; head_dim must match")
+    if out_pos is not None and out_pos.numel() != out_idx.numel():
+        raise QcfError("out_pos must match out_idx")
+    if seg_req.numel() != seg_start.numel():
+        raise QcfError("seg_req needs one request per segment")
+    _invoke("qcf_probe_scores_select_noalloc", _ptr(scores), int(bool(accumulate)), _ptr(q), nq,
+            _ptr(k), T, _rows(k, "k"), _dtype(q), ctx_len.numel(), _ptr(cu_q), _ptr(cu_kv),
+            _ptr(ctx_len), int(max_q_len), int(max_ctx_len), hq, hkv, d, float(softmax_scale),
+            _ptr(out_idx), _ptr(out_pos), out_idx.numel(), seg_start.numel(), _ptr(seg_start),
+            _ptr(seg_len), _ptr(seg_k), _ptr(out_start), _ptr(seg_req), int(max_seg_len))
 
 
 def qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, n_q_heads, n_kv_heads, head_dim,

@@ -41,7 +41,8 @@ def test_every_declared_symbol_is_exported(L):
                          "qcf_gather_rows",
                          "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
                          "qcf_rope_table", "qcf_probe_scores_pic", "qcf_select_topk",
-                         "qcf_probe_scores_select", "qcf_sparse_prefill_attn_workspace_size",
+                         "qcf_probe_scores_select", "qcf_probe_scores_select_noalloc",
+                         "qcf_sparse_prefill_attn_workspace_size",
                          "qcf_sparse_prefill_attn"}
     for name, nargs in decl.items():
         assert hasattr(L, name), name
@@ -187,6 +188,15 @@ def test_scores_select_validation(L):
     assert L.qcf_probe_scores_select(*base(wsb=need - 1)) == WORKSPACE
     # no segments: the scores' own checks alone apply
     assert L.qcf_probe_scores_select(*base(n_seg=0, out=None, req=None, wsb=need - 1)) == WORKSPACE
+
+
+def test_scores_select_noalloc_rejects_oversize_shapes(L):
+    # a shape whose scratch need exceeds the fixed array is refused before anything runs
+    big = L.qcf_probe_scores_workspace_size(64, 128, 65536, 64, 8, 128)
+    assert big > 48 << 20
+    args = [A, 0, A, 64 * 128, A, 64 * 65664, 1024, BF16, 64, A, A, A, 128, 65536, 64, 8, 128, 0.088,
+            A, None, 300, 20, A, A, A, A, A, 512, None]
+    assert L.qcf_probe_scores_select_noalloc(*args) == WORKSPACE
 
 
 def test_topk_and_attn_validation(L):

@@ -78,11 +78,13 @@ def assemble_bytes(step):
 
 
 def scatter_bytes(step):
-    """Fresh rows of R: q, k, v read, rotated q and k plus v written."""
+    """Fresh rows of R: k, v read, rotated k plus v written (and q read, rotated q written when
+    the attention does not rotate the queries itself)."""
     w = step.w
     n = int(step.R_idx.numel())
     es = step.k.element_size()
-    return n * (2 * w.n_q_heads + 4 * w.n_kv_heads) * w.head_dim * es
+    nq = 0 if step.rot_in_attn else 2 * w.n_q_heads
+    return n * (nq + 4 * w.n_kv_heads) * w.head_dim * es
 
 
 def probe_attn_flops(step):

@@ -364,6 +364,36 @@ qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const i
                                    int n_kv_heads, int head_dim, float softmax_scale,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * qcf_sparse_prefill_attn_rope -- qcf_sparse_prefill_attn (bf16, recomputed
+ * rows, no kv_pos) on un-rotated query rows: the kernel turns row r's query by
+ * the rotation of its position row_pos[r] in registers (Section 2.1.3: the
+ * recomputed rows' fresh queries are rotated at their request positions), so
+ * no rotated copy of the queries is written or read.  The rotation is bit for
+ * bit the one qcf_scatter_kv applies to q_new.
+ *   q_raw       [n_q_raw, n_q_heads, head_dim] un-rotated queries
+ *   q_src       int32 [n_rows]: row of q_raw for recomputed row r (values are
+ *               clamped to [0, n_q_raw)), or NULL: row r of q_raw (n_q_raw >= n_rows)
+ *   rope_table  float32 [n_table, head_dim/2, 2] from qcf_rope_table at positions
+ *               0 .. n_table-1 (a constant of theta and head_dim: one table
+ *               serves every layer and request); row_pos[r] must be < n_table
+ *               (larger positions are clamped to the last row: a wrong
+ *               rotation, never an out-of-range read)
+ *   all other arguments as for qcf_sparse_prefill_attn (same workspace size).
+ * QCF_ERR_UNSUPPORTED for float32; QCF_ERR_INVALID_ARG for a missing table.
+ */
+qcf_status qcf_sparse_prefill_attn_rope(void* out, float* lse, const void* q_raw,
+                                        const int32_t* q_src, int64_t n_q_raw,
+                                        const int32_t* row_pos, int64_t n_rows,
+                                        const int32_t* cu_rows, const void* k_cache,
+                                        const void* v_cache, int64_t n_kv_rows,
+                                        int64_t kv_row_stride, const int32_t* cu_kv,
+                                        const float* rope_table, int64_t n_table,
+                                        qcf_dtype dtype, int batch, int max_rows, int max_kv,
+                                        int n_q_heads, int n_kv_heads, int head_dim,
+                                        float softmax_scale, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -380,13 +380,17 @@ size_t qcf_sparse_prefill_attn_workspace_size(int batch, int max_rows, int max_k
   return qcf::attn_workspace(s, dtype == QCF_BF16);
 }
 
-qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
-                                   int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
-                                   const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
-                                   const int32_t* cu_kv, const int32_t* kv_pos, qcf_dtype dtype,
-                                   int batch, int max_rows, int max_kv, int n_q_heads,
-                                   int n_kv_heads, int head_dim, float softmax_scale,
-                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+qcf_status attn_impl(void* out, float* lse, const void* q, const int32_t* row_pos, int64_t n_rows,
+                     const int32_t* cu_rows, const void* k_cache, const void* v_cache,
+                     int64_t n_kv_rows, int64_t kv_row_stride, const int32_t* cu_kv,
+                     const int32_t* kv_pos, qcf_dtype dtype, int batch, int max_rows, int max_kv,
+                     int n_q_heads, int n_kv_heads, int head_dim, float softmax_scale,
+                     void* workspace, size_t workspace_bytes, hipStream_t stream,
+                     const qcf::QueryRot& qrot) {
   if (!dtype_ok(dtype)) return QCF_ERR_UNSUPPORTED;
   qcf_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
   if (st != QCF_OK) return st;
@@ -404,6 +408,13 @@ qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const i
     return QCF_ERR_INVALID_ARG;
   if (lse && !index_ok(lse, false)) return QCF_ERR_INVALID_ARG;
   if (kv_pos && !index_ok(kv_pos, false)) return QCF_ERR_INVALID_ARG;
+  if (qrot.table) {
+    if (dtype != QCF_BF16 || kv_pos) return QCF_ERR_UNSUPPORTED;
+    if (!tensor_ok(qrot.table, empty) || qrot.n_table <= 0 || qrot.n_table > INT32_MAX)
+      return QCF_ERR_INVALID_ARG;
+    if (qrot.src && (!index_ok(qrot.src, empty) || qrot.n_src <= 0 || qrot.n_src > INT32_MAX))
+      return QCF_ERR_INVALID_ARG;
+  }
   if (empty) return QCF_OK;
   if (dtype == QCF_F32 && n_rows > 0x7fffffff) return QCF_ERR_UNSUPPORTED;
   const size_t need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, n_q_heads,
@@ -413,7 +424,44 @@ qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const i
   qcf::AttnShape s{batch, max_rows, max_kv, n_q_heads, n_kv_heads, head_dim};
   return hip_status(qcf::launch_sparse_attn(out, lse, q, row_pos, n_rows, cu_rows, k_cache, v_cache,
                                             n_kv_rows, kv_row_stride, cu_kv, kv_pos,
-                                            dtype == QCF_BF16, s, softmax_scale, workspace, stream));
+                                            dtype == QCF_BF16, s, softmax_scale, workspace, stream,
+                                            qrot));
+}
+
+}  // namespace
+
+extern "C" {
+
+qcf_status qcf_sparse_prefill_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
+                                   int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
+                                   const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
+                                   const int32_t* cu_kv, const int32_t* kv_pos, qcf_dtype dtype,
+                                   int batch, int max_rows, int max_kv, int n_q_heads,
+                                   int n_kv_heads, int head_dim, float softmax_scale,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return attn_impl(out, lse, q, row_pos, n_rows, cu_rows, k_cache, v_cache, n_kv_rows,
+                   kv_row_stride, cu_kv, kv_pos, dtype, batch, max_rows, max_kv, n_q_heads,
+                   n_kv_heads, head_dim, softmax_scale, workspace, workspace_bytes, stream,
+                   qcf::QueryRot{nullptr, 0, nullptr, 0});
+}
+
+qcf_status qcf_sparse_prefill_attn_rope(void* out, float* lse, const void* q_raw,
+                                        const int32_t* q_src, int64_t n_q_raw,
+                                        const int32_t* row_pos, int64_t n_rows,
+                                        const int32_t* cu_rows, const void* k_cache,
+                                        const void* v_cache, int64_t n_kv_rows,
+                                        int64_t kv_row_stride, const int32_t* cu_kv,
+                                        const float* rope_table, int64_t n_table,
+                                        qcf_dtype dtype, int batch, int max_rows, int max_kv,
+                                        int n_q_heads, int n_kv_heads, int head_dim,
+                                        float softmax_scale, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  if (!rope_table) return QCF_ERR_INVALID_ARG;
+  if (!q_src && n_q_raw < n_rows) return QCF_ERR_INVALID_ARG;
+  return attn_impl(out, lse, q_raw, row_pos, n_rows, cu_rows, k_cache, v_cache, n_kv_rows,
+                   kv_row_stride, cu_kv, nullptr, dtype, batch, max_rows, max_kv, n_q_heads,
+                   n_kv_heads, head_dim, softmax_scale, workspace, workspace_bytes, stream,
+                   qcf::QueryRot{q_src, q_src ? n_q_raw : n_rows, rope_table, n_table});
 }
 
 }  // extern "C"

@@ -402,14 +402,44 @@ constexpr int kPlanInts = kPlanBndOff + kStreamBlocks + 1;
 // a block that starts several tiles gets fewer key steps.
 constexpr int kSegCost = 4;
 
-template <int D, bool kStream>
+// Turns a lane's query fragments by the rotation of its row's position (Section
+// 2.1.3: a recomputed row's fresh query is rotated at its request position).  The
+// lane holds pieces 16 st + 8 hi + e (e < 8) of slots st < D/16; rotate-half pairs
+// (j, j + D/2) sit in slots st and st + D/32 of the same lane.  tr is the row's
+// D/2 (cos, sin) pairs of qcf_rope_table, and the arithmetic is rope_pair's, so
+// the result is bit for bit the scatter's rotated query.
+template <int D>
+__device__ __forceinline__ void rotate_query(bf16x8 (&qr)[D / 16], const float2* __restrict__ tr,
+                                             int hi) {
+  constexpr int H = D / 32;
+#pragma unroll
+  for (int st = 0; st < H; ++st) {
+    const float4* t4 = reinterpret_cast<const float4*>(tr + 16 * st + 8 * hi);
+    float4 c4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) c4[i] = t4[i];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float4 c = c4[e >> 1];
+      const float2 cs = (e & 1) ? make_float2(c.z, c.w) : make_float2(c.x, c.y);
+      float y1, y2;
+      rope_pair((float)qr[st][e], (float)qr[st + H][e], cs, y1, y2);
+      qr[st][e] = (__bf16)y1;
+      qr[st + H][e] = (__bf16)y2;
+    }
+  }
+}
+
+template <int D, bool kStream, bool kRot>
 __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, const uint16_t* __restrict__ q,
     const int32_t* __restrict__ row_pos, int64_t n_rows, const int32_t* __restrict__ cu_rows,
     const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int64_t n_kv_rows,
     int64_t kv_stride, const int32_t* __restrict__ cu_kv, int batch, int max_tiles, int hkv,
     int hq, int lg, float scale2, int nbg, int32_t* __restrict__ plan_out,
-    uint16_t* __restrict__ part_o, float2* __restrict__ part_ml) {
+    uint16_t* __restrict__ part_o, float2* __restrict__ part_ml,
+    const int32_t* __restrict__ q_src, int64_t n_q_src, const float2* __restrict__ rtab,
+    int n_tab) {
   constexpr int KCH = D / 8 + 1, VCH = D / 8 + 4;  // 16-byte chunks per LDS row (padded)
   constexpr int KSTR = KCH * 8, VSTR = VCH * 8;    // bf16 elements per LDS row
   constexpr int KST = kKT * KSTR, VST = kKT * VSTR;  // elements per stage
@@ -503,10 +533,14 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     const int pos_raw = row_pos[crow];
     bf16x8 qreg[D / 16];
     {
-      const uint16_t* qp = q + crow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
+      // with kRot the query rows are un-rotated, read through q_src when it is given
+      int64_t qrow = crow;
+      if (kRot && q_src) qrow = min(max((int64_t)q_src[crow], (int64_t)0), n_q_src - 1);
+      const uint16_t* qp = q + qrow * (int64_t)hq * D + (int64_t)head * D + 8 * hi;
 #pragma unroll
       for (int st = 0; st < D / 16; ++st) qreg[st] = as_bf16x8(ld16(qp + 16 * st));
     }
+    if (kRot) rotate_query<D>(qreg, rtab + (int64_t)min(max(pos_raw, 0), n_tab - 1) * (D / 2), hi);
     const int qpos = valid ? pos_raw : INT_MIN;
     const int wmax = wave_max_i(valid ? qpos : -1);
     const int wmin = wave_min_i(valid ? qpos : INT_MAX);
@@ -1090,8 +1124,12 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
                               int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
                               const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
                               const int32_t* cu_kv, const int32_t* kv_pos, bool bf16,
-                              const AttnShape& s, float scale, void* ws, hipStream_t stream) {
+                              const AttnShape& s, float scale, void* ws, hipStream_t stream,
+                              const QueryRot& qrot) {
   if (n_rows == 0 || s.batch == 0 || s.max_rows == 0) return hipSuccess;
+  const bool rot = qrot.table != nullptr;
+  if (rot && (!bf16 || kv_pos)) return hipErrorInvalidValue;
+  const float2* rtab = reinterpret_cast<const float2*>(qrot.table);
   const float scale2 = scale * kLog2e;
   int lg = 0;
   while ((1 << lg) < s.hq / s.hkv) ++lg;
@@ -1106,30 +1144,38 @@ hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_
       uint16_t* part_o = reinterpret_cast<uint16_t*>(wb + L.o_off);
       float2* part_ml = reinterpret_cast<float2*>(wb + L.ml_off);
       dim3 grid((unsigned)(L.nbg * s.hkv));
-#define QCF_W8S(D)                                                                                \
-  attn_w8_kernel<D, true><<<grid, kW8 * 64, 0, stream>>>(                                         \
+#define QCF_W8S(D, R)                                                                             \
+  attn_w8_kernel<D, true, R><<<grid, kW8 * 64, 0, stream>>>(                                      \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
       kv_row_stride, cu_kv, s.batch, max_tiles, s.hkv, s.hq, lg, scale2, L.nbg, plan, part_o,     \
-      part_ml);                                                                                   \
+      part_ml, qrot.src, qrot.n_src, rtab, (int)qrot.n_table);                                    \
   attn_stream_merge_kernel<D><<<dim3((unsigned)(4 * max_tiles * s.batch * s.hkv)), kThreads, 0,   \
                                  stream>>>(static_cast<uint16_t*>(out), lse, n_rows, cu_rows,      \
                                            s.batch, max_tiles, s.hkv, s.hq, lg, L.nbg, plan,       \
                                            part_o, part_ml)
-      if (s.d == 64) { QCF_W8S(64); } else { QCF_W8S(128); }
+      if (s.d == 64) {
+        if (rot) { QCF_W8S(64, true); } else { QCF_W8S(64, false); }
+      } else {
+        if (rot) { QCF_W8S(128, true); } else { QCF_W8S(128, false); }
+      }
 #undef QCF_W8S
       return hipGetLastError();
     }
     const int64_t nblocks = (int64_t)max_tiles * s.batch * s.hkv;
     if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
     dim3 grid((unsigned)nblocks);
-#define QCF_W8(D)                                                                                 \
-  attn_w8_kernel<D, false><<<grid, kW8 * 64, 0, stream>>>(                                        \
+#define QCF_W8(D, R)                                                                              \
+  attn_w8_kernel<D, false, R><<<grid, kW8 * 64, 0, stream>>>(                                     \
       static_cast<uint16_t*>(out), lse, static_cast<const uint16_t*>(q), row_pos, n_rows, cu_rows, \
       static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), n_kv_rows,    \
       kv_row_stride, cu_kv, s.batch, max_tiles, s.hkv, s.hq, lg, scale2, 0, nullptr, nullptr,     \
-      nullptr)
-    if (s.d == 64) QCF_W8(64); else QCF_W8(128);
+      nullptr, qrot.src, qrot.n_src, rtab, (int)qrot.n_table)
+    if (s.d == 64) {
+      if (rot) QCF_W8(64, true); else QCF_W8(64, false);
+    } else {
+      if (rot) QCF_W8(128, true); else QCF_W8(128, false);
+    }
 #undef QCF_W8
     return hipGetLastError();
   }

@@ -103,11 +103,22 @@ hipError_t launch_probe_scores(float* scores, int accumulate, const void* q, int
 struct AttnShape {
   int batch, max_rows, max_kv, hq, hkv, d;
 };
+// Un-rotated queries: the rows of q are turned in the kernel by table row
+// row_pos[r] (table from qcf_rope_table at positions 0..n_table-1), read
+// through src[r] when src is given (n_src rows of q).  table == nullptr: q is
+// already rotated and indexed by r.
+struct QueryRot {
+  const int32_t* src;
+  int64_t n_src;
+  const float* table;
+  int64_t n_table;
+};
 size_t attn_workspace(const AttnShape& s, bool bf16);
 hipError_t launch_sparse_attn(void* out, float* lse, const void* q, const int32_t* row_pos,
                               int64_t n_rows, const int32_t* cu_rows, const void* k_cache,
                               const void* v_cache, int64_t n_kv_rows, int64_t kv_row_stride,
                               const int32_t* cu_kv, const int32_t* kv_pos, bool bf16,
-                              const AttnShape& s, float scale, void* ws, hipStream_t stream);
+                              const AttnShape& s, float scale, void* ws, hipStream_t stream,
+                              const QueryRot& qrot = QueryRot{nullptr, 0, nullptr, 0});
 
 }  // namespace qcf

@@ -20,7 +20,7 @@ __all__ = [
     "qcf_assemble", "qcf_gather_rows", "qcf_scatter_kv", "qcf_probe_scores", "qcf_probe_scores_workspace_size",
     "qcf_rope_table", "qcf_probe_scores_pic",
     "qcf_select_topk", "qcf_probe_scores_select", "qcf_probe_scores_select_noalloc",
-    "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_workspace_size",
+    "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_rope", "rope_position_table", "qcf_sparse_prefill_attn_workspace_size",
     "EXPORTS", "Prepared", "prepare",
 ]
 
@@ -59,6 +59,9 @@ EXPORTS = {
                                              _I, _I, _I, _I, ctypes.c_float, _P, _P, _I64, _I, _P, _P,
                                              _P, _P, _P, _I, _P]),
     "qcf_sparse_prefill_attn_workspace_size": (_SZ, [_I, _I, _I, _I, _I, _I, _I]),
+    "qcf_sparse_prefill_attn_rope": (_I, [_P, _P, _P, _P, _I64, _P, _I64, _P, _P, _P, _I64, _I64, _P,
+                                          _P, _I64, _I, _I, _I, _I, _I, _I, _I, ctypes.c_float, _P,
+                                          _SZ, _P]),
     "qcf_sparse_prefill_attn": (_I, [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I, _I,
                                      _I, _I, _I, _I, _I, ctypes.c_float, _P, _SZ, _P]),
 }
@@ -486,3 +489,51 @@ def qcf_sparse_prefill_attn(out, q, row_pos, cu_rows, k_cache, v_cache, cu_kv, m
                                        _ptr(cu_kv), _ptr(kv_pos), _dtype(q), batch, int(max_rows),
                                        int(max_kv), hq, hkv, d, float(softmax_scale), _ptr(workspace),
                                        0 if workspace is None else workspace.numel(), keep=workspace)
+
+
+def rope_position_table(n_pos, head_dim, rope_theta, device="cuda"):
+    """The (cos, sin) table of positions 0..n_pos-1 that qcf_sparse_prefill_attn_rope reads
+    (qcf_rope_table at those positions; a constant of theta and head_dim)."""
+    pos = torch.arange(n_pos, dtype=torch.int32, device=device)
+    table = torch.empty((n_pos, head_dim // 2, 2), dtype=torch.float32, device=device)
+    qcf_rope_table(table, pos, rope_theta)
+    return table
+
+
+def qcf_sparse_prefill_attn_rope(out, q_raw, row_pos, cu_rows, k_cache, v_cache, cu_kv, max_rows,
+                                 max_kv, softmax_scale, rope_table, q_src=None, lse=None,
+                                 workspace=None):
+    """qcf_sparse_prefill_attn on un-rotated query rows (read through q_src when given), turned
+    in the kernel by rope_table[row_pos[r]]."""
+    _dev(out, "out", torch.bfloat16)
+    _dev(q_raw, "q_raw", torch.bfloat16)
+    _dev(k_cache, "k_cache", torch.bfloat16)
+    _dev(v_cache, "v_cache", torch.bfloat16)
+    _dev(rope_table, "rope_table", torch.float32)
+    _dev(lse, "lse", torch.float32)
+    for n, t in (("row_pos", row_pos), ("cu_rows", cu_rows), ("cu_kv", cu_kv), ("q_src", q_src)):
+        _i32(t, n)
+    if not (q_raw.is_contiguous() and out.is_contiguous() and rope_table.is_contiguous()):
+        raise QcfError("q_raw, out and rope_table must be dense")
+    n, hq, d = out.shape
+    nq_raw = q_raw.shape[0]
+    T, hkv, d2 = k_cache.shape
+    if q_raw.shape[1:] != (hq, d) or rope_table.shape[1:] != (d // 2, 2):
+        raise QcfError("q_raw must be [rows, H_q, d] and rope_table [positions, d/2, 2]")
+    if v_cache.shape != k_cache.shape or v_cache.stride(0) != k_cache.stride(0) or d2 != d:
+        raise QcfError("k_cache/v_cache mismatch")
+    if row_pos.numel() != n or (q_src is not None and q_src.numel() != n):
+        raise QcfError("row_pos (and q_src) must have one entry per recomputed row")
+    if q_src is None and nq_raw < n:
+        raise QcfError("without q_src, q_raw needs a row per recomputed row")
+    if lse is not None and lse.shape != (n, hq):
+        raise QcfError("lse must be [n_rows, H_q]")
+    batch = cu_rows.numel() - 1
+    need = qcf_sparse_prefill_attn_workspace_size(batch, max_rows, max_kv, hq, hkv, d, torch.bfloat16)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=out.device)
+    _invoke("qcf_sparse_prefill_attn_rope", _ptr(out), _ptr(lse), _ptr(q_raw), _ptr(q_src), nq_raw,
+            _ptr(row_pos), n, _ptr(cu_rows), _ptr(k_cache), _ptr(v_cache), T, _rows(k_cache, "k_cache"),
+            _ptr(cu_kv), _ptr(rope_table), rope_table.shape[0], _dtype(out), batch, int(max_rows),
+            int(max_kv), hq, hkv, d, float(softmax_scale), _ptr(workspace),
+            0 if workspace is None else workspace.numel(), keep=workspace)

@@ -92,7 +92,10 @@ class FusionStack:
         self.scores = torch.zeros(T, dtype=torch.float32, device=dev)
         self.R_idx = self.R_idx_init.clone()
         self.R_pos = self.R_pos_init.clone()
-        self.q_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
+        # bf16: the recompute's attention rotates the queries itself (table of every position)
+        self.pos_table = (qcf.rope_position_table(max(self.max_kv_rows(sw), 1), d, sw.rope_theta, dev)
+                          if dt == torch.bfloat16 else None)
+        self.q_R = torch.empty((nR, hq, d), dtype=dt, device=dev) if self.pos_table is None else None
         self.o_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
         self.max_kv = int(np.diff(sw.cu_kv).max()) if sw.batch else 1
         nws = qcf.qcf_probe_scores_workspace_size(sw.batch, p.max_q, p.max_ctx, hq, hkv, d)
@@ -109,6 +112,10 @@ class FusionStack:
         # tr_pic[l] (offline chunk pass), tr_sel[l] (query probe), tr_rec[l] (recompute)
         self.trace: set = set()
         self.tr_pic, self.tr_sel, self.tr_rec = {}, {}, {}
+
+    @staticmethod
+    def max_kv_rows(sw):
+        return int(np.diff(sw.cu_kv).max()) if sw.batch else 1
 
     # -- glue: RMSNorm, projections, residual (torch) ---------------------------
     def _qkv(self, l, h):
@@ -222,15 +229,30 @@ class FusionStack:
                                p.max_seg, sw.rope_theta, v_out=self.v_req[l], v_in=vp)
                 src.release(l)
             q, k, v = self._qkv(l, hR)
-            qcf.qcf_scatter_kv(self.k_req[l], self.v_req[l], k, v, self.R_idx, self.R_pos, sw.rope_theta,
-                               q_new=q, q_out=self.q_R)
-            qcf.qcf_sparse_prefill_attn(self.o_R, self.q_R, self.R_pos, self.cu_R, self.k_req[l],
-                                        self.v_req[l], self.cu_kv, p.max_R, self.max_kv, self.scale,
-                                        workspace=self.ws_attn)
+            if self.pos_table is not None:
+                # fresh K/V into the cache; the attention rotates the queries itself
+                qcf.qcf_scatter_kv(self.k_req[l], self.v_req[l], k, v, self.R_idx, self.R_pos,
+                                   sw.rope_theta)
+                qcf.qcf_sparse_prefill_attn_rope(self.o_R, q, self.R_pos, self.cu_R, self.k_req[l],
+                                                 self.v_req[l], self.cu_kv, p.max_R, self.max_kv,
+                                                 self.scale, self.pos_table, workspace=self.ws_attn)
+            else:
+                qcf.qcf_scatter_kv(self.k_req[l], self.v_req[l], k, v, self.R_idx, self.R_pos,
+                                   sw.rope_theta, q_new=q, q_out=self.q_R)
+                qcf.qcf_sparse_prefill_attn(self.o_R, self.q_R, self.R_pos, self.cu_R, self.k_req[l],
+                                            self.v_req[l], self.cu_kv, p.max_R, self.max_kv, self.scale,
+                                            workspace=self.ws_attn)
             h_in = hR
             hR = self._residual(l, hR, self.o_R)
             if l in self.trace:
-                self.tr_rec[l] = dict(h=h_in.clone(), q_raw=q.clone(), k_raw=k.clone(), q=self.q_R.clone(),
+                q_rot = self.q_R
+                if self.pos_table is not None:
+                    # the rotated queries are not stored by this flow: the scatter forms them
+                    # for the record (the same K/V rows are written again)
+                    q_rot = torch.empty_like(q)
+                    qcf.qcf_scatter_kv(self.k_req[l], self.v_req[l], k, v, self.R_idx, self.R_pos,
+                                       sw.rope_theta, q_new=q, q_out=q_rot)
+                self.tr_rec[l] = dict(h=h_in.clone(), q_raw=q.clone(), k_raw=k.clone(), q=q_rot.clone(),
                                       o=self.o_R.clone(), h_out=hR.clone())
         self.h_R = hR
 

@@ -166,7 +166,10 @@ class FusionStep:
     """
 
     def __init__(self, w, rho_bp: int | None = None, device="cuda", fused: bool = False,
-                 selection: str = "chunk", fused_select: bool = True):
+                 selection: str = "chunk", fused_select: bool = True, rot_in_attn: bool = True):
+        """``rot_in_attn`` (bf16): the recomputed rows' queries are rotated inside the
+        attention (qcf_sparse_prefill_attn_rope, reading q_new through R_idx) and the scatter
+        writes K/V only; otherwise the scatter writes rotated queries q_R for the attention."""
         self.w = w
         self.fused = bool(fused)
         # scores and selection through qcf_probe_scores_select (one launch less) or the two calls
@@ -176,6 +179,7 @@ class FusionStep:
         self.plan = p = FusionPlan.build(w, self.rho_bp, selection)
         dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.dtype = dt
+        self.rot_in_attn = bool(rot_in_attn) and dt == torch.bfloat16
         dev = torch.device(device)
         self.device = dev
         T, hq, hkv, d = w.n_rows, w.n_q_heads, w.n_kv_heads, w.head_dim
@@ -207,7 +211,7 @@ class FusionStep:
         self.R_pos = self.R_pos_init.clone()
         nU, nR, nP = p.u_idx.size, p.R_idx_init.size, p.probe_idx.size
         self.q_u = torch.empty((nU, hq, d), dtype=dt, device=dev)
-        self.q_R = torch.empty((nR, hq, d), dtype=dt, device=dev)
+        self.q_R = None if self.rot_in_attn else torch.empty((nR, hq, d), dtype=dt, device=dev)
         self.k_probe = kv_buffer(nP, hkv, d, dt, dev)
         self.v_probe = kv_buffer(nP, hkv, d, dt, dev)
         self.o_probe = torch.empty((nU, hq, d), dtype=dt, device=dev)
@@ -222,6 +226,9 @@ class FusionStep:
         nwp = qcf.qcf_sparse_prefill_attn_workspace_size(w.batch, p.max_q, max(p.max_probe, 1), hq,
                                                          hkv, d, dt)
         self.ws_probe = torch.empty(max(nwp, 256), dtype=torch.uint8, device=dev)
+        # (cos, sin) of every request position, for the attention's query rotation
+        self.pos_table = (qcf.rope_position_table(max(self.max_kv, 1), d, w.rope_theta, dev)
+                          if self.rot_in_attn else None)
         # the anchor probe depends only on the assembled buffers and nothing later in the
         # step reads its output, so it runs on a second stream (default priority) beside
         # the score -> select -> scatter chain and is joined at the end of the step
@@ -323,15 +330,24 @@ class FusionStep:
                    pos_base=self.pos_base)
 
     def stage_scatter(self):
-        self._call("scatter", qcf.qcf_scatter_kv, self.k, self.v, self.k_new, self.v_new,
-                   self.R_idx, self.R_pos, self.w.rope_theta, q_new=self.q_new, q_out=self.q_R,
-                   src_idx=self.R_idx)
+        if self.rot_in_attn:
+            self._call("scatter", qcf.qcf_scatter_kv, self.k, self.v, self.k_new, self.v_new,
+                       self.R_idx, self.R_pos, self.w.rope_theta, src_idx=self.R_idx)
+        else:
+            self._call("scatter", qcf.qcf_scatter_kv, self.k, self.v, self.k_new, self.v_new,
+                       self.R_idx, self.R_pos, self.w.rope_theta, q_new=self.q_new, q_out=self.q_R,
+                       src_idx=self.R_idx)
 
     def stage_attn(self):
         p = self.plan
-        self._call("attn", qcf.qcf_sparse_prefill_attn, self.o, self.q_R, self.R_pos, self.cu_R,
-                   self.k, self.v, self.cu_kv, p.max_R, self.max_kv, self.scale,
-                   workspace=self.ws_attn)
+        if self.rot_in_attn:
+            self._call("attn", qcf.qcf_sparse_prefill_attn_rope, self.o, self.q_new, self.R_pos,
+                       self.cu_R, self.k, self.v, self.cu_kv, p.max_R, self.max_kv, self.scale,
+                       self.pos_table, q_src=self.R_idx, workspace=self.ws_attn)
+        else:
+            self._call("attn", qcf.qcf_sparse_prefill_attn, self.o, self.q_R, self.R_pos, self.cu_R,
+                       self.k, self.v, self.cu_kv, p.max_R, self.max_kv, self.scale,
+                       workspace=self.ws_attn)
 
     STAGES = ("assemble", "probe_attn", "scores_select", "scatter", "attn")
     STAGES_FUSED = ("rope_table", "rerope", "query_assemble", "probe_attn", "scores_pic", "select",
@@ -419,4 +435,4 @@ class FusionStep:
         return dict(k_fuse=c(self.k), v_fuse=c(self.v), scores=self.scores.double().cpu().numpy(),
                     R=R, R_pos=Rp, P=P, cu_R=p.cu_R, o=c(self.o), o_probe=op,
                     o_probe_list=[op[cq[b]:cq[b + 1]] for b in range(self.w.batch)],
-                    q_u=c(self.q_u), q_R=c(self.q_R))
+                    q_u=c(self.q_u), **({} if self.rot_in_attn else dict(q_R=c(self.q_R))))

@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported(L):
                          "qcf_scatter_kv", "qcf_probe_scores_workspace_size", "qcf_probe_scores",
                          "qcf_rope_table", "qcf_probe_scores_pic", "qcf_select_topk",
                          "qcf_probe_scores_select", "qcf_probe_scores_select_noalloc",
-                         "qcf_sparse_prefill_attn_workspace_size",
+                         "qcf_sparse_prefill_attn_workspace_size", "qcf_sparse_prefill_attn_rope",
                          "qcf_sparse_prefill_attn"}
     for name, nargs in decl.items():
         assert hasattr(L, name), name
@@ -206,6 +206,15 @@ def test_topk_and_attn_validation(L):
     a = lambda **kw: [A, None, A, A, kw.get("n", 10), A, A, A, 100, kw.get("stride", 1024), A, None,
                       kw.get("dt", BF16), 1, 10, 100, kw.get("hq", 32), 8, 128, 0.088, None, 0, None]
     assert L.qcf_sparse_prefill_attn(*a(dt=3)) == UNSUPPORTED
+    r = lambda **kw: [A, None, A, kw.get("src", A), kw.get("nraw", 10), A, 10, A, A, A, 100, 1024, A,
+                      kw.get("tab", A), kw.get("ntab", 100), kw.get("dt", BF16), 1, 10, 100, 32, 8, 128,
+                      0.088, None, 0, None]
+    assert L.qcf_sparse_prefill_attn_rope(*r(tab=None)) == INVALID
+    assert L.qcf_sparse_prefill_attn_rope(*r(ntab=0)) == INVALID
+    assert L.qcf_sparse_prefill_attn_rope(*r(src=MIS + 1)) == INVALID
+    assert L.qcf_sparse_prefill_attn_rope(*r(src=None, nraw=9)) == INVALID
+    assert L.qcf_sparse_prefill_attn_rope(*r(dt=F32)) == UNSUPPORTED
+    assert L.qcf_sparse_prefill_attn_rope(*r(tab=MIS)) == INVALID
     assert L.qcf_sparse_prefill_attn(*a(hq=36)) == INVALID
     assert L.qcf_sparse_prefill_attn(*a(stride=1000)) == INVALID
     assert L.qcf_sparse_prefill_attn(*a(n=-2)) == INVALID

@@ -117,7 +117,7 @@ def test_fused_assembly_matches_separate_calls(name):
     b = FusionStep(w, fused=False)
     b.run()
     g2 = b.results()
-    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u", "q_R"):
+    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u"):
         np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)
     assert torch.equal(a.k_probe, b.k_probe) and torch.equal(a.v_probe, b.v_probe)
 
@@ -135,7 +135,7 @@ def test_fused_scores_flow_matches_unfused(name, dtype):
     for _ in range(3):               # no synchronisation between the steps
         b.run()
     g2 = b.results()
-    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u", "q_R"):
+    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u"):
         np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)
     assert torch.equal(a.k_probe, b.k_probe) and torch.equal(a.v_probe, b.v_probe)
 
@@ -201,3 +201,21 @@ def test_scores_select_matches_separate_calls(name, selection, rho_bp):
     np.testing.assert_array_equal(a.scores.cpu().numpy(), b.scores.cpu().numpy())
     np.testing.assert_array_equal(a.R_idx.cpu().numpy(), b.R_idx.cpu().numpy())
     np.testing.assert_array_equal(a.R_pos.cpu().numpy(), b.R_pos.cpu().numpy())
+
+
+@pytest.mark.parametrize("name,kw", [("c2", {}), ("c4", {}), ("c5", {}),
+                                     ("c2", dict(chunk_lens=[[300, 212], [64], [129, 1, 511, 40]],
+                                                 q_lens=[5, 64, 17], anchors_per_chunk=3))])
+def test_query_rotation_in_attention_is_bit_identical(name, kw):
+    """The attention turning q_new's rows in registers (qcf_sparse_prefill_attn_rope) gives
+    the bits of the scatter writing rotated queries that the attention then reads."""
+    w = make_workload(name, **kw)
+    say(w.name, "rows", w.n_rows, "query rotation in the attention vs in the scatter")
+    a = FusionStep(w, rot_in_attn=False)
+    a.run()
+    g1 = a.results()
+    b = FusionStep(w, rot_in_attn=True)
+    b.run()
+    g2 = b.results()
+    for key in ("k_fuse", "v_fuse", "scores", "R", "R_pos", "o", "o_probe", "q_u"):
+        np.testing.assert_array_equal(g1[key], g2[key], err_msg=key)

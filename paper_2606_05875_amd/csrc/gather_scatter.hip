@@ -115,12 +115,88 @@ __global__ __launch_bounds__(kThreads) void scatter_kv_kernel(
   }
 }
 
+// The scatter without queries (fresh K/V only): four rows per block, 64
+// threads per row.  A thread loads its row's key rotate-half units and value
+// chunks of a round (for bf16 with 8 x 128 key heads: one unit and two chunks,
+// the whole row in one round), forms one (cos, sin) pair of the row meanwhile,
+// and stores after the block's table is complete.  Same rotation arithmetic as
+// scatter_kv_kernel, so the same bits.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void scatter_kv_rows_kernel(
+    T* k_cache, T* v_cache, int64_t n_cache_rows, int64_t cache_stride, const T* k_new,
+    const T* v_new, int64_t n_src_rows, const int32_t* src_idx, const int32_t* __restrict__ row_idx,
+    const int32_t* __restrict__ row_pos, int64_t n_rows, int hkv, double theta) {
+  constexpr int HALF = D / 2;
+  constexpr int VEC = Vec16<T>::N;
+  constexpr int UPH = HALF / VEC;
+  constexpr int TPR = 64, RPB = kThreads / TPR;
+  constexpr int KR = sizeof(T) == 2 ? 1 : 2, VR = 2 * KR;  // units per thread and round
+  __shared__ float2 cs[RPB][HALF];
+  const int sub = threadIdx.x / TPR, lt = threadIdx.x % TPR;
+  const int64_t r = (int64_t)blockIdx.x * RPB + sub;
+  const int64_t rc = min(r, n_rows - 1);
+  const int64_t s = src_idx ? (int64_t)src_idx[rc] : rc;
+  const bool s_ok = s >= 0 && s < n_src_rows;
+  const int64_t dst = row_idx[rc];
+  const bool ok = r < n_rows && s_ok && dst >= 0 && dst < n_cache_rows;
+  const int kv_row = hkv * D;
+  const int nv = kv_row / VEC, nk = hkv * UPH;
+  const T* vs = v_new + (s_ok ? s : 0) * kv_row;
+  const T* ks = k_new + (s_ok ? s : 0) * kv_row;
+  T* vd = v_cache + (ok ? dst : 0) * cache_stride;
+  T* kd = k_cache + (ok ? dst : 0) * cache_stride;
+  for (int round = 0; round * TPR * KR < nk || round * TPR * VR < nv; ++round) {
+    uint4 vb[VR], ka[KR], kb[KR];
+    int koff[KR], kj[KR];
+#pragma unroll
+    for (int i = 0; i < VR; ++i) vb[i] = ld16(vs + min(round * TPR * VR + lt + TPR * i, nv - 1) * VEC);
+#pragma unroll
+    for (int i = 0; i < KR; ++i) {
+      const int u = min(round * TPR * KR + lt + TPR * i, nk - 1);
+      const int h = u / UPH;
+      kj[i] = (u - h * UPH) * VEC;
+      koff[i] = h * D + kj[i];
+      ka[i] = ld16(ks + koff[i]);
+      kb[i] = ld16(ks + koff[i] + HALF);
+    }
+    if (round == 0) {
+      for (int j = lt; j < HALF; j += TPR) cs[sub][j] = rope_cs((double)row_pos[rc], j, D, theta);
+      __syncthreads();
+    }
+    if (!ok) continue;
+#pragma unroll
+    for (int i = 0; i < VR; ++i) {
+      const int c = round * TPR * VR + lt + TPR * i;
+      if (c < nv) st16(vd + c * VEC, vb[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < KR; ++i) {
+      if (round * TPR * KR + lt + TPR * i >= nk) continue;
+      float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
+      Vec16<T>::unpack(ka[i], x1);
+      Vec16<T>::unpack(kb[i], x2);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) rope_pair(x1[e], x2[e], cs[sub][kj[i] + e], y1[e], y2[e]);
+      st16(kd + koff[i], Vec16<T>::pack(y1));
+      st16(kd + koff[i] + HALF, Vec16<T>::pack(y2));
+    }
+  }
+}
+
 template <typename T, int D>
 hipError_t scatter_t(void* k_cache, void* v_cache, int64_t n_cache_rows, int64_t cache_stride,
                      const void* k_new, const void* v_new, const void* q_new, void* q_out,
                      int64_t n_src_rows, const int32_t* src_idx, int64_t n_rows,
                      const int32_t* row_idx, const int32_t* row_pos, int hq, int hkv,
                      double theta, hipStream_t stream) {
+  if (!q_new && !q_out) {
+    constexpr int RPB = kThreads / 64;
+    scatter_kv_rows_kernel<T, D><<<dim3((unsigned)((n_rows + RPB - 1) / RPB)), kThreads, 0, stream>>>(
+        static_cast<T*>(k_cache), static_cast<T*>(v_cache), n_cache_rows, cache_stride,
+        static_cast<const T*>(k_new), static_cast<const T*>(v_new), n_src_rows, src_idx, row_idx,
+        row_pos, n_rows, hkv, theta);
+    return hipGetLastError();
+  }
   scatter_kv_kernel<T, D><<<dim3((unsigned)n_rows), kThreads, 0, stream>>>(
       static_cast<T*>(k_cache), static_cast<T*>(v_cache), n_cache_rows, cache_stride,
       static_cast<const T*>(k_new), static_cast<const T*>(v_new), static_cast<const T*>(q_new),

@@ -182,6 +182,36 @@ def stack_study(args):
         "full_prefill_ms": full}), flush=True)
 
 
+def recompute_study(args):
+    """c3 at rho 30%: the recompute of every layer alone (selection done once before), timed over
+    ``--steps`` runs.  Under a kernel trace the run holds only recompute launches, so its
+    statistics split a layer between libqcf's kernels and the stack's glue (RMSNorm, the
+    projections and the residual product)."""
+    import torch
+    from paper_2606_05875_amd.stack import FusionStack
+    from paper_2606_05875_amd.workloads import make_stack_workload
+
+    torch.cuda.set_device(0)
+    sw = make_stack_workload("c3")
+    st = FusionStack(sw)
+    st.build_pic()
+    st.select()
+    for _ in range(max(1, args.warmup)):
+        st.recompute()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(args.steps):
+        st.recompute()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    n_R = int(st.R_idx.numel())
+    print(json.dumps({"study": "c3 recompute alone", "rho_bp": st.rho_bp, "layers": sw.n_layers,
+                      "recomputed_rows": n_R, "runs": args.steps, "warmup": args.warmup,
+                      "ms_per_recompute": ms, "us_per_layer": ms * 1e3 / sw.n_layers}), flush=True)
+
+
 def pipeline_study(args):
     """c3 with the PIC caches in pinned host memory: each layer's cache loads on a copy
     stream while earlier layers compute (Section 3.5).  Reports the copy-only time, the
@@ -434,6 +464,8 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="the c3 multi-layer stack instead: selection (anchor view vs full view) and "
                          "recompute times, one JSON line (not the headline metric)")
+    ap.add_argument("--recompute-only", action="store_true",
+                    help="with --stack: time the recompute of every layer alone (c3, rho 30%%)")
     ap.add_argument("--pipeline", action="store_true",
                     help="with --stack: the stored chunk caches stream layer by layer from pinned host "
                          "memory (copy-only, compute-only and overlapped times)")
@@ -471,6 +503,8 @@ def main():
     if args.stack:
         if args.anchor_profile:
             return anchor_profile(args)
+        if args.recompute_only:
+            return recompute_study(args)
         return pipeline_study(args) if args.pipeline else stack_study(args)
     from paper_2606_05875_amd.step import FusionStep
     from paper_2606_05875_amd.workloads import make_workload

@@ -121,7 +121,8 @@ class FusionStack:
     def _qkv(self, l, h):
         sw = self.sw
         n = h.shape[0]
-        x = F.rms_norm(h.float(), (h.shape[-1],), eps=sw.rms_eps).to(self.dtype)
+        # float32 statistics inside the kernel, one rounding of the normed row to the storage dtype
+        x = F.rms_norm(h, (h.shape[-1],), eps=sw.rms_eps)
         y = x @ self.wqkv[l]
         nq, nkv = sw.n_q_heads * sw.head_dim, sw.n_kv_heads * sw.head_dim
         q = y[:, :nq].reshape(n, sw.n_q_heads, sw.head_dim)

@@ -663,6 +663,11 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
       bf16x8 pb[2][2];
       if (do_cur) softmax_pre(sc, kt0);
+      // The wave issuing this block (the next tile's products interleaved with this tile's
+      // exponentials, the step's vector-heavy part) goes first at the SIMD's arbiter; the
+      // other wave of the SIMD fills the remaining issue slots, often with its P.V
+      // products (c4 4887 -> 4804 us, c5 -1.8%, bit-identical).
+      __builtin_amdgcn_s_setprio(1);
       if (do_next) {
         const uint16_t* kn = k_lds + ((t + 1) & 3) * KST + krd;
         qk_half(kn, 0, sn[0]);
@@ -676,6 +681,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       } else if (do_cur) {
         softmax_exp(sc, pb);
       }
+      __builtin_amdgcn_s_setprio(0);
       if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
       step_barrier();
     };

@@ -641,12 +641,14 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       }
     };
 
-    // Ring: K(t) and V(t) live in stage t % 4.  Step t issues tile t+3 into the
-    // stage of tile t-1 (its K was last read in step t-2, its V in step t-1),
-    // computes S(t+1) while the softmax of tile t runs, then O += P(t) V(t); at
-    // its end everything issued before step t -- K(t+2) and V(t+1) among it --
-    // has landed.  Past the last tile the transfers still go out (zeros, no
-    // memory traffic), so every step issues the same number of them.
+    // Ring: K(t) and V(t) live in stage t % 4.  Step t computes S(t+1) while the
+    // softmax of tile t runs, then issues tile t+3 into the stage of tile t-1
+    // (its K was last read in step t-2, its V in step t-1), then O += P(t) V(t);
+    // at its end everything issued before step t -- K(t+2) and V(t+1) among it
+    // -- has landed.  Past the last tile the transfers still go out (zeros, no
+    // memory traffic), so every step issues the same number of them.  Issued
+    // at the start of the step instead, the transfers delayed the softmax
+    // (c2 call +4%, c5 +1.5%).
     f32x16 sa[2], sb[2];
     asm volatile("" ::: "memory");
     wait_vm_lgkm0<0>();
@@ -658,7 +660,6 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     }
     auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
       const int kt0 = kt_lo + t * kKT;
-      issue(t + 3);
       const bool do_cur = kt0 < wave_end;
       const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
       bf16x8 pb[2][2];
@@ -682,6 +683,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
         softmax_exp(sc, pb);
       }
       __builtin_amdgcn_s_setprio(0);
+      issue(t + 3);
       if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
       step_barrier();
     };

@@ -44,7 +44,7 @@ struct AssembleArgs {
   double theta;
 };
 
-template <typename T, int D>
+template <typename T, int D, bool kStreamIn>
 __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A) {
   constexpr int HALF = D / 2;
   __shared__ float2 cs[HALF];
@@ -63,9 +63,9 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     // holds them across the float64 work and costs occupancy (measured slower)
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.seg_delta[s], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D, kThreads, kUnits>(A.k_cache, A.v_cache, A.row_stride, A.k_pic, A.v_pic,
-                                       A.pic_stride, s0, d0, min(A.rows_per_block, len - r0),
-                                       A.hkv, A.n_pic_rows, A.n_rows, cs, [] {});
+    remap_rows<T, D, kThreads, kUnits, kStreamIn, true>(
+        A.k_cache, A.v_cache, A.row_stride, A.k_pic, A.v_pic, A.pic_stride, s0, d0,
+        min(A.rows_per_block, len - r0), A.hkv, A.n_pic_rows, A.n_rows, cs, [] {});
     return;
   }
   if (bid < n_remap + A.n_query) {
@@ -78,11 +78,13 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     const int64_t slot = A.query_slot ? (int64_t)A.query_slot[i] : -1;
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.query_pos[i], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D, kThreads, kUnits>(A.k_cache, A.v_cache, A.row_stride, A.k_new, A.v_new, kvw,
-                                       src, row, 1, A.hkv, A.n_src_rows, A.n_rows, cs, [] {});
+    remap_rows<T, D, kThreads, kUnits, false, false>(A.k_cache, A.v_cache, A.row_stride, A.k_new,
+                                                     A.v_new, kvw, src, row, 1, A.hkv,
+                                                     A.n_src_rows, A.n_rows, cs, [] {});
     if (slot >= 0)
-      remap_rows<T, D, kThreads, kUnits>(A.probe_k, A.probe_v, A.probe_stride, A.k_new, A.v_new, kvw,
-                                         src, slot, 1, A.hkv, A.n_src_rows, A.n_probe, cs, [] {});
+      remap_rows<T, D, kThreads, kUnits, false, false>(A.probe_k, A.probe_v, A.probe_stride,
+                                                       A.k_new, A.v_new, kvw, src, slot, 1, A.hkv,
+                                                       A.n_src_rows, A.n_probe, cs, [] {});
     // q: hq heads rotated into q_u[i]
     constexpr int VEC = Vec16<T>::N;
     constexpr int UPH = HALF / VEC;
@@ -112,9 +114,9 @@ __global__ __launch_bounds__(kThreads) void assemble_kernel(AssembleArgs<T, D> A
     if (src < 0) continue;  // a query slot (written by that query row's block)
     if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)A.probe_delta[p], threadIdx.x, D, A.theta);
     __syncthreads();
-    remap_rows<T, D, kThreads, kUnits>(A.probe_k, A.probe_v, A.probe_stride, A.k_pic, A.v_pic,
-                                       A.pic_stride, src, p, 1, A.hkv, A.n_pic_rows, A.n_probe, cs,
-                                       [] {});
+    remap_rows<T, D, kThreads, kUnits, false, false>(A.probe_k, A.probe_v, A.probe_stride,
+                                                     A.k_pic, A.v_pic, A.pic_stride, src, p, 1,
+                                                     A.hkv, A.n_pic_rows, A.n_probe, cs, [] {});
   }
 }
 
@@ -163,7 +165,12 @@ hipError_t assemble_t(const AssembleShape& s, const AssemblePtrs& p, hipStream_t
   const int64_t blocks = n_remap + s.n_query + n_probe_blocks;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  assemble_kernel<T, D><<<dim3((unsigned)blocks), kThreads, 0, stream>>>(A);
+  // the stored chunk caches' K and V bytes
+  const int64_t src_bytes = s.n_pic_rows * (int64_t)s.hkv * D * (int64_t)sizeof(T) * 2;
+  if (src_bytes > kStreamSourceBytes)
+    assemble_kernel<T, D, true><<<dim3((unsigned)blocks), kThreads, 0, stream>>>(A);
+  else
+    assemble_kernel<T, D, false><<<dim3((unsigned)blocks), kThreads, 0, stream>>>(A);
   return hipGetLastError();
 }
 

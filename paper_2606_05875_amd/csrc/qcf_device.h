@@ -54,6 +54,18 @@ template <> struct Vec16<uint16_t> {
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
 
+// The same 16-byte accesses with the non-temporal hint, for streams that should
+// not displace cache lines that the next kernels of a step read again.
+typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16_nt(const void* p) {
+  const u32x4_nt x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+  return make_uint4(x[0], x[1], x[2], x[3]);
+}
+__device__ __forceinline__ void st16_nt(void* p, const uint4& v) {
+  const u32x4_nt x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4_nt*>(p));
+}
+
 // Rotary frequency omega_j = theta^(-2j/d) and the (cos, sin) of p * omega_j,
 // formed in float64 and rounded to float32.
 __device__ __forceinline__ float2 rope_cs(double pos, int j, int d, double theta) {

@@ -16,8 +16,10 @@ namespace qcf {
 // loads are in flight, so the float64 angle work overlaps them; every thread of
 // the block must call this function with the same nrows.  A unit is read and
 // written by the same thread, so in-place calls (same buffers, same rows) are
-// safe.
-template <typename T, int D, int kThreads, int kUnits, typename MakeCs>
+// safe.  kStreamIn reads the sources with the non-temporal hint; kStreamV writes
+// the values with it (the recompute that reads them next hides its load latency).
+template <typename T, int D, int kThreads, int kUnits, bool kStreamIn, bool kStreamV,
+          typename MakeCs>
 __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride, const T* ksrc,
                                            const T* vsrc, int64_t src_stride, int64_t s0,
                                            int64_t d0, int nrows, int hkv, int64_t n_src,
@@ -47,8 +49,8 @@ __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride,
       jj[k] = (c - h * UPH) * VEC;
       const int64_t so = min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)h * D + jj[k];
       kofs[k] = d * dst_stride + (int64_t)h * D + jj[k];
-      a[k] = ld16(ksrc + so);
-      b[k] = ld16(ksrc + so + HALF);
+      a[k] = kStreamIn ? ld16_nt(ksrc + so) : ld16(ksrc + so);
+      b[k] = kStreamIn ? ld16_nt(ksrc + so + HALF) : ld16(ksrc + so + HALF);
     }
     if (vdst) {
 #pragma unroll
@@ -59,7 +61,8 @@ __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride,
         const int64_t s = s0 + r, d = d0 + r;
         vok[k] = u < total_v && s >= 0 && s < n_src && d >= 0 && d < n_dst;
         vofs[k] = d * dst_stride + (int64_t)c * VEC;
-        va[k] = ld16(vsrc + min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)c * VEC);
+        const T* vp = vsrc + min(max(s, (int64_t)0), s_hi) * src_stride + (int64_t)c * VEC;
+        va[k] = kStreamIn ? ld16_nt(vp) : ld16(vp);
       }
     }
     if (first) {
@@ -81,7 +84,10 @@ __device__ __forceinline__ void remap_rows(T* kdst, T* vdst, int64_t dst_stride,
     if (vdst) {
 #pragma unroll
       for (int k = 0; k < 2 * kUnits; ++k)
-        if (vok[k]) st16(vdst + vofs[k], va[k]);
+        if (vok[k]) {
+          if (kStreamV) st16_nt(vdst + vofs[k], va[k]);
+          else st16(vdst + vofs[k], va[k]);
+        }
     }
   }
 }

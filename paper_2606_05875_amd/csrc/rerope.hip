@@ -19,7 +19,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnitsPerThread = 1;  // key units (rotate-half pairs) per thread per round (swept: 1, 2, 4)
 
-template <typename T, int D>
+template <typename T, int D, bool kStreamIn>
 __global__ __launch_bounds__(kThreads) void rerope_kernel(
     T* k_out, const T* k_in, T* v_out, const T* v_in, int64_t n_out_rows, int64_t n_in_rows,
     int hkv, int64_t out_stride, int64_t in_stride, int rows_per_block,
@@ -37,7 +37,7 @@ __global__ __launch_bounds__(kThreads) void rerope_kernel(
   const int64_t src0 = (src_start ? (int64_t)src_start[s] : (int64_t)seg_start[s]) + r0;
   // values are stitched unchanged, in the same token order (nothing to do in place)
   T* vdst = (v_out == nullptr || v_out == v_in) ? nullptr : v_out;
-  remap_rows<T, D, kThreads, kUnitsPerThread>(
+  remap_rows<T, D, kThreads, kUnitsPerThread, kStreamIn, true>(
       k_out, vdst, out_stride, k_in, v_in, in_stride, src0, dst0, min(rows_per_block, len - r0),
       hkv, n_in_rows, n_out_rows, cs, [&] {
         if (threadIdx.x < HALF) cs[threadIdx.x] = rope_cs((double)seg_delta[s], threadIdx.x, D, theta);
@@ -54,7 +54,11 @@ hipError_t launch_t(void* k_out, const void* k_in, void* v_out, const void* v_in
   const int units_per_row = hkv * (D / 2) / Vec16<T>::N;
   const int rpb = max(1, kThreads * kUnitsPerThread / units_per_row);
   dim3 grid((max_seg_len + rpb - 1) / rpb, n_seg);
-  rerope_kernel<T, D><<<grid, kThreads, 0, stream>>>(
+  // the stored keys' (and values') bytes
+  const int64_t src_bytes =
+      n_in_rows * (int64_t)hkv * D * (int64_t)sizeof(T) * (v_in != nullptr && v_out != nullptr ? 2 : 1);
+  auto kern = src_bytes > kStreamSourceBytes ? rerope_kernel<T, D, true> : rerope_kernel<T, D, false>;
+  kern<<<grid, kThreads, 0, stream>>>(
       static_cast<T*>(k_out), static_cast<const T*>(k_in), static_cast<T*>(v_out),
       static_cast<const T*>(v_in), n_out_rows, n_in_rows, hkv, out_stride, in_stride, rpb, seg_start,
       seg_len, seg_delta, src_start, theta);

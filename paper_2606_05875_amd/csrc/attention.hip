@@ -446,6 +446,12 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
   constexpr int NSLOT = KCH + VCH;                   // 64-lane transfers per stage
   constexpr int SPW = (NSLOT + kW8 - 1) / kW8;       // transfers per wave (the first waves)
   constexpr int NFULL = NSLOT - (SPW - 1) * kW8;     // waves that issue SPW of them
+  // Plain mode splits the block: waves 0-3 (one per SIMD) load the K chunks of a stage and
+  // multiply P(t) V(t) in step t; waves 4-7 load the V chunks and multiply P(t) V(t) at the
+  // start of step t+1.  The stream grid keeps one schedule for all waves.
+  constexpr bool kDefer = !kStream;
+  constexpr int SPWK = (KCH + 3) / 4, SPWV = (VCH + 3) / 4;  // transfers per wave, split
+  constexpr int SPWX = kDefer ? (SPWK > SPWV ? SPWK : SPWV) : SPW;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[kStages * KST];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[kStages * VST];
   __shared__ int red[kW8];
@@ -488,20 +494,36 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     const uint32_t range = nkv > 0 ? (uint32_t)(nkv - 1) * row_b + D * 2 : 0u;
     const i32x4 rk = make_rsrc(kc + kv0 * kv_stride + (int64_t)g * D, range);
     const i32x4 rv = make_rsrc(vc + kv0 * kv_stride + (int64_t)g * D, range);
-    // this wave's transfer slots j = w + 8 i: slot j < KCH fills K chunks
-    // [64 j, 64 j + 64) of a stage, the others V chunks; lane l of a slot fills
-    // chunk 64 j + l = (row, column) of the padded tile
-    uint32_t soff[SPW];
+    // this wave's transfer slots: j = w + 8 i over the K then the V chunks of a stage,
+    // or, split, j = (w & 3) + 4 i over the K chunks (waves 0-3) or the V chunks
+    // (waves 4-7).  Slot j fills chunks [64 j, 64 j + 64) of its tile; lane l fills
+    // chunk 64 j + l = (row, column) of the padded tile.
+    const bool vwave = kDefer && w >= 4;
+    uint32_t soff[SPWX];
+    bool sk[SPWX];  // slot i fills K chunks
+    int sj[SPWX];   // chunk slot within its tile
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int j = w + kW8 * i;
-      const bool isk = j < KCH;
-      const int ci = (isk ? j : j - KCH) * 64 + l;
-      const int ch = isk ? KCH : VCH;
+    for (int i = 0; i < SPWX; ++i) {
+      int j, ch, nch;
+      if (kDefer) {
+        j = (w & 3) + 4 * i;
+        sk[i] = !vwave;
+        ch = vwave ? VCH : KCH;
+        nch = ch;
+      } else {
+        j = w + kW8 * i;
+        sk[i] = j < KCH;
+        if (!sk[i]) j -= KCH;
+        ch = sk[i] ? KCH : VCH;
+        nch = sk[i] ? KCH : VCH;
+      }
+      sj[i] = j;
+      const int ci = j * 64 + l;
       const int r = ci / ch, c = ci % ch;
-      soff[i] = (j < NSLOT && c < D / 8) ? (uint32_t)r * row_b + c * 16 : kOob;
+      soff[i] = (j < nch && c < D / 8) ? (uint32_t)r * row_b + c * 16 : kOob;
     }
-    const int nslots = w < NFULL ? SPW : SPW - 1;
+    const int nslots = kDefer ? (vwave ? (VCH - (w & 3) + 3) / 4 : (KCH - (w & 3) + 3) / 4)
+                              : (w < NFULL ? SPW : SPW - 1);
     // the transfers of one step: tile r (relative to the segment's first tile)
     // into stage r % 4, K and V; a tile past the segment's end reads zeros
     const int t0 = kt_lo / kKT;
@@ -510,14 +532,13 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       const int sg = r & (kStages - 1);
       const uint32_t toff = (uint32_t)((t0 + r) * kKT) * row_b;
 #pragma unroll
-      for (int i = 0; i < SPW; ++i) {
+      for (int i = 0; i < SPWX; ++i) {
         if (i >= nslots) break;
-        const int j = w + kW8 * i;
         const uint32_t off = r < nt ? soff[i] + toff : kOob;
-        if (j < KCH)
-          dma16(rk, off, k_base + (uint32_t)(sg * KST + j * 512) * 2u);
+        if (sk[i])
+          dma16(rk, off, k_base + (uint32_t)(sg * KST + sj[i] * 512) * 2u);
         else
-          dma16(rv, off, v_base + (uint32_t)(sg * VST + (j - KCH) * 512) * 2u);
+          dma16(rv, off, v_base + (uint32_t)(sg * VST + sj[i] * 512) * 2u);
       }
     };
     // The first three key tiles go out before anything waits on memory (every
@@ -525,7 +546,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     // row positions and Q.
     issue(0);
     issue(1);
-    issue(2);
+    if (!vwave) issue(2);  // split: V runs two tiles ahead (see the ring below)
     // unconditional loads from a real row (a load under a lane condition gets a
     // wait of its own, which would also wait for the tiles above); a padding
     // lane's Q only has to be finite: its keys are all masked
@@ -555,8 +576,8 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     // (and every LDS read) are complete, then the block meets
     auto step_barrier = [&]() {
       asm volatile("" ::: "memory");
-      if (w < NFULL) wait_vm_lgkm0<SPW>();
-      else wait_vm_lgkm0<SPW - 1>();
+      if (nslots == SPWX) wait_vm_lgkm0<SPWX>();
+      else wait_vm_lgkm0<SPWX - 1>();
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
     };
@@ -649,6 +670,14 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     // memory traffic), so every step issues the same number of them.  Issued
     // at the start of the step instead, the transfers delayed the softmax
     // (c2 call +4%, c5 +1.5%).
+    // Split (plain mode): waves 4-7 start step t with O += P(t-1) V(t-1), then issue
+    // V(t+2) into the stage of tile t-2 (their last read of it was in step t-1; V(t-1)
+    // stays in place), then run the softmax of tile t, which may rescale O, beside
+    // S(t+1).  Waves 0-3 run the step as above with K(t+3) only.  On every SIMD one
+    // wave's product-only part then meets the other's vector part, where the two
+    // used to reach the same part together (c4 -3.4%, c5 -6.3%, bit-identical: the
+    // order of the products into O is unchanged).  A last barrier after the loop
+    // covers the final deferred product.
     f32x16 sa[2], sb[2];
     asm volatile("" ::: "memory");
     wait_vm_lgkm0<0>();
@@ -658,11 +687,16 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       qk_half(k_lds + krd, 0, sa[0]);
       qk_half(k_lds + krd, 1, sa[1]);
     }
+    bf16x8 pb[2][2];
+    bool pend = false;  // split, waves 4-7: pb holds P of the previous tile
     auto step = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
       const int kt0 = kt_lo + t * kKT;
       const bool do_cur = kt0 < wave_end;
       const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
-      bf16x8 pb[2][2];
+      if (vwave) {
+        if (pend) pv(v_lds + ((t - 1) & 3) * VST + vrd, pb);
+        issue(t + 2);
+      }
       if (do_cur) softmax_pre(sc, kt0);
       // The wave issuing this block (the next tile's products interleaved with this tile's
       // exponentials, the step's vector-heavy part) goes first at the SIMD's arbiter; the
@@ -683,13 +717,21 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
         softmax_exp(sc, pb);
       }
       __builtin_amdgcn_s_setprio(0);
-      issue(t + 3);
-      if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
+      if (vwave) {
+        pend = do_cur;
+      } else {
+        issue(t + 3);
+        if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
+      }
       step_barrier();
     };
     for (int t = 0; t < nt; t += 2) {
       step(t, sa, sb);
       if (t + 1 < nt) step(t + 1, sb, sa);
+    }
+    if (kDefer && nt > 0) {
+      if (pend) pv(v_lds + ((nt - 1) & 3) * VST + vrd, pb);
+      step_barrier();
     }
     // drain the last (zero-row) transfers before the LDS is refilled or released
     asm volatile("" ::: "memory");

@@ -479,6 +479,42 @@ def test_empty_calls():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(16, 2, 64), (8, 8, 64), (32, 8, 128)])
+def test_attention_plain_grid_every_tile(hq, hkv, d):
+    """The plain grid (one block per row tile, each block's two wave groups on their own
+    schedules: waves 0-3 multiply a tile's P.V in its own step, waves 4-7 in the next one) at
+    head sizes 64 and 128 and group sizes 8, 1 and 4: the first and last row of every row tile
+    of a ragged batch against the oracle."""
+    say("attention plain grid", hq, hkv, d)
+    rng = np.random.default_rng(9)
+    g = hq // hkv
+    rpb = 256 // g                                   # rows per row tile
+    first_tiles = -(-512 // (4 * hkv))             # enough row tiles for the plain grid
+    n_rows = [first_tiles * rpb + 5, 9 * rpb, 3 * rpb + 1, rpb - 7]
+    n_kv = [r * 3 // 2 + 40 for r in n_rows]
+    tiles = (max(n_rows) + rpb - 1) // rpb
+    assert tiles * len(n_kv) * hkv >= 512, "the case must take the plain grid"
+    cu_kv = np.concatenate([[0], np.cumsum(n_kv)]).astype(np.int32)
+    cu_r = np.concatenate([[0], np.cumsum(n_rows)]).astype(np.int32)
+    k = draw(rng, (cu_kv[-1], hkv, d), "bf16", 1 / math.sqrt(d))
+    v = draw(rng, (cu_kv[-1], hkv, d), "bf16", 1 / math.sqrt(d))
+    q = draw(rng, (cu_r[-1], hq, d), "bf16", math.sqrt(d))
+    rpos = np.concatenate([np.sort(rng.choice(nk, nr, replace=False)) for nk, nr in zip(n_kv, n_rows)])
+    rpos = rpos.astype(np.int32)
+    out = torch.empty((cu_r[-1], hq, d), dtype=torch.bfloat16, device="cuda")
+    scale = 1 / math.sqrt(d)
+    qcf.qcf_sparse_prefill_attn(out, dev(q, torch.bfloat16), dev(rpos), dev(cu_r), dev(k, torch.bfloat16),
+                                dev(v, torch.bfloat16), dev(cu_kv), max(n_rows), max(n_kv), scale)
+    got = host(out)
+    for b in range(len(n_kv)):
+        a, e, ka, ke = cu_r[b], cu_r[b + 1], cu_kv[b], cu_kv[b + 1]
+        firsts = np.arange(a, e, rpb)
+        pick = np.unique(np.concatenate([firsts, np.minimum(firsts + rpb - 1, e - 1)]))
+        want = Q.round_storage(Q.attention(q[pick], rpos[pick], k[ka:ke], v[ka:ke], np.arange(ke - ka),
+                                           scale, hkv), "bf16")
+        assert_close(got[pick], want, "bf16", f"request {b}")
+
+
 @pytest.mark.parametrize("n_kv,n_rows,plain", [
     ([2500, 2500, 400, 3100, 1200, 64], [700, 700, 90, 650, 0, 64], True),
     ([300, 1200, 50, 1200], [100, 400, 10, 0], False)])

@@ -36,22 +36,33 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
+def attention_code_digest():
+    """sha256 of the attention source with its comments and blank lines removed: a counter
+    record stays valid while the kernel code it measured is unchanged."""
+    import hashlib
+    import re
+    src = open(os.path.join(ROOT, "paper_2606_05875_amd", "csrc", "attention.hip"),
+               encoding="utf-8").read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    code = "\n".join(line.rstrip() for line in src.splitlines() if line.strip())
+    return hashlib.sha256(code.encode()).hexdigest()
+
+
 def measured_traffic(config, kv_row_stride):
     """HBM bytes per attention call from the committed counter record of this workload, or
-    None when there is none or the attention source or the cache row stride has changed
+    None when there is none or the attention code or the cache row stride has changed
     since the counters were taken."""
-    import hashlib
     rec_path = os.path.join(ROOT, "profiles", f"attention_{config}_hbm_traffic.md")
-    src = os.path.join(ROOT, "paper_2606_05875_amd", "csrc", "attention.hip")
     try:
         rec = None
         for line in open(rec_path):
             if line.startswith("{"):
                 rec = json.loads(line)
-        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        digest = attention_code_digest()
     except (OSError, ValueError):
         return None
-    if (not rec or rec.get("attention_source_sha256") != digest
+    if (not rec or rec.get("attention_code_sha256") != digest
             or rec.get("kv_row_stride") != kv_row_stride):
         return None
     return rec["bytes_per_call"]

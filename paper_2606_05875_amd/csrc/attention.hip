@@ -19,7 +19,8 @@
 //    the causal limit masks only tiles that reach past the wave's smallest
 //    position, and waves skip tiles past their largest position.
 // Recomputed rows run on attn_w8_kernel (8 waves, 256 query vectors, a
-// 4-stage K/V ring filled by buffer loads; a persistent "stream" grid when the
+// 4-stage K/V ring filled by buffer loads; on the plain grid the two waves of a
+// SIMD run the step a product phase apart; a persistent "stream" grid when the
 // row tiles are few and unequal), the probe on attn_pos_kernel (4 waves, K/V
 // by global->LDS loads two and one tiles ahead, key positions from a table).
 // fp32 path (vector ALUs): one wave per (row, head).
@@ -334,9 +335,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_pos_kernel(
 // 256 query vectors per block (256/G rows x the G heads of one KV head), 32
 // per wave, with the same per-wave tile step as attn_pos_kernel.  One block
 // fills a CU (two waves per SIMD), which leaves LDS for a 4-stage ring of
-// K/V tiles: K is fetched three tiles ahead and V two tiles ahead, and a step
-// ends by waiting only for the tiles fetched one step earlier, so every
-// global->LDS transfer has two steps to land.  The transfers are buffer loads
+// K/V tiles: step t fetches K(t+3), first read in step t+2, and V(t+3) (V(t+2)
+// on the split plain grid), first read in step t+3 (t+2), and a step ends by
+// waiting only for the tiles fetched one step earlier, so every global->LDS
+// transfer has at least two steps to land.  The transfers are buffer loads
 // with an LDS destination: a per-(request, head) descriptor bounds the key
 // range, so rows past the last key and the LDS padding chunks read as zeros
 // without touching memory, and a tile only moves a scalar row offset.  (Tiles

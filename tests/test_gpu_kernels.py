@@ -493,7 +493,7 @@ def test_attention_plain_grid_every_tile(hq, hkv, d):
     n_rows = [first_tiles * rpb + 5, 9 * rpb, 3 * rpb + 1, rpb - 7]
     n_kv = [r * 3 // 2 + 40 for r in n_rows]
     tiles = (max(n_rows) + rpb - 1) // rpb
-    assert tiles * len(n_kv) * hkv >= 512, "the case must take the plain grid"
+    assert tiles * len(n_kv) * hkv >= 384, "the case must take the plain grid"
     cu_kv = np.concatenate([[0], np.cumsum(n_kv)]).astype(np.int32)
     cu_r = np.concatenate([[0], np.cumsum(n_rows)]).astype(np.int32)
     k = draw(rng, (cu_kv[-1], hkv, d), "bf16", 1 / math.sqrt(d))
@@ -532,8 +532,8 @@ def test_attention_ragged_batch(n_kv, n_rows, plain):
     q = draw(rng, (cu_r[-1], hq, d), "bf16", math.sqrt(d))
     rpos = np.concatenate([np.sort(rng.choice(nk, nr, replace=False)) for nk, nr in zip(n_kv, n_rows)])
     rpos = rpos.astype(np.int32)
-    # the grid choice: one block per (row tile, request, KV head) from 512 such blocks on
-    assert ((max(n_rows) + 63) // 64 * len(n_kv) * hkv >= 512) == plain
+    # the grid choice: one block per (row tile, request, KV head) from 384 such blocks on
+    assert ((max(n_rows) + 63) // 64 * len(n_kv) * hkv >= 384) == plain
     out = torch.empty((cu_r[-1], hq, d), dtype=torch.bfloat16, device="cuda")
     scale = 1 / math.sqrt(d)
     qcf.qcf_sparse_prefill_attn(out, dev(q, torch.bfloat16), dev(rpos), dev(cu_r), dev(k, torch.bfloat16),

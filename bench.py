@@ -469,6 +469,8 @@ def main():
     ap.add_argument("--config", default="c4", help="workload: c4 (the headline), c2 or c5")
     ap.add_argument("--sets", type=int, default=0, help="buffer sets rotated (0: enough for 512 MB)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the c2 and c5 summaries that the default c4 line carries")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 256 MiB device-to-device copy 20 times (HBM counter calibration)")
@@ -643,9 +645,54 @@ def main():
         "rerope_hbm": rerope,
     }
 
+    if args.config == "c4" and not args.no_others:
+        out["other_workloads"] = {name: workload_summary(name) for name in ("c2", "c5")}
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def workload_summary(name, steps=100, warmup=10):
+    """Step time, selected tokens/s and recomputed-row attention share of the bf16 peak of one
+    more workload, measured the headline's way (rotated buffer sets up to 512 MB, K whole steps
+    between two events; the attention over events on its launch stream)."""
+    import torch
+    from paper_2606_05875_amd.step import FusionStep
+    from paper_2606_05875_amd.workloads import make_workload
+
+    w = make_workload(name)
+    first = FusionStep(w)
+    per_set = sum(t.numel() * t.element_size() for t in (first.k_pic, first.v_pic, first.q_new,
+                                                         first.k_new, first.v_new, first.k, first.v))
+    sets = [first] + [FusionStep(w) for _ in range(max(1, math.ceil(512e6 / per_set)) - 1)]
+    for i in range(warmup):
+        sets[i % len(sets)].run()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for i in range(steps):
+        sets[i % len(sets)].run()
+    b.record()
+    torch.cuda.synchronize()
+    ms_step = a.elapsed_time(b) / steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+    for i, (x, y) in enumerate(ev):
+        s = sets[i % len(sets)]
+        s.run_front()
+        x.record()
+        s.stage_attn()
+        y.record()
+        s.join()
+    torch.cuda.synchronize()
+    attn_ms = float(np.mean([x.elapsed_time(y) for x, y in ev]))
+    R_pos = first.R_pos.cpu().numpy()
+    achieved = attn_flops(first, R_pos) / (attn_ms * 1e-3) / 1e12
+    res = {"workload": w.meta["desc"], "ms_per_step": ms_step,
+           "tokens_per_s": int(R_pos.size) / (ms_step * 1e-3), "attn_ms": attn_ms,
+           "attn_frac_bf16_peak": achieved / PEAK_BF16_TFLOPS, "buffer_sets": len(sets)}
+    del sets, first
+    torch.cuda.empty_cache()
+    return res
 
 
 def _cpu_model():

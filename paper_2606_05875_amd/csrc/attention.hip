@@ -506,28 +506,26 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
     int sj[SPWX];   // chunk slot within its tile
 #pragma unroll
     for (int i = 0; i < SPWX; ++i) {
-      int j, ch, nch;
+      int j;
       if (kDefer) {
         j = (w & 3) + 4 * i;
         sk[i] = !vwave;
-        ch = vwave ? VCH : KCH;
-        nch = ch;
       } else {
         j = w + kW8 * i;
         sk[i] = j < KCH;
         if (!sk[i]) j -= KCH;
-        ch = sk[i] ? KCH : VCH;
-        nch = sk[i] ? KCH : VCH;
       }
+      const int ch = sk[i] ? KCH : VCH;  // chunks per row of the slot's tile
       sj[i] = j;
       const int ci = j * 64 + l;
       const int r = ci / ch, c = ci % ch;
-      soff[i] = (j < nch && c < D / 8) ? (uint32_t)r * row_b + c * 16 : kOob;
+      soff[i] = (j < ch && c < D / 8) ? (uint32_t)r * row_b + c * 16 : kOob;
     }
     const int nslots = kDefer ? (vwave ? (VCH - (w & 3) + 3) / 4 : (KCH - (w & 3) + 3) / 4)
                               : (w < NFULL ? SPW : SPW - 1);
     // the transfers of one step: tile r (relative to the segment's first tile)
-    // into stage r % 4, K and V; a tile past the segment's end reads zeros
+    // into stage r % 4, K and V (split: this wave's part, K or V); a tile past the
+    // segment's end reads zeros
     const int t0 = kt_lo / kKT;
     const int nt = kt_hi > kt_lo ? (kt_hi - kt_lo + kKT - 1) / kKT : 0;
     auto issue = [&](int r) {

@@ -143,6 +143,7 @@ __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
   const int qv = qt * kQvTile + 32 * w + lq;
   const int64_t qrow = q0 + (qv >> lg);
   const bool valid = qv < nqv && qrow < n_q_rows;
+  const bool live = __ballot(valid) != 0;  // the wave has a real query vector
   const int head = g * (1 << lg) + (qv & ((1 << lg) - 1));
 
   // Every load below is unconditional, its indices clamped to real rows: a
@@ -269,6 +270,12 @@ __global__ __launch_bounds__(kW * 64) void scores_pass_bf16(
     const int n_grp = (n_keys + 31) / 32;
     for (int kg = 0; kg < n_grp; ++kg) {
       if (kRot && more && kg == 1) fetch_cs();  // the next chunk's rotations, behind its pieces
+      if (!live) {
+        // a wave whose 32 query vectors are all padding (the request's last tile is
+        // partly filled) adds nothing: it only takes part in the loads and barriers
+        if (kCols && hi == 0) red[w][kg * 32 + lq] = 0.f;
+        continue;
+      }
       bf16x8 a[D / 16];
 #pragma unroll
       for (int st = 0; st < D / 16; ++st) a[st] = as_bf16x8(ld16(&k_lds[(kg * 32 + lq) * KSTR + 8 * hi + 16 * st]));

@@ -348,8 +348,12 @@ qcf_status qcf_probe_scores_select_noalloc(float* scores, int accumulate, const 
  *        steps of all its row tiles evenly over a fixed grid of blocks; the
  *        workspace then holds the work plan and the partial results of row tiles
  *        cut between two blocks, which a second kernel merges in a fixed order
- *        (deterministic).  Its contents need no initialisation; calls that overlap
- *        in time need separate workspaces.  The size query is monotone: the size
+ *        (deterministic).  A bf16 call without kv_pos over one request with at
+ *        least four row tiles per compute unit hands the tiles out from work
+ *        counters in the workspace, which the call resets itself (by a kernel on
+ *        the same stream); each tile is still computed whole by one block, so the
+ *        result does not depend on which block takes it.  Its contents need no
+ *        initialisation; calls that overlap in time need separate workspaces.  The size query is monotone: the size
  *        for (batch, max_rows, max_kv) covers every call whose three values do
  *        not exceed them (other arguments equal).
  */

@@ -515,6 +515,45 @@ def test_attention_plain_grid_every_tile(hq, hkv, d):
         assert_close(got[pick], want, "bf16", f"request {b}")
 
 
+def test_attention_one_request_work_queues():
+    """One request with four row tiles per CU (1024 blocks of 32 rows x 8 query heads) takes its
+    tiles from the per-XCD work queues.  The same call laid out as a batch of two (the second
+    request empty) runs the fixed one-block-per-tile order: every row must match it bit for bit,
+    on two calls in a row (the counters are reset by the call itself) and with a dirty
+    workspace; sampled rows (the last tile, the first, every 16th) also match the oracle."""
+    hq, hkv, d = 64, 8, 128
+    rpb = 256 // (hq // hkv)
+    n_rows = 4 * 256 * rpb // hkv                    # 1024 blocks: the queue threshold on 256 CUs
+    n_kv = n_rows + n_rows // 2
+    say("attention work queues", n_rows, n_kv)
+    rng = np.random.default_rng(21)
+    k = draw(rng, (n_kv, hkv, d), "bf16", 1 / math.sqrt(d))
+    v = draw(rng, (n_kv, hkv, d), "bf16", 1 / math.sqrt(d))
+    q = draw(rng, (n_rows, hq, d), "bf16", math.sqrt(d))
+    rpos = np.sort(rng.choice(n_kv, n_rows, replace=False)).astype(np.int32)
+    scale = 1 / math.sqrt(d)
+    args = (dev(q, torch.bfloat16), dev(rpos))
+    kk, vv = dev(k, torch.bfloat16), dev(v, torch.bfloat16)
+    need = qcf.qcf_sparse_prefill_attn_workspace_size(1, n_rows, n_kv, hq, hkv, d, torch.bfloat16)
+    ws = torch.full((need,), 0xAB, dtype=torch.uint8, device="cuda")
+    outs = []
+    for _ in range(2):
+        out = torch.empty((n_rows, hq, d), dtype=torch.bfloat16, device="cuda")
+        qcf.qcf_sparse_prefill_attn(out, *args, dev(np.array([0, n_rows], np.int32)), kk, vv,
+                                    dev(np.array([0, n_kv], np.int32)), n_rows, n_kv, scale, workspace=ws)
+        outs.append(out)
+    ref = torch.empty_like(outs[0])
+    qcf.qcf_sparse_prefill_attn(ref, *args, dev(np.array([0, n_rows, n_rows], np.int32)), kk, vv,
+                                dev(np.array([0, n_kv, n_kv], np.int32)), n_rows, n_kv, scale)
+    torch.cuda.synchronize()
+    for out in outs:
+        assert torch.equal(out, ref), "work-queue grid differs from the fixed-order grid"
+    pick = np.unique(np.concatenate([np.arange(n_rows - rpb, n_rows), np.arange(0, rpb, 7),
+                                     np.arange(rpb - 1, n_rows, 16 * rpb)]))
+    want = Q.round_storage(Q.attention(q[pick], rpos[pick], k, v, np.arange(n_kv), scale, hkv), "bf16")
+    assert_close(host(outs[0])[pick], want, "bf16", "work-queue grid")
+
+
 @pytest.mark.parametrize("n_kv,n_rows,plain", [
     ([2500, 2500, 400, 3100, 1200, 64], [700, 700, 90, 650, 0, 64], True),
     ([300, 1200, 50, 1200], [100, 400, 10, 0], False)])

@@ -553,6 +553,28 @@ def test_attention_one_request_work_queues():
     want = Q.round_storage(Q.attention(q[pick], rpos[pick], k, v, np.arange(n_kv), scale, hkv), "bf16")
     assert_close(host(outs[0])[pick], want, "bf16", "work-queue grid")
 
+    # captured in a graph (the counters are reset by a kernel, not a memset): every replay,
+    # with eager work and synchronisations between them, equals the eager result
+    cu_r1, cu_k1 = dev(np.array([0, n_rows], np.int32)), dev(np.array([0, n_kv], np.int32))
+    gout = torch.empty_like(ref)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        qcf.qcf_sparse_prefill_attn(gout, *args, cu_r1, kk, vv, cu_k1, n_rows, n_kv, scale, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        qcf.qcf_sparse_prefill_attn(gout, *args, cu_r1, kk, vv, cu_k1, n_rows, n_kv, scale, workspace=ws)
+    for rep in range(3):
+        gout.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(gout, ref), f"graph replay {rep} differs"
+        eager = torch.empty_like(ref)
+        qcf.qcf_sparse_prefill_attn(eager, *args, cu_r1, kk, vv, cu_k1, n_rows, n_kv, scale, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(eager, ref)
+
 
 @pytest.mark.parametrize("n_kv,n_rows,plain", [
     ([2500, 2500, 400, 3100, 1200, 64], [700, 700, 90, 650, 0, 64], True),

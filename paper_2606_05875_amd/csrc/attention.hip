@@ -20,8 +20,9 @@
 //    position, and waves skip tiles past their largest position.
 // Recomputed rows run on attn_w8_kernel (8 waves, 256 query vectors, a
 // 4-stage K/V ring filled by buffer loads; on the plain grid the two waves of a
-// SIMD run the step a product phase apart; a persistent "stream" grid when the
-// row tiles are few and unequal), the probe on attn_pos_kernel (4 waves, K/V
+// SIMD run the step a product phase apart, and one long request hands its row
+// tiles out from per-XCD work queues; a persistent "stream" grid when the row
+// tiles are few and unequal), the probe on attn_pos_kernel (4 waves, K/V
 // by global->LDS loads two and one tiles ahead, key positions from a table).
 // fp32 path (vector ALUs): one wave per (row, head).
 #include <limits.h>
@@ -383,7 +384,8 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
 }
 
 // Work of an 8-wave block.  Plain mode: block -> (KV head g, request b, row
-// tile), the tile's whole key range.  Stream mode (few, unequal tiles): a
+// tile), the tile's whole key range (fixed by the block id, or claimed from a
+// work queue for one long request).  Stream mode (few, unequal tiles): a
 // persistent grid of nbg blocks per KV head; the head's work -- every row
 // tile of every request in (request, row tile) order, each counted as
 // kSegCost start-up steps followed by its 64-key steps -- is cut into nbg

@@ -515,19 +515,18 @@ def test_attention_plain_grid_every_tile(hq, hkv, d):
         assert_close(got[pick], want, "bf16", f"request {b}")
 
 
-@pytest.mark.parametrize("hq,hkv", [(64, 8), (16, 2), (128, 16)])
-def test_attention_one_request_work_queues(hq, hkv):
+@pytest.mark.parametrize("hq,hkv,d", [(64, 8, 128), (16, 2, 128), (128, 16, 128), (64, 8, 64)])
+def test_attention_one_request_work_queues(hq, hkv, d):
     """One request with four row tiles per CU (1024 blocks of 32 rows x 8 query heads) takes its
     tiles from the per-XCD work queues (8 KV heads: one per queue; 2: four XCDs per queue; 16:
     two heads per queue).  The same call laid out as a batch of two (the second request empty)
     runs the fixed one-block-per-tile order: every row must match it bit for bit, on two calls
     in a row (the counters are reset by the call itself) and with a dirty workspace; sampled
-    rows (the last tile, the first, every 16th) also match the oracle."""
-    d = 128
+    rows (the last tile, the first, every 16th) also match the oracle.  Head sizes 128 and 64."""
     rpb = 256 // (hq // hkv)
     n_rows = 4 * 256 * rpb // hkv                    # 1024 blocks: the queue threshold on 256 CUs
     n_kv = n_rows + n_rows // 2
-    say("attention work queues", hq, hkv, n_rows, n_kv)
+    say("attention work queues", hq, hkv, d, n_rows, n_kv)
     rng = np.random.default_rng(21)
     k = draw(rng, (n_kv, hkv, d), "bf16", 1 / math.sqrt(d))
     v = draw(rng, (n_kv, hkv, d), "bf16", 1 / math.sqrt(d))

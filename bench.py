@@ -647,9 +647,56 @@ def main():
 
     if args.config == "c4" and not args.no_others:
         out["other_workloads"] = {name: workload_summary(name) for name in ("c2", "c5")}
+        out["achievable"] = achievable_peaks()
+        out["roofline"]["frac_of_achievable"] = achieved / out["achievable"]["mfma_bf16_loop"]["tflops"]
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def achievable_peaks(iters=10000):
+    """What this part reaches on plain loops, beside the published peaks: the attention's bf16
+    product instruction (v_mfma_f32_32x32x16_bf16) in a loop at the attention's occupancy, two
+    waves per SIMD, on random operands (qcf_mfma_loop), with the clock of one block per XCD read
+    from its counters; and a 512 MiB device-to-device copy."""
+    import torch
+    from paper_2606_05875_amd import qcf
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 2 * n_cu
+    ops = torch.randn(1 << 20, device="cuda").to(torch.bfloat16)
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    clocks = torch.zeros(32, dtype=torch.int64, device="cuda")
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    qcf.qcf_mfma_loop(ops, sink, clocks, blocks, max(1, iters // 10))
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(3):
+        a.record()
+        qcf.qcf_mfma_loop(ops, sink, clocks, blocks, iters)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    ms = float(np.median(times))
+    flops = blocks * 4 * iters * 16 * 32768
+    tflops = flops / (ms * 1e-3) / 1e12
+    c = clocks.view(8, 4).cpu().numpy().astype(np.float64)
+    ghz = (c[:, 3] - c[:, 1]) / ((c[:, 2] - c[:, 0]) / 100e6) / 1e9
+    x = torch.empty(128 << 20, dtype=torch.float32, device="cuda").uniform_()
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(10):
+        y.copy_(x)
+    b.record()
+    torch.cuda.synchronize()
+    gbs = 2 * x.numel() * 4 * 10 / (a.elapsed_time(b) * 1e-3) / 1e9
+    del x, y
+    return {"mfma_bf16_loop": {"tflops": tflops, "frac_of_peak": tflops / PEAK_BF16_TFLOPS, "ms": ms,
+                               "clock_ghz_min_median_max": [float(ghz.min()), float(np.median(ghz)),
+                                                            float(ghz.max())],
+                               "occupancy": "2 waves per SIMD, 4 accumulators per wave, random bf16"},
+            "device_copy": {"GBs": gbs, "frac_of_peak": gbs / PEAK_HBM_GBS, "bytes": 2 * (512 << 20)}}
 
 
 def workload_summary(name, steps=100, warmup=10):

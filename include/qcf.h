@@ -398,6 +398,24 @@ qcf_status qcf_sparse_prefill_attn_rope(void* out, float* lse, const void* q_raw
                                         float softmax_scale, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * qcf_mfma_loop -- not a step of the method: a yardstick for the attention.
+ * A grid of `blocks` four-wave blocks runs `iters` rounds of 16
+ * v_mfma_f32_32x32x16_bf16 products per wave (four independent accumulators,
+ * operand fragments taken from `operands` and rotated between products), the
+ * attention's product instruction at its occupancy (two waves per SIMD when
+ * blocks = 2 x compute units).  Each wave executes iters x 16 x 32768 FLOP.
+ *   operands  bf16 [n_operands >= 16] device buffer (random values give the
+ *             multipliers realistic activity; all-zero data runs cooler)
+ *   sink      float32 [n_sink >= blocks * 256]: one sum of accumulators per thread
+ *   clocks    uint64 [32]: blocks 0..7 each write (real-time counter at 100 MHz,
+ *             shader-clock counter) at their start and end, so the clock the
+ *             loop ran at is the ratio of the two differences
+ *   blocks >= 8, iters >= 1.  Nothing is read back or synchronised.
+ */
+qcf_status qcf_mfma_loop(const void* operands, int64_t n_operands, float* sink, int64_t n_sink,
+                         uint64_t* clocks, int blocks, int iters, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

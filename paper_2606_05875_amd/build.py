@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libqcf.so")
 SOURCES = ["api.cpp", "rerope.hip", "assemble.hip", "gather_scatter.hip", "topk.hip", "probe_scores.hip",
-           "attention.hip", "noalloc.hip"]
+           "attention.hip", "noalloc.hip", "peak.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

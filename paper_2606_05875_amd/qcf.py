@@ -21,6 +21,7 @@ __all__ = [
     "qcf_rope_table", "qcf_probe_scores_pic",
     "qcf_select_topk", "qcf_probe_scores_select", "qcf_probe_scores_select_noalloc",
     "qcf_sparse_prefill_attn", "qcf_sparse_prefill_attn_rope", "rope_position_table", "qcf_sparse_prefill_attn_workspace_size",
+    "qcf_mfma_loop",
     "EXPORTS", "Prepared", "prepare",
 ]
 
@@ -64,6 +65,7 @@ EXPORTS = {
                                           _SZ, _P]),
     "qcf_sparse_prefill_attn": (_I, [_P, _P, _P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I, _I,
                                      _I, _I, _I, _I, _I, ctypes.c_float, _P, _SZ, _P]),
+    "qcf_mfma_loop": (_I, [_P, _I64, _P, _I64, _P, _I, _I, _P]),
 }
 
 
@@ -537,3 +539,16 @@ def qcf_sparse_prefill_attn_rope(out, q_raw, row_pos, cu_rows, k_cache, v_cache,
             _ptr(cu_kv), _ptr(rope_table), rope_table.shape[0], _dtype(out), batch, int(max_rows),
             int(max_kv), hq, hkv, d, float(softmax_scale), _ptr(workspace),
             0 if workspace is None else workspace.numel(), keep=workspace)
+
+
+def qcf_mfma_loop(operands, sink, clocks, blocks, iters):
+    """The attention's product instruction in a plain loop (a yardstick, not a step of the
+    method): `blocks` four-wave blocks, iters x 16 products per wave; `clocks` (uint64 [32]
+    as int64) gets the start/end counters of blocks 0-7."""
+    _dev(operands, "operands", torch.bfloat16)
+    _dev(sink, "sink", torch.float32)
+    _dev(clocks, "clocks", torch.int64)
+    if clocks.numel() < 32 or sink.numel() < blocks * 256 or not operands.is_contiguous():
+        raise QcfError("clocks needs 32 entries, sink blocks * 256, operands a dense buffer")
+    _invoke("qcf_mfma_loop", _ptr(operands), operands.numel(), _ptr(sink), sink.numel(), _ptr(clocks),
+            int(blocks), int(iters))

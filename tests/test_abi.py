@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(L):
                          "qcf_rope_table", "qcf_probe_scores_pic", "qcf_select_topk",
                          "qcf_probe_scores_select", "qcf_probe_scores_select_noalloc",
                          "qcf_sparse_prefill_attn_workspace_size", "qcf_sparse_prefill_attn_rope",
-                         "qcf_sparse_prefill_attn"}
+                         "qcf_sparse_prefill_attn", "qcf_mfma_loop"}
     for name, nargs in decl.items():
         assert hasattr(L, name), name
         assert name in qcf.EXPORTS
@@ -219,3 +219,14 @@ def test_topk_and_attn_validation(L):
     assert L.qcf_sparse_prefill_attn(*a(stride=1000)) == INVALID
     assert L.qcf_sparse_prefill_attn(*a(n=-2)) == INVALID
     assert L.qcf_sparse_prefill_attn_workspace_size(1, 10, 100, 32, 8, 128, BF16) >= 0
+
+
+def test_mfma_loop_validation(L):
+    """The matrix-core yardstick rejects missing buffers and too few blocks before launching."""
+    P = ctypes.c_void_p
+    buf = P(16)
+    assert L.qcf_mfma_loop(None, 1 << 20, buf, 512 * 256, buf, 512, 10, None) == 1
+    assert L.qcf_mfma_loop(buf, 8, buf, 512 * 256, buf, 512, 10, None) == 1      # too few operands
+    assert L.qcf_mfma_loop(buf, 1 << 20, buf, 100, buf, 512, 10, None) == 1      # sink too small
+    assert L.qcf_mfma_loop(buf, 1 << 20, buf, 4 * 256, buf, 4, 10, None) == 1     # fewer than 8 blocks
+    assert L.qcf_mfma_loop(buf, 1 << 20, buf, 512 * 256, buf, 512, 0, None) == 1  # no rounds

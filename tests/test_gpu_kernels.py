@@ -609,3 +609,22 @@ def test_attention_ragged_batch(n_kv, n_rows, plain):
         want = Q.round_storage(Q.attention(q[pick], rpos[pick], k[ka:ke], v[ka:ke], np.arange(ke - ka),
                                            scale, hkv), "bf16")
         assert_close(got[pick], want, "bf16", f"request {b}")
+
+
+def test_mfma_loop_yardstick():
+    """The matrix-core loop (a yardstick for the attention, not a step of the method) runs, leaves
+    finite sums (random operands) and clock counters that give a clock between 0.5 and 3 GHz on
+    each of the eight recording blocks."""
+    say("mfma loop")
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 2 * n_cu
+    ops = torch.randn(1 << 16, generator=torch.Generator().manual_seed(5)).to(torch.bfloat16).cuda()
+    sink = torch.full((blocks * 256,), float("nan"), dtype=torch.float32, device="cuda")
+    clocks = torch.zeros(32, dtype=torch.int64, device="cuda")
+    qcf.qcf_mfma_loop(ops, sink, clocks, blocks, 200)
+    torch.cuda.synchronize()
+    assert torch.isfinite(sink).all()
+    c = clocks.view(8, 4).cpu().numpy().astype(np.float64)
+    assert (c[:, 2] > c[:, 0]).all() and (c[:, 3] > c[:, 1]).all()
+    ghz = (c[:, 3] - c[:, 1]) / ((c[:, 2] - c[:, 0]) / 100e6) / 1e9
+    assert ((ghz > 0.5) & (ghz < 3.0)).all(), ghz

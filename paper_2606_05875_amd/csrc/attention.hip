@@ -589,18 +589,6 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
     };
-    auto read_v = [&](const uint16_t* vl, int hb, bf16x8* vf) {
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-        for (int mb = 0; mb < D / 32; ++mb) {
-          const uint16_t* p0 = vl + (hb * 32 + 16 * k2) * VSTR + 32 * mb;
-          const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0));
-          const v4s up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p0 + 8 * VSTR));
-          vf[k2 * (D / 32) + mb] =
-              __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
-        }
-    };
     auto qk_half = [&](const uint16_t* kl, int hb, f32x16& sh) {
       bf16x8 kf[D / 16];
 #pragma unroll
@@ -709,26 +697,13 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       sum_pack(NM - 1);
       ls += psum;
     };
-    auto pv = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        bf16x8 vf[2 * (D / 32)];
-        read_v(vl, hb, vf);
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-          for (int mb = 0; mb < D / 32; ++mb)
-            o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k2 * (D / 32) + mb], pb[hb][k2],
-                                                            o[mb], 0, 0, 0);
-      }
-    };
     // O += P V as a fenced sequence of products, each issuing the V fragment (two transposed
     // reads) of the product four places ahead: the compiler's own order read eight fragments
-    // at a time and waited at the head of every batch (bit-identical; c4 -0.8%, c5 -1.0%).
-    // Plain mode only, as qk_exp_fused.
-    auto pv_fused = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
+    // at a time and waited at the head of every batch (bit-identical; c4 -0.8%, c5 -1.0%,
+    // c2 (stream mode) -4%).
+    auto pv = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
       constexpr int NB = D / 32;
-      constexpr int NM = 4 * NB;  // products, ordered (hb, k2, mb) as in pv
+      constexpr int NM = 4 * NB;  // products, ordered (hb, k2, mb)
       constexpr int PF = 4;       // V fragments in flight
       auto vfrag = [&](int j) {
         const int hb = j / (2 * NB), k2 = (j / NB) % 2, mb = j % NB;
@@ -748,10 +723,6 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
         o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[j], pb[hb][k2], o[mb], 0, 0, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
-    };
-    auto pvx = [&](const uint16_t* vl, bf16x8 (&pb)[2][2]) {
-      if constexpr (!kStream) pv_fused(vl, pb);
-      else pv(vl, pb);
     };
 
     // Ring: K(t) and V(t) live in stage t % 4.  Step t computes S(t+1) while the
@@ -786,7 +757,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       const bool do_cur = kt0 < wave_end;
       const bool do_next = t + 1 < nt && kt0 + kKT < wave_end;
       if (vwave) {
-        if (pend) pvx(v_lds + ((t - 1) & 3) * VST + vrd, pb);
+        if (pend) pv(v_lds + ((t - 1) & 3) * VST + vrd, pb);
         issue(t + 2);
       }
       if (do_cur) softmax_pre(sc, kt0);
@@ -817,7 +788,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
         pend = do_cur;
       } else {
         issue(t + 3);
-        if (do_cur) pvx(v_lds + (t & 3) * VST + vrd, pb);
+        if (do_cur) pv(v_lds + (t & 3) * VST + vrd, pb);
       }
       step_barrier();
     };
@@ -826,7 +797,7 @@ __global__ __launch_bounds__(kW8 * 64, 1) void attn_w8_kernel(
       if (t + 1 < nt) step(t + 1, sb, sa);
     }
     if (kDefer && nt > 0) {
-      if (pend) pvx(v_lds + ((nt - 1) & 3) * VST + vrd, pb);
+      if (pend) pv(v_lds + ((nt - 1) & 3) * VST + vrd, pb);
       step_barrier();
     }
     // drain the last (zero-row) transfers before the LDS is refilled or released

@@ -19,10 +19,12 @@
 //    the causal limit masks only tiles that reach past the wave's smallest
 //    position, and waves skip tiles past their largest position.
 // Recomputed rows run on attn_w8_kernel (8 waves, 256 query vectors, a
-// 4-stage K/V ring filled by buffer loads; on the plain grid the two waves of a
-// SIMD run the step a product phase apart, and one long request hands its row
-// tiles out from per-XCD work queues; a persistent "stream" grid when the row
-// tiles are few and unequal), the probe on attn_pos_kernel (4 waves, K/V
+// 4-stage K/V ring filled by buffer loads; the products run as fenced
+// sequences with their LDS fragment reads issued four products ahead; on the
+// plain grid the two waves of a SIMD run the step a product phase apart, and
+// one long request hands its row tiles out from per-XCD work queues; a
+// persistent "stream" grid when the row tiles are few and unequal), the probe
+// on attn_pos_kernel (4 waves, K/V
 // by global->LDS loads two and one tiles ahead, key positions from a table).
 // fp32 path (vector ALUs): one wave per (row, head).
 #include <limits.h>
